@@ -1,0 +1,185 @@
+"""FlashNorm CPU oracle (fp64) -- TEST INFRASTRUCTURE ONLY.
+
+Plain, slow, obviously correct reference for the norm-then-project hot path of
+"FlashNorm: Fast Normalization for Transformers" (arXiv 2407.09577), written in C
+(``flashnorm_oracle.c``) and driven from here through ctypes.  Only ``tests/``,
+``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import
+this package.  It shares no code with the GPU library in
+``paper_2407_09577_amd/``: neither imports, includes or links the other.
+
+Every function takes the values the GPU receives (bf16 or fp32 tensors, fp32
+``g``/``beta``, the fp32 ``eps``) and computes in fp64.  ``rows`` selects a subset
+of input rows (sampled parity at full workload sizes); the result has one row
+per selected input row.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "flashnorm_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+STORAGE_F32 = 0
+STORAGE_BF16 = 1
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no fast-math, no FP contraction)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + f".tmp{os.getpid()}"
+        cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-shared", "-fPIC",
+               "-fvisibility=hidden", _SRC, "-o", tmp, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    I = ctypes.c_int64
+    D = ctypes.c_double
+    lib.fn_oracle_rms.argtypes = [P, I, D]
+    lib.fn_oracle_rms.restype = D
+    for name in ("fn_oracle_rmsnorm_linear", "fn_oracle_weightless", "fn_oracle_deferred"):
+        getattr(lib, name).argtypes = [P, I, I, P, P, I, D, P, P, I, P]
+        getattr(lib, name).restype = None
+    lib.fn_oracle_rmsnorm_swiglu.argtypes = [P, I, I, P, P, I, D, P, I, P]
+    lib.fn_oracle_rmsnorm_swiglu.restype = None
+    for name in ("fn_oracle_layernorm_linear", "fn_oracle_layernorm_linear_deferred"):
+        getattr(lib, name).argtypes = [P, I, I, P, P, P, I, D, P, P, I, P]
+        getattr(lib, name).restype = None
+    lib.fn_oracle_round_bf16.argtypes = [D]
+    lib.fn_oracle_round_bf16.restype = D
+    lib.fn_oracle_round_f32.argtypes = [D]
+    lib.fn_oracle_round_f32.restype = D
+    lib.fn_oracle_fold.argtypes = [P, P, P, I, I, ctypes.c_int, P, P, P]
+    lib.fn_oracle_fold.restype = None
+    _lib = lib
+    return lib
+
+
+def _f64(x) -> np.ndarray:
+    """fp64 C-contiguous copy of a numpy array or a (CPU) torch tensor of any float dtype."""
+    if x is None:
+        return None
+    if hasattr(x, "detach"):  # torch tensor: bf16 has no numpy dtype, go through fp32 (exact)
+        import torch
+        x = x.detach().to("cpu", torch.float64).numpy()
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _ptr(x):
+    return None if x is None else x.ctypes.data_as(ctypes.c_void_p)
+
+
+def _rows(rows, M):
+    if rows is None:
+        return None, M
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+    if r.ndim != 1 or (r.size and (r.min() < 0 or r.max() >= M)):
+        raise ValueError("rows must be a 1-D list of indices into a")
+    return r, int(r.size)
+
+
+def _eps(eps) -> float:
+    # the kernels receive eps as an fp32 scalar; the oracle uses that exact value
+    return float(np.float32(eps))
+
+
+def rms(a, eps: float = 0.0) -> float:
+    """RMSe(a) = sqrt(eps + mean(a^2)) of one row (App. "RMS with epsilon")."""
+    a = _f64(a).ravel()
+    return _load().fn_oracle_rms(_ptr(a), a.size, float(eps))
+
+
+def _linear_like(fn, a, g, W, eps, bias, rows):
+    a, g, W, bias = _f64(a), _f64(g), _f64(W), _f64(bias)
+    M, K = a.shape
+    K2, N = W.shape
+    if K2 != K or g.shape != (K,) or (bias is not None and bias.shape != (N,)):
+        raise ValueError("shape mismatch")
+    r, nr = _rows(rows, M)
+    y = np.empty((nr, N), dtype=np.float64)
+    fn(_ptr(a), M, K, _ptr(g), _ptr(W), N, _eps(eps), _ptr(bias), _ptr(r), nr, _ptr(y))
+    return y
+
+
+def rmsnorm_linear(a, g, W, eps, bias=None, rows=None) -> np.ndarray:
+    """Standard form (a): y = RMSNorm(a; g) W (+ c after the normalisation), Sec. 3.1."""
+    return _linear_like(_load().fn_oracle_rmsnorm_linear, a, g, W, eps, bias, rows)
+
+
+def weightless(a, g, W, eps, bias=None, rows=None) -> np.ndarray:
+    """Form (b): y = (a / RMS(a)) W* with W* = diag(g) W in fp64 (Prop. 1). Self-check."""
+    return _linear_like(_load().fn_oracle_weightless, a, g, W, eps, bias, rows)
+
+
+def deferred(a, g, W, eps, bias=None, rows=None) -> np.ndarray:
+    """Form (c): y = (a W*) / RMS(a) (Prop. 2). Self-check."""
+    return _linear_like(_load().fn_oracle_deferred, a, g, W, eps, bias, rows)
+
+
+def rmsnorm_swiglu(a, g, Wgu, eps, rows=None) -> np.ndarray:
+    """out = silu(x Wg) * (x Wu), x = RMSNorm(a; g), Wgu = [Wg | Wu] of shape [K, 2F] (Sec. 4.1)."""
+    a, g, Wgu = _f64(a), _f64(g), _f64(Wgu)
+    M, K = a.shape
+    K2, N2 = Wgu.shape
+    if K2 != K or N2 % 2 or g.shape != (K,):
+        raise ValueError("shape mismatch")
+    F = N2 // 2
+    r, nr = _rows(rows, M)
+    out = np.empty((nr, F), dtype=np.float64)
+    _load().fn_oracle_rmsnorm_swiglu(_ptr(a), M, K, _ptr(g), _ptr(Wgu), F, _eps(eps), _ptr(r), nr, _ptr(out))
+    return out
+
+
+def _ln_like(fn, a, g, beta, W, eps, bias, rows):
+    a, g, beta, W, bias = _f64(a), _f64(g), _f64(beta), _f64(W), _f64(bias)
+    M, K = a.shape
+    K2, N = W.shape
+    if K2 != K or g.shape != (K,) or beta.shape != (K,):
+        raise ValueError("shape mismatch")
+    r, nr = _rows(rows, M)
+    y = np.empty((nr, N), dtype=np.float64)
+    fn(_ptr(a), M, K, _ptr(g), _ptr(beta), _ptr(W), N, _eps(eps), _ptr(bias), _ptr(r), nr, _ptr(y))
+    return y
+
+
+def layernorm_linear(a, g, beta, W, eps, bias=None, rows=None) -> np.ndarray:
+    """Standard LayerNorm -> linear: x = (a - mu)/sqrt(var + eps) * g + beta, y = x W (+ c)."""
+    return _ln_like(_load().fn_oracle_layernorm_linear, a, g, beta, W, eps, bias, rows)
+
+
+def layernorm_linear_deferred(a, g, beta, W, eps, bias=None, rows=None) -> np.ndarray:
+    """Deferred LayerNorm -> linear: ((a W*) - mu colsum(W*)) / sigma + beta W (+ c). Self-check."""
+    return _ln_like(_load().fn_oracle_layernorm_linear_deferred, a, g, beta, W, eps, bias, rows)
+
+
+def round_bf16(x) -> np.ndarray:
+    """Round fp64 values to the nearest bfloat16 value (ties to even), returned as fp64."""
+    f = _load().fn_oracle_round_bf16
+    x = np.asarray(x, dtype=np.float64)
+    return np.vectorize(f, otypes=[np.float64])(x) if x.ndim else np.float64(f(float(x)))
+
+
+def fold(W, g, beta=None, storage: int = STORAGE_BF16):
+    """Expected fold (Prop. 1, Sec. 3.4): stored W* = round(g_k W[k,n]) in the storage type,
+    colsum of the stored W*, and c* = beta W with the unfolded W (None without beta)."""
+    W, g, beta = _f64(W), _f64(g), _f64(beta)
+    K, N = W.shape
+    Ws = np.empty((K, N), dtype=np.float64)
+    colsum = np.empty(N, dtype=np.float64)
+    cstar = np.empty(N, dtype=np.float64) if beta is not None else None
+    _load().fn_oracle_fold(_ptr(W), _ptr(g), _ptr(beta), K, N, int(storage), _ptr(Ws), _ptr(colsum), _ptr(cstar))
+    return Ws, colsum, cstar

@@ -1,0 +1,381 @@
+"""Pins of the fp64 CPU oracle against what the paper and the mathematics fix.
+
+Nothing here compares the oracle with itself alone: every function is checked
+against exact rational worked examples derived from the paper's definitions
+(tests/golden), closed forms, textbook library routines it reduces to
+(torch's rms_norm / layer_norm / silu in fp64), or invariants the paper states.
+Each group is chosen so that a plausible slip in the oracle (a dropped 1/K, eps
+outside the root, a wrong index into g, a transposed W, the bias added before
+the scaling, a wrong sign) fails at least one test.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2407_09577_amd import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _frac(s):
+    return Fraction(s)
+
+
+def _read_fixture(name):
+    rows = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, *vals = line.split()
+            rows.setdefault(key, []).append(vals)
+    return rows
+
+
+def _rand_case(M, K, N, seed, neg_g=False):
+    rng = np.random.default_rng(seed)
+    a = rng.standard_normal((M, K))
+    g = rng.uniform(0.5, 1.5, K)
+    if neg_g:
+        g *= np.where(rng.random(K) < 0.3, -1.0, 1.0)
+    W = rng.standard_normal((K, N)) / math.sqrt(K)
+    return a, g, W
+
+
+def _rel(x, ref):
+    return np.max(np.abs(x - ref)) / max(np.max(np.abs(ref)), 1e-300)
+
+
+# ---------------------------------------------------------------- worked examples
+def test_rmsnorm_linear_exact_worked_example():
+    fx = _read_fixture("rmsnorm_linear_worked_example.txt")
+    a = np.array([[float(_frac(v)) for v in fx["a"][0]]])
+    g = np.array([float(_frac(v)) for v in fx["g"][0]])
+    W = np.array([[float(_frac(v)) for v in r] for r in fx["W"]])
+    c = np.array([float(_frac(v)) for v in fx["c"][0]])
+    for case in fx["case"]:
+        eps = float(_frac(case[0]))
+        bar = case.index("|")
+        want = np.array([float(_frac(v)) for v in case[1:bar]])
+        want_c = np.array([float(_frac(v)) for v in case[bar + 1:]])
+        y = oracle.rmsnorm_linear(a, g, W, eps)
+        np.testing.assert_allclose(y[0], want, rtol=1e-15, atol=1e-15)
+        yc = oracle.rmsnorm_linear(a, g, W, eps, bias=c)
+        np.testing.assert_allclose(yc[0], want_c, rtol=1e-15, atol=1e-15)
+        # the weightless and deferred forms reach the same exact values (Props. 1-2)
+        np.testing.assert_allclose(oracle.weightless(a, g, W, eps, bias=c)[0], want_c, rtol=1e-15, atol=1e-15)
+        np.testing.assert_allclose(oracle.deferred(a, g, W, eps, bias=c)[0], want_c, rtol=1e-15, atol=1e-15)
+
+
+def test_layernorm_linear_exact_worked_example():
+    fx = _read_fixture("layernorm_linear_worked_example.txt")
+    a = np.array([[float(_frac(v)) for v in fx["a"][0]]])
+    g = np.array([float(_frac(v)) for v in fx["g"][0]])
+    beta = np.array([float(_frac(v)) for v in fx["beta"][0]])
+    W = np.array([[float(_frac(v)) for v in r] for r in fx["W"]])
+    eps = float(_frac(fx["eps"][0][0]))
+    want = np.array([float(_frac(v)) for v in fx["y"][0]])
+    cstar = np.array([float(_frac(v)) for v in fx["cstar"][0]])
+    np.testing.assert_allclose(oracle.layernorm_linear(a, g, beta, W, eps)[0], want, rtol=1e-15, atol=1e-15)
+    np.testing.assert_allclose(oracle.layernorm_linear_deferred(a, g, beta, W, eps)[0], want, rtol=1e-15, atol=1e-15)
+    _, _, cs = oracle.fold(W, g, beta, storage=oracle.STORAGE_F32)
+    np.testing.assert_allclose(cs, cstar, rtol=0, atol=0)
+
+
+# ---------------------------------------------------------------- closed forms
+@pytest.mark.parametrize("c", [-3.0, 0.5, 7.0])
+@pytest.mark.parametrize("K", [1, 4, 576])
+def test_rms_of_constant_vector(c, K):
+    # RMS(c * 1_K) = |c| (scale invariance of RMS, Sec. 3.3); with eps: sqrt(c^2 + eps)
+    a = np.full(K, c)
+    assert oracle.rms(a, 0.0) == pytest.approx(abs(c), rel=1e-15)
+    assert oracle.rms(a, 0.25) == pytest.approx(math.sqrt(c * c + 0.25), rel=1e-15)
+
+
+@pytest.mark.parametrize("c", [-3.0, 0.5, 7.0])
+def test_constant_row_gives_signed_weighted_column_sum(c):
+    # a = c * 1: x_k = sign(c) g_k, so y = sign(c) * sum_k g_k W[k, :]
+    K, N = 8, 5
+    _, g, W = _rand_case(1, K, N, 3)
+    y = oracle.rmsnorm_linear(np.full((1, K), c), g, W, 0.0)[0]
+    np.testing.assert_allclose(y, math.copysign(1.0, c) * (g @ W), rtol=1e-13)
+
+
+@pytest.mark.parametrize("k,v", [(0, 2.5), (3, -0.75), (6, 40.0)])
+def test_one_hot_row(k, v):
+    # a = v e_k, eps = 0: RMS = |v|/sqrt(K), so y = sign(v) sqrt(K) g_k W[k, :]
+    K, N = 7, 4
+    _, g, W = _rand_case(1, K, N, 5, neg_g=True)
+    a = np.zeros((1, K))
+    a[0, k] = v
+    want = math.copysign(1.0, v) * math.sqrt(K) * g[k] * W[k]
+    np.testing.assert_allclose(oracle.rmsnorm_linear(a, g, W, 0.0)[0], want, rtol=1e-14)
+
+
+def test_zero_row():
+    # eps > 0: an all-zero row gives exactly zero; eps = 0 gives 0/0 = NaN in the standard form
+    K, N = 16, 8
+    _, g, W = _rand_case(1, K, N, 9)
+    a = np.zeros((1, K))
+    assert np.all(oracle.rmsnorm_linear(a, g, W, 1e-6) == 0.0)
+    assert np.all(np.isnan(oracle.rmsnorm_linear(a, g, W, 0.0)))
+    Wgu = np.concatenate([W, W[:, ::-1]], axis=1)
+    assert np.all(oracle.rmsnorm_swiglu(a, g, Wgu, 1e-6) == 0.0)
+
+
+# ---------------------------------------------------------------- library reductions
+@pytest.mark.parametrize("M,K,N,eps,seed", [(5, 16, 7, 1e-6, 0), (3, 576, 33, 1e-5, 1), (16, 64, 64, 0.0, 2)])
+def test_rmsnorm_linear_matches_torch_rms_norm(M, K, N, eps, seed):
+    a, g, W = _rand_case(M, K, N, seed, neg_g=True)
+    bias = np.random.default_rng(seed + 100).standard_normal(N)
+    ta, tg, tW, tb = (torch.from_numpy(x) for x in (a, g, W, bias))
+    eps32 = float(np.float32(eps))
+    ref = F.rms_norm(ta, (K,), weight=tg, eps=eps32) @ tW
+    np.testing.assert_allclose(oracle.rmsnorm_linear(a, g, W, eps), ref.numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(oracle.rmsnorm_linear(a, g, W, eps, bias=bias), (ref + tb).numpy(),
+                               rtol=1e-12, atol=1e-13)
+
+
+def test_plain_rmsnorm_is_identity_projection():
+    # g = 1, W = I: the op is plain RMSNorm of the row (torch.nn.functional.rms_norm)
+    a, _, _ = _rand_case(4, 12, 12, 7)
+    y = oracle.rmsnorm_linear(a, np.ones(12), np.eye(12), 1e-6)
+    ref = F.rms_norm(torch.from_numpy(a), (12,), eps=float(np.float32(1e-6))).numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-14, atol=1e-15)
+
+
+@pytest.mark.parametrize("M,K,F_,eps,seed", [(4, 32, 9, 1e-6, 0), (2, 576, 40, 1e-5, 1)])
+def test_swiglu_matches_torch(M, K, F_, eps, seed):
+    a, g, Wgu = _rand_case(M, K, 2 * F_, seed, neg_g=True)
+    ta, tg, tW = (torch.from_numpy(x) for x in (a, g, Wgu))
+    x = F.rms_norm(ta, (K,), weight=tg, eps=float(np.float32(eps)))
+    ref = F.silu(x @ tW[:, :F_]) * (x @ tW[:, F_:])
+    np.testing.assert_allclose(oracle.rmsnorm_swiglu(a, g, Wgu, eps), ref.numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_swiglu_one_hot_closed_form():
+    # a = v e_k, eps = 0: x = sign(v) sqrt(K) g_k e_k, so h = x_k W[k,:], out = h_g * sigmoid(h_g) * h_u
+    K, F_ = 9, 5
+    _, g, Wgu = _rand_case(1, K, 2 * F_, 11)
+    a = np.zeros((1, K))
+    a[0, 4] = -1.5
+    xk = -math.sqrt(K) * g[4]
+    hg, hu = xk * Wgu[4, :F_], xk * Wgu[4, F_:]
+    want = hg / (1.0 + np.exp(-hg)) * hu
+    np.testing.assert_allclose(oracle.rmsnorm_swiglu(a, g, Wgu, 0.0)[0], want, rtol=1e-13)
+
+
+@pytest.mark.parametrize("M,K,N,eps,seed", [(5, 16, 7, 1e-5, 0), (3, 256, 20, 1e-5, 1)])
+def test_layernorm_linear_matches_torch_layer_norm(M, K, N, eps, seed):
+    a, g, W = _rand_case(M, K, N, seed, neg_g=True)
+    a = a + 0.5
+    rng = np.random.default_rng(seed + 7)
+    beta = rng.standard_normal(K) * 0.3
+    bias = rng.standard_normal(N)
+    ta, tg, tb, tW = (torch.from_numpy(x) for x in (a, g, beta, W))
+    ref = F.layer_norm(ta, (K,), weight=tg, bias=tb, eps=float(np.float32(eps))) @ tW
+    np.testing.assert_allclose(oracle.layernorm_linear(a, g, beta, W, eps), ref.numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(oracle.layernorm_linear(a, g, beta, W, eps, bias=bias),
+                               ref.numpy() + bias, rtol=1e-12, atol=1e-13)
+    # plain standardisation: g = 1, beta = 0, W = I
+    st = oracle.layernorm_linear(a, np.ones(K), np.zeros(K), np.eye(K), eps)
+    ref_st = F.layer_norm(ta, (K,), eps=float(np.float32(eps))).numpy()
+    np.testing.assert_allclose(st, ref_st, rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- the paper's identities
+@pytest.mark.parametrize("M,K,N,seed", [(1, 1, 1, 0), (3, 5, 4, 1), (8, 16, 8, 2), (6, 9, 3, 3)])
+def test_forms_a_b_c_agree(M, K, N, seed):
+    # Props. 1 and 2: standard (a), weightless (b) and deferred (c) are the same function
+    a, g, W = _rand_case(M, K, N, seed, neg_g=True)
+    bias = np.random.default_rng(seed).standard_normal(N)
+    for eps in (0.0, 1e-6):
+        for b in (None, bias):
+            ya = oracle.rmsnorm_linear(a, g, W, eps, bias=b)
+            assert _rel(oracle.weightless(a, g, W, eps, bias=b), ya) <= 1e-12
+            assert _rel(oracle.deferred(a, g, W, eps, bias=b), ya) <= 1e-12
+
+
+def test_forms_agree_on_tiny_fp32_workload():
+    w = workloads.tiny_fp32()
+    ya = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+    yb = oracle.weightless(w.a, w.g, w.W, w.eps)
+    yc = oracle.deferred(w.a, w.g, w.W, w.eps)
+    for y in (yb, yc):
+        assert np.max(np.abs(y - ya).max(axis=1) / np.abs(ya).max(axis=1)) <= 1e-12
+    # an independent contraction of the same standard form (numpy einsum in fp64)
+    a, g, W = (x.double().numpy() for x in (w.a, w.g, w.W))
+    r = np.sqrt(np.float64(np.float32(w.eps)) + np.einsum("mk,mk->m", a, a) / a.shape[1])
+    ref = np.einsum("mk,k,kn->mn", a / r[:, None], g, W)
+    assert _rel(ya, ref) <= 1e-12
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_layernorm_deferred_agrees(seed):
+    a, g, W = _rand_case(6, 24, 10, seed, neg_g=True)
+    a = a * 2 + 0.5
+    beta = np.random.default_rng(seed).standard_normal(24)
+    bias = np.random.default_rng(seed + 1).standard_normal(10)
+    for b in (None, bias):
+        ya = oracle.layernorm_linear(a, g, beta, W, 1e-5, bias=b)
+        assert _rel(oracle.layernorm_linear_deferred(a, g, beta, W, 1e-5, bias=b), ya) <= 1e-12
+
+
+@pytest.mark.parametrize("c", [2.0 ** -10, 3.0, 2.0 ** 10, -0.5, -7.0])
+def test_scale_invariance(c):
+    # RMS(c a) = |c| RMS(a) (Sec. 3.3), so at eps = 0 y(c a) = sign(c) y(a)
+    a, g, W = _rand_case(4, 32, 6, 13, neg_g=True)
+    y = oracle.rmsnorm_linear(a, g, W, 0.0)
+    yc = oracle.rmsnorm_linear(c * a, g, W, 0.0)
+    assert _rel(yc, math.copysign(1.0, c) * y) <= 1e-13
+
+
+def test_epsilon_caveat_only_matters_at_low_energy():
+    # Sec. 3.3 "Epsilon caveat": with eps > 0 scale invariance is broken, materially only
+    # when the row's energy is near zero
+    a, g, W = _rand_case(1, 64, 8, 17)
+    eps = 1e-6
+    y = oracle.rmsnorm_linear(a, g, W, eps)
+    # at unit energy the deviation is of order eps / mean(a^2)
+    assert _rel(oracle.rmsnorm_linear(1e2 * a, g, W, eps), y) < 2 * eps / np.mean(a * a)
+    low = oracle.rmsnorm_linear(1e-4 * a, g, W, eps)
+    assert _rel(low, y) > 1e-3                   # eps limits the up-scaling
+    # and it is then exactly the eps-regularised value
+    r = math.sqrt(float(np.float32(eps)) + np.mean((1e-4 * a) ** 2))
+    np.testing.assert_allclose(low[0], (1e-4 * a[0] / r * g) @ W, rtol=1e-12)
+
+
+def test_rmsnorm_cancellation_prop3():
+    # Prop. 3: RMSNorm((a / RMS(a)) W*) = RMSNorm(a W*) (unit weights, eps = 0)
+    a, g, W = _rand_case(5, 20, 12, 19, neg_g=True)
+    inner = oracle.weightless(a, g, W, 0.0)            # (a / RMS(a)) W*
+    Ws = g[:, None] * W
+    ones = np.ones(12)
+    lhs = oracle.rmsnorm_linear(inner, ones, np.eye(12), 0.0)
+    rhs = oracle.rmsnorm_linear(a @ Ws, ones, np.eye(12), 0.0)
+    assert _rel(lhs, rhs) <= 1e-13
+
+
+def test_layernorm_shift_invariance_and_constant_row():
+    a, g, W = _rand_case(3, 16, 5, 23, neg_g=True)
+    beta = np.random.default_rng(1).standard_normal(16)
+    y = oracle.layernorm_linear(a, g, beta, W, 1e-5)
+    assert _rel(oracle.layernorm_linear(a + 3.25, g, beta, W, 1e-5), y) <= 1e-12
+    # a constant row is centred to zero, so y = beta W = c*
+    yc = oracle.layernorm_linear(np.full((1, 16), 0.7), g, beta, W, 1e-5)
+    np.testing.assert_allclose(yc[0], beta @ W, rtol=1e-13, atol=1e-15)
+
+
+def test_rss_form_eliminating_one_over_n():
+    # App. "Eliminating 1/n": a_i/RMSe(a) g_i = a_i/RSSe(a) g*_i with g* = sqrt(n) g,
+    # RSSe(a) = sqrt(n eps + sum a^2)
+    a, g, W = _rand_case(3, 50, 7, 29)
+    eps = 1e-5
+    y = oracle.rmsnorm_linear(a, g, W, eps)
+    n = a.shape[1]
+    e = float(np.float32(eps))
+    rss = np.sqrt(n * e + (a * a).sum(axis=1))
+    alt = (a / rss[:, None] * (math.sqrt(n) * g)) @ W
+    assert _rel(y, alt) <= 1e-13
+
+
+def test_row_subset_matches_full():
+    a, g, W = _rand_case(9, 16, 5, 31)
+    rows = [8, 0, 4, 4]
+    full = oracle.rmsnorm_linear(a, g, W, 1e-6)
+    np.testing.assert_array_equal(oracle.rmsnorm_linear(a, g, W, 1e-6, rows=rows), full[rows])
+    Wgu = np.concatenate([W, W + 1], axis=1)
+    fullg = oracle.rmsnorm_swiglu(a, g, Wgu, 1e-6)
+    np.testing.assert_array_equal(oracle.rmsnorm_swiglu(a, g, Wgu, 1e-6, rows=rows), fullg[rows])
+
+
+# ---------------------------------------------------------------- fold and rounding
+def _eval_expr(s):
+    return float(eval(s, {"__builtins__": {}}, {"inf": math.inf}))
+
+
+def test_bf16_rounding_golden():
+    with open(os.path.join(GOLDEN, "bf16_rounding.txt")) as f:
+        lines = [ln.split("#", 1)[0].split() for ln in f]
+    cases = [(l[0], l[1]) for l in lines if len(l) == 2]
+    assert len(cases) >= 10
+    for src, want in cases:
+        assert oracle.round_bf16(_eval_expr(src)) == _eval_expr(want), src
+
+
+def test_bf16_rounding_matches_torch_on_fp32_values():
+    # for fp32-representable inputs, one rounding from fp64 equals torch's fp32 -> bf16 (RNE)
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-30, 30, 4000),
+                        rng.standard_normal(1000) * 1e-39]).astype(np.float32)
+    want = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(oracle.round_bf16(x.astype(np.float64)), want)
+
+
+def _bf16_magnitude(code):
+    return float(np.array([code << 16], dtype=np.uint32).view(np.float32)[0])
+
+
+def _is_rne_bf16(p, s):
+    """Check s is the bf16 value nearest to p, ties to even, from the format definition:
+    s is representable, and neither bf16 neighbour of s is nearer to p (an equally near
+    neighbour is allowed only when s has the even significand)."""
+    fs = np.float32(s)
+    if float(fs) != s:
+        return False
+    bits = int(np.array([fs]).view(np.uint32)[0])
+    if bits & 0xFFFF:
+        return False                             # not representable in bf16
+    if s != 0 and (p < 0) != (s < 0):
+        return False
+    code = (bits >> 16) & 0x7FFF
+    d = abs(abs(p) - abs(s))
+    for nb in (code - 1, code + 1):
+        if nb < 0 or nb >= 0x7F80:               # below zero, or the infinity code
+            continue
+        dn = abs(abs(p) - _bf16_magnitude(nb))
+        if dn < d or (dn == d and code % 2):
+            return False
+    return True
+
+
+@pytest.mark.parametrize("storage", [oracle.STORAGE_BF16, oracle.STORAGE_F32])
+def test_fold_matches_definition(storage):
+    w = workloads.make("layernorm", 3, 40, 24, dtype=torch.bfloat16, seed=4)
+    W = w.W.double().numpy()
+    g = w.g.double().numpy()
+    beta = w.beta.double().numpy()
+    Ws, colsum, cstar = oracle.fold(W, g, beta, storage=storage)
+    P = g[:, None] * W                           # exact: bf16 x fp32 fits in fp64
+    if storage == oracle.STORAGE_BF16:
+        assert all(_is_rne_bf16(p, s) for p, s in zip(P.ravel(), Ws.ravel()))
+        assert np.any(Ws != P)                   # rounding actually happened
+    else:
+        np.testing.assert_array_equal(Ws, P.astype(np.float32).astype(np.float64))
+    np.testing.assert_allclose(colsum, Ws.sum(axis=0), rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(cstar, torch.from_numpy(beta) @ torch.from_numpy(W), rtol=1e-13, atol=1e-15)
+    # the unfolded product with stored weights reproduces the weightless form
+    a = w.a.double().numpy()
+    y_stored = (a / np.sqrt(float(np.float32(w.eps)) + (a * a).mean(1))[:, None]) @ P
+    assert _rel(y_stored, oracle.weightless(a, g, W, w.eps)) <= 1e-12
+
+
+def test_workload_recipe():
+    w = workloads.smollm2_prefill()
+    assert w.a.shape == (2048, 576) and w.W.shape == (576, 1536) and w.a.dtype == torch.bfloat16
+    assert w.outlier_rows.numel() == 20
+    mags = w.a.float().abs().mean(dim=1)
+    assert mags[w.outlier_rows].min() > 10 * mags.median()
+    d = workloads.llama7b_swiglu_decode(M=4)
+    d16 = workloads.llama7b_swiglu_decode(M=16)
+    assert torch.equal(d.a, d16.a[:4]) and d.W.shape == (4096, 22016)
+    t = workloads.tiny_fp32()
+    assert t.a.dtype == torch.float32 and t.W.shape == (576, 576)
+    assert abs(t.W.std().item() - 1 / 24) < 2e-3
