@@ -1,0 +1,177 @@
+/*
+ * flashnorm.h -- C ABI of the FlashNorm norm-then-project library for AMD MI355X (gfx950).
+ *
+ * FlashNorm ("FlashNorm: Fast Normalization for Transformers", arXiv 2407.09577)
+ * computes an RMSNorm followed by a linear layer, z = RMSNorm(a; g) W (Sec. 3.1),
+ * in the deferred form z = (a W*) * (1 / RMS(a)) with W* = diag(g) W folded once,
+ * offline (Prop. 1 "weightless normalization", Prop. 2 "deferred normalization").
+ * The per-row sum of squares is accumulated from the same activation tiles the
+ * matrix multiply consumes, so the two run side by side (Cor. 1) and a single
+ * per-row scale is applied in the epilogue.
+ *
+ * Notation: a[M,K] holds M activation rows of width K (the paper's n);
+ * W[K,N] maps K inputs to N outputs (the paper's k).  eps sits inside the root,
+ * RMSe(a) = sqrt(eps + (1/K) sum_k a_k^2) (App. "RMS with epsilon").
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers to tensors are DEVICE pointers owned by the caller.  The library
+ *    never allocates device memory, never synchronises, and keeps no mutable
+ *    global state: calls on different streams may run concurrently.
+ *  - Tensors are row-major with an explicit leading dimension (elements between
+ *    consecutive rows).  Every tensor pointer must be 16-byte aligned and every
+ *    leading dimension a multiple of 8 elements for bf16, 4 for fp32.
+ *  - Arguments are validated on the host before anything is launched; on any
+ *    error nothing is written and a negative fn_status is returned.  M == 0 is
+ *    a valid no-op.  Kernel launch failures return FN_ERR_HIP; faults during
+ *    execution surface at the caller's next synchronisation.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream).
+ *  - Results are deterministic: no atomics and no split reductions across
+ *    workgroups, so repeated calls give bitwise-identical outputs.
+ *  - The packed weight layout written by fold_weights is opaque; only the
+ *    library reads it.  One buffer serves both the many-row (matrix-core) and
+ *    the few-row (bandwidth-bound) kernels.
+ */
+#ifndef FLASHNORM_H
+#define FLASHNORM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FN_OK = 0,
+  FN_ERR_NULL = -1,        /* a required pointer is NULL */
+  FN_ERR_SHAPE = -2,       /* M < 0, K <= 0, N <= 0, leading dimension too small, K not a multiple of 8 (bf16) or 4 (fp32) */
+  FN_ERR_DTYPE = -3,       /* unknown dtype, or dtypes that do not match */
+  FN_ERR_ALIGN = -4,       /* a pointer is not 16-byte aligned or a leading dimension breaks row alignment */
+  FN_ERR_UNSUPPORTED = -5, /* valid request this build does not implement (e.g. a forced path that cannot run it) */
+  FN_ERR_VALUE = -6,       /* eps negative or not finite; unknown layout or path */
+  FN_ERR_HIP = -7,         /* the HIP runtime reported an error while launching */
+  FN_ERR_ALIAS = -8,       /* the output overlaps an input */
+  FN_ERR_SIZE = -9         /* a tensor exceeds the 32-bit byte extents the kernels address */
+} fn_status;
+
+typedef enum { FN_F32 = 0, FN_BF16 = 1 } fn_dtype;
+
+/* FN_LAYOUT_GLU: the logical weight is [K, 2F] = [Wg | Wu] (gate columns first,
+ * then up columns, Sec. 4.1 Fig. 3(a)); the packed layout pairs each gate column
+ * with its up column so one workgroup owns both. */
+typedef enum { FN_LAYOUT_LINEAR = 0, FN_LAYOUT_GLU = 1 } fn_layout;
+
+/* Kernel selection (Sec. 6 and App. "Production path": shape-specialised dispatch).
+ * AUTO picks by M; PREFILL forces the matrix-core tile kernel (any M);
+ * DECODE forces the bandwidth-bound few-row kernel (bf16, M <= 16, else
+ * FN_ERR_UNSUPPORTED).  fp32 always runs the fp32 kernel. */
+typedef enum { FN_PATH_AUTO = 0, FN_PATH_PREFILL = 1, FN_PATH_DECODE = 2 } fn_path;
+
+/* Largest M the DECODE path accepts. */
+#define FN_DECODE_MAX_M 16
+
+/* Bytes of the packed weight buffer that fold_weights writes for a logical
+ * weight with K rows and N columns (N = 2F for FN_LAYOUT_GLU) stored as
+ * ws_dtype.  Returns 0 for invalid arguments.  Host only; no device work. */
+size_t fold_weights_size(int64_t K, int64_t N, int layout, int ws_dtype);
+
+/* Fold the normalisation weights into the linear layer, once, offline
+ * (Prop. 1: W*[k,n] = g_k W[k,n]; Sec. 3.4: c* = beta W).
+ *   W       [K, N] row-major, leading dimension ldw >= N, dtype w_dtype (fp32 or bf16).
+ *           For FN_LAYOUT_GLU, N = 2F and W = [Wg | Wu].
+ *   g       [K] fp32, or NULL for g = 1 (plain packing of W, used by the unfused baseline).
+ *   beta    [K] fp32 LayerNorm bias, or NULL; needed only for c_star.
+ *   W_star  output, fold_weights_size(K, N, layout, ws_dtype) bytes, 16-byte aligned.
+ *           Each element is the exact product g_k W[k,n] rounded once
+ *           (to nearest, ties to even) to ws_dtype; padding is zero.
+ *           ws_dtype must equal the dtype of the activations it will be used with.
+ *   colsum  optional [N] fp32: sum over k of the STORED W*[k,n] (the mean correction
+ *           of the deferred LayerNorm), accumulated in fp64 and rounded once.
+ *   c_star  optional [N] fp32: sum over k of beta_k W[k,n] with the unfolded W,
+ *           accumulated in fp64 and rounded once; requires beta.
+ *   colsum and c_star are available for FN_LAYOUT_LINEAR only. */
+int fold_weights(const void* W, int64_t ldw, int w_dtype, const float* g, const float* beta,
+                 int64_t K, int64_t N, int layout, void* W_star, int ws_dtype, float* colsum,
+                 float* c_star, void* stream);
+
+/* Inverse of the packing: write the logical [K, N] weight held in W_star (as
+ * written by fold_weights with the same K, N, layout, ws_dtype) to out, row-major
+ * with leading dimension ldo >= N, in ws_dtype.  Inspection and tests only. */
+int unpack_weights(const void* W_star, int64_t K, int64_t N, int layout, int ws_dtype, void* out,
+                   int64_t ldo, void* stream);
+
+/* Deferred RMSNorm -> linear (Prop. 2; with a bias, the Remark "Bias case": the
+ * scale is applied before the bias is added):
+ *   y[m,n] = (sum_k a[m,k] W*[k,n]) * s_m  (+ bias[n]),  s_m = 1/sqrt(eps + ss_m/K),
+ *   ss_m = sum_k a[m,k]^2 accumulated from the tiles the product reads.
+ *   a       [M, K] activations, leading dimension lda >= K, dtype a_dtype.
+ *   W_star  packed by fold_weights(..., N, FN_LAYOUT_LINEAR, a_dtype, ...).
+ *   bias    optional [N] fp32 output bias.
+ *   y       [M, N] output, leading dimension ldy >= N, dtype y_dtype == a_dtype;
+ *           computed in fp32 and rounded once (to nearest even) on the store.
+ *   inv_rms optional [M] fp32 side output of s_m (for consumers that defer the scale further). */
+int flashnorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                     const void* W_star, int64_t N, float eps, const float* bias, void* y,
+                     int64_t ldy, int y_dtype, float* inv_rms, void* stream);
+
+/* RMSNorm -> SwiGLU FFN input projection with both branch scales deferred to the
+ * products (Sec. 4.1, Fig. 3(a)):
+ *   out[m,f] = silu(s_m (a W*g)[m,f]) * (s_m (a W*u)[m,f]),  silu(t) = t / (1 + e^-t).
+ *   W_star_gu  packed by fold_weights(..., 2F, FN_LAYOUT_GLU, a_dtype, ...).
+ *   out        [M, F], leading dimension ldo >= F, dtype out_dtype == a_dtype. */
+int flashnorm_glu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                  const void* W_star_gu, int64_t F, float eps, void* out, int64_t ldo,
+                  int out_dtype, void* stream);
+
+/* Deferred LayerNorm -> linear.  LayerNorm is centering followed by RMS scaling
+ * with g and the bias beta (Sec. 2); beta moves past W as c* = beta W (Sec. 3.4),
+ * g folds into W* (Prop. 1), the 1/sigma scale is deferred (Prop. 2) and the
+ * centering is exchanged with the sum over k as in Sec. 3.5:
+ *   y[m,n] = ((a W*)[m,n] - mu_m colsum[n]) / sigma_m + c_star[n],
+ *   mu_m = sa_m/K, sigma_m = sqrt(ss_m/K - mu_m^2 + eps), sa and ss accumulated
+ *   from the tiles the product reads.
+ *   colsum  [N] fp32 from fold_weights (required);  c_star  [N] fp32 or NULL (= 0).
+ *   The one-pass variance loses precision when |mu| >> sigma (relative error of
+ *   order (mu/sigma)^2 * 2^-24 in fp32). */
+int flashnorm_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                               const void* W_star, const float* colsum, const float* c_star,
+                               int64_t N, float eps, void* y, int64_t ldy, int y_dtype,
+                               void* stream);
+
+/* The same three operations with an explicit kernel selection (fn_path). */
+int flashnorm_linear_ex(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                        const void* W_star, int64_t N, float eps, const float* bias, void* y,
+                        int64_t ldy, int y_dtype, float* inv_rms, int path, void* stream);
+int flashnorm_glu_ex(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                     const void* W_star_gu, int64_t F, float eps, void* out, int64_t ldo,
+                     int out_dtype, int path, void* stream);
+int flashnorm_layernorm_linear_ex(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                                  const void* W_star, const float* colsum, const float* c_star,
+                                  int64_t N, float eps, void* y, int64_t ldy, int y_dtype,
+                                  int path, void* stream);
+
+/* Unfused baselines in the same library (the sequential RMSNorm -> GEMM of Fig. 1(a)
+ * and Sec. 6): a normalisation kernel writes the normalised activations
+ * x = RMSNorm(a; g) (or LayerNorm(a; g, beta)) to the caller's workspace x_ws
+ * ([M, K], leading dimension K, dtype a_dtype), then the same matrix-multiply
+ * kernels run on x without any normalisation epilogue.
+ *   W_packed is the UNFOLDED weight packed by fold_weights with g = NULL.
+ *   baseline_layernorm_linear adds no c*: beta enters through x. */
+int baseline_rmsnorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                            const float* g, const void* W_packed, int64_t N, float eps, void* x_ws,
+                            void* y, int64_t ldy, int path, void* stream);
+int baseline_rmsnorm_glu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                         const float* g, const void* W_packed_gu, int64_t F, float eps,
+                         void* x_ws, void* out, int64_t ldo, int path, void* stream);
+int baseline_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                              const float* g, const float* beta, const void* W_packed, int64_t N,
+                              float eps, void* x_ws, void* y, int64_t ldy, int path, void* stream);
+
+/* Human-readable name of a status code (static string; never NULL). */
+const char* flashnorm_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHNORM_H */

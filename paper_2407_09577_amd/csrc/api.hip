@@ -1,0 +1,268 @@
+// C ABI of the FlashNorm library: argument validation (before anything is
+// launched), shape-specialised kernel selection, and launches on the caller's
+// stream.  No allocation, no synchronisation, no mutable global state.
+#include <math.h>
+#include <stdint.h>
+
+#include "flashnorm.h"
+#include "fn_launch.h"
+
+namespace {
+
+using fn::EpiArgs;
+
+constexpr int64_t kMaxLd = int64_t(1) << 21;    // leading dimensions, K (keeps tile extents < 2^31)
+constexpr int64_t kMaxRows = int64_t(1) << 30;  // M, N
+
+bool dtype_ok(int d) { return d == FN_F32 || d == FN_BF16; }
+int64_t elem_size(int d) { return d == FN_BF16 ? 2 : 4; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+int64_t row_align(int d) { return 16 / elem_size(d); }
+
+bool overlaps(const void* p, int64_t pbytes, const void* q, int64_t qbytes) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(p), b0 = reinterpret_cast<uintptr_t>(q);
+  return a0 < b0 + (uintptr_t)qbytes && b0 < a0 + (uintptr_t)pbytes;
+}
+
+int64_t extent_bytes(int64_t rows, int64_t cols, int64_t ld, int dtype) {
+  return rows > 0 ? ((rows - 1) * ld + cols) * elem_size(dtype) : 0;
+}
+
+// Common checks of an activation-like operand [M, K] with leading dimension ld.
+int check_matrix(const void* p, int64_t M, int64_t K, int64_t ld, int dtype, bool required) {
+  if (M < 0 || K <= 0 || M > kMaxRows) return FN_ERR_SHAPE;
+  if (ld < K) return FN_ERR_SHAPE;
+  if (ld > kMaxLd) return FN_ERR_SIZE;
+  if (required && M > 0 && !p) return FN_ERR_NULL;
+  if (!aligned16(p) || ld % row_align(dtype)) return FN_ERR_ALIGN;
+  return FN_OK;
+}
+
+int check_eps(float eps) { return (isfinite(eps) && eps >= 0.0f) ? FN_OK : FN_ERR_VALUE; }
+
+int status_of(hipError_t e) { return e == hipSuccess ? FN_OK : FN_ERR_HIP; }
+
+struct OpDesc {
+  const void* a;
+  int64_t M, K, lda;
+  int dtype;
+  const void* ws;
+  int64_t ncols;  // N, or F for a GLU
+  int glu;
+  void* y;
+  int64_t ldy;
+  int epi;
+  EpiArgs ep;
+  int path;
+  hipStream_t stream;
+};
+
+// Validation shared by the three fused ops (and the baselines' matrix multiply).
+int validate_op(const OpDesc& d, int y_dtype) {
+  if (!dtype_ok(d.dtype) || !dtype_ok(y_dtype)) return FN_ERR_DTYPE;
+  if (y_dtype != d.dtype) return FN_ERR_DTYPE;
+  if (d.path < FN_PATH_AUTO || d.path > FN_PATH_DECODE) return FN_ERR_VALUE;
+  if (d.K > kMaxLd) return FN_ERR_SIZE;
+  if (d.K % (d.dtype == FN_BF16 ? 8 : 4)) return FN_ERR_SHAPE;
+  int s = check_matrix(d.a, d.M, d.K, d.lda, d.dtype, true);
+  if (s) return s;
+  if (d.ncols <= 0 || d.ncols > kMaxRows) return FN_ERR_SHAPE;
+  s = check_matrix(d.y, d.M, d.ncols, d.ldy, d.dtype, true);
+  if (s) return s;
+  if (!d.ws) return FN_ERR_NULL;
+  if (!aligned16(d.ws)) return FN_ERR_ALIGN;
+  s = check_eps(d.ep.eps);
+  if (s) return s;
+  if (d.M > 0) {
+    const int64_t ybytes = extent_bytes(d.M, d.ncols, d.ldy, d.dtype);
+    const int64_t N = d.glu ? 2 * d.ncols : d.ncols;
+    const int64_t wbytes = fold_weights_size(d.K, N, d.glu ? FN_LAYOUT_GLU : FN_LAYOUT_LINEAR, d.dtype);
+    if (overlaps(d.y, ybytes, d.a, extent_bytes(d.M, d.K, d.lda, d.dtype))) return FN_ERR_ALIAS;
+    if (overlaps(d.y, ybytes, d.ws, wbytes)) return FN_ERR_ALIAS;
+  }
+  if (d.path == FN_PATH_DECODE && (d.dtype != FN_BF16 || d.M > FN_DECODE_MAX_M)) return FN_ERR_UNSUPPORTED;
+  return FN_OK;
+}
+
+int run_op(const OpDesc& d) {
+  if (d.M == 0) return FN_OK;
+  const int64_t N = d.glu ? 2 * d.ncols : d.ncols;
+  const int NP = (int)fn::packed_cols(N, d.glu), KP = (int)fn::packed_rows(d.K);
+  if (d.dtype == FN_F32) {
+    fn::F32Args p{(const float*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const float*)d.ws, NP, KP,
+                  (int)d.ncols, (float*)d.y, (int)d.ldy, d.epi, d.ep, d.stream};
+    return status_of(fn::launch_f32(p));
+  }
+  const bool decode = d.path == FN_PATH_DECODE || (d.path == FN_PATH_AUTO && d.M <= FN_DECODE_MAX_M);
+  if (decode) {
+    fn::DecodeArgs p{(const __bf16*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const __bf16*)d.ws, NP, KP,
+                     (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, d.ep, d.stream};
+    return status_of(fn::launch_decode_bf16(p));
+  }
+  fn::PrefillArgs p{(const __bf16*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const __bf16*)d.ws, NP, KP,
+                    (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, fn::TILE_AUTO, d.ep, d.stream};
+  return status_of(fn::launch_prefill_bf16(p));
+}
+
+EpiArgs make_ep(float eps, int64_t K) {
+  EpiArgs ep{};
+  ep.eps = eps;
+  ep.inv_k = 1.0f / (float)K;
+  return ep;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t fold_weights_size(int64_t K, int64_t N, int layout, int ws_dtype) {
+  if (K <= 0 || N <= 0 || K > kMaxLd || N > kMaxRows || !dtype_ok(ws_dtype)) return 0;
+  if (layout != FN_LAYOUT_LINEAR && layout != FN_LAYOUT_GLU) return 0;
+  if (layout == FN_LAYOUT_GLU && N % 2) return 0;
+  return (size_t)(fn::packed_rows(K) * fn::packed_cols(N, layout == FN_LAYOUT_GLU) * elem_size(ws_dtype));
+}
+
+int fold_weights(const void* W, int64_t ldw, int w_dtype, const float* g, const float* beta, int64_t K,
+                 int64_t N, int layout, void* W_star, int ws_dtype, float* colsum, float* c_star,
+                 void* stream) {
+  if (!dtype_ok(w_dtype) || !dtype_ok(ws_dtype)) return FN_ERR_DTYPE;
+  if (layout != FN_LAYOUT_LINEAR && layout != FN_LAYOUT_GLU) return FN_ERR_VALUE;
+  if (K <= 0 || N <= 0 || ldw < N || (layout == FN_LAYOUT_GLU && N % 2)) return FN_ERR_SHAPE;
+  if (K > kMaxLd || N > kMaxRows) return FN_ERR_SIZE;
+  if (!W || !W_star) return FN_ERR_NULL;
+  if (c_star && !beta) return FN_ERR_NULL;
+  if (layout == FN_LAYOUT_GLU && (colsum || c_star)) return FN_ERR_UNSUPPORTED;
+  if (!aligned16(W_star) || (reinterpret_cast<uintptr_t>(W) % elem_size(w_dtype))) return FN_ERR_ALIGN;
+  const int64_t wsb = (int64_t)fold_weights_size(K, N, layout, ws_dtype);
+  if (overlaps(W_star, wsb, W, extent_bytes(K, N, ldw, w_dtype))) return FN_ERR_ALIAS;
+  fn::FoldArgs p{W, ldw, w_dtype, g, beta, K, N, layout == FN_LAYOUT_GLU, W_star, ws_dtype, colsum,
+                 c_star, (hipStream_t)stream};
+  return status_of(fn::launch_fold(p));
+}
+
+int unpack_weights(const void* W_star, int64_t K, int64_t N, int layout, int ws_dtype, void* out,
+                   int64_t ldo, void* stream) {
+  if (!dtype_ok(ws_dtype)) return FN_ERR_DTYPE;
+  if (layout != FN_LAYOUT_LINEAR && layout != FN_LAYOUT_GLU) return FN_ERR_VALUE;
+  if (K <= 0 || N <= 0 || ldo < N || (layout == FN_LAYOUT_GLU && N % 2)) return FN_ERR_SHAPE;
+  if (K > kMaxLd || N > kMaxRows) return FN_ERR_SIZE;
+  if (!W_star || !out) return FN_ERR_NULL;
+  if (!aligned16(W_star) || (reinterpret_cast<uintptr_t>(out) % elem_size(ws_dtype))) return FN_ERR_ALIGN;
+  const int64_t wsb = (int64_t)fold_weights_size(K, N, layout, ws_dtype);
+  if (overlaps(out, extent_bytes(K, N, ldo, ws_dtype), W_star, wsb)) return FN_ERR_ALIAS;
+  return status_of(fn::launch_unpack(W_star, K, N, layout == FN_LAYOUT_GLU, ws_dtype, out, ldo,
+                                     (hipStream_t)stream));
+}
+
+int flashnorm_linear_ex(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star,
+                        int64_t N, float eps, const float* bias, void* y, int64_t ldy, int y_dtype,
+                        float* inv_rms, int path, void* stream) {
+  OpDesc d{a, M, K, lda, a_dtype, W_star, N, 0, y, ldy, fn::EPI_RMS, make_ep(eps, K), path, (hipStream_t)stream};
+  d.ep.bias = bias;
+  d.ep.inv_rms = inv_rms;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  return run_op(d);
+}
+
+int flashnorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star,
+                     int64_t N, float eps, const float* bias, void* y, int64_t ldy, int y_dtype,
+                     float* inv_rms, void* stream) {
+  return flashnorm_linear_ex(a, M, K, lda, a_dtype, W_star, N, eps, bias, y, ldy, y_dtype, inv_rms,
+                             FN_PATH_AUTO, stream);
+}
+
+int flashnorm_glu_ex(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star_gu,
+                     int64_t F, float eps, void* out, int64_t ldo, int out_dtype, int path, void* stream) {
+  OpDesc d{a, M, K, lda, a_dtype, W_star_gu, F, 1, out, ldo, fn::EPI_GLU, make_ep(eps, K), path,
+           (hipStream_t)stream};
+  int s = validate_op(d, out_dtype);
+  if (s) return s;
+  return run_op(d);
+}
+
+int flashnorm_glu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star_gu,
+                  int64_t F, float eps, void* out, int64_t ldo, int out_dtype, void* stream) {
+  return flashnorm_glu_ex(a, M, K, lda, a_dtype, W_star_gu, F, eps, out, ldo, out_dtype, FN_PATH_AUTO,
+                          stream);
+}
+
+int flashnorm_layernorm_linear_ex(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                                  const void* W_star, const float* colsum, const float* c_star, int64_t N,
+                                  float eps, void* y, int64_t ldy, int y_dtype, int path, void* stream) {
+  OpDesc d{a, M, K, lda, a_dtype, W_star, N, 0, y, ldy, fn::EPI_LN, make_ep(eps, K), path, (hipStream_t)stream};
+  d.ep.colsum = colsum;
+  d.ep.cstar = c_star;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  if (!colsum) return FN_ERR_NULL;
+  return run_op(d);
+}
+
+int flashnorm_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                               const void* W_star, const float* colsum, const float* c_star, int64_t N,
+                               float eps, void* y, int64_t ldy, int y_dtype, void* stream) {
+  return flashnorm_layernorm_linear_ex(a, M, K, lda, a_dtype, W_star, colsum, c_star, N, eps, y, ldy,
+                                       y_dtype, FN_PATH_AUTO, stream);
+}
+
+// Unfused baselines: normalise into the workspace, then the plain matrix multiply.
+static int baseline_common(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
+                           const float* beta, const void* Wp, int64_t ncols, int glu, float eps, void* x_ws,
+                           void* y, int64_t ldy, int path, void* stream) {
+  OpDesc d{x_ws, M, K, K, a_dtype, Wp, ncols, glu, y, ldy, glu ? fn::EPI_GLU_NOSCALE : fn::EPI_NONE,
+           make_ep(eps, K), path, (hipStream_t)stream};
+  int s = validate_op(d, a_dtype);
+  if (s) return s;
+  s = check_matrix(a, M, K, lda, a_dtype, true);
+  if (s) return s;
+  if (!g) return FN_ERR_NULL;
+  if (K > 16384) return FN_ERR_UNSUPPORTED;  // one row per workgroup held in registers
+  if (M == 0) return FN_OK;
+  const int64_t xb = extent_bytes(M, K, K, a_dtype);
+  if (overlaps(x_ws, xb, a, extent_bytes(M, K, lda, a_dtype)) ||
+      overlaps(x_ws, xb, y, extent_bytes(M, ncols, ldy, a_dtype)))
+    return FN_ERR_ALIAS;
+  s = status_of(fn::launch_norm_rows(a, (int)M, (int)K, (int)lda, a_dtype, g, beta, eps, x_ws, (int)K,
+                                     (hipStream_t)stream));
+  if (s) return s;
+  return run_op(d);
+}
+
+int baseline_rmsnorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
+                            const void* W_packed, int64_t N, float eps, void* x_ws, void* y, int64_t ldy,
+                            int path, void* stream) {
+  return baseline_common(a, M, K, lda, a_dtype, g, nullptr, W_packed, N, 0, eps, x_ws, y, ldy, path, stream);
+}
+
+int baseline_rmsnorm_glu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
+                         const void* W_packed_gu, int64_t F, float eps, void* x_ws, void* out, int64_t ldo,
+                         int path, void* stream) {
+  return baseline_common(a, M, K, lda, a_dtype, g, nullptr, W_packed_gu, F, 1, eps, x_ws, out, ldo, path,
+                         stream);
+}
+
+int baseline_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
+                              const float* beta, const void* W_packed, int64_t N, float eps, void* x_ws,
+                              void* y, int64_t ldy, int path, void* stream) {
+  if (!beta) return FN_ERR_NULL;
+  return baseline_common(a, M, K, lda, a_dtype, g, beta, W_packed, N, 0, eps, x_ws, y, ldy, path, stream);
+}
+
+const char* flashnorm_status_string(int status) {
+  switch (status) {
+    case FN_OK: return "FN_OK";
+    case FN_ERR_NULL: return "FN_ERR_NULL: a required pointer is NULL";
+    case FN_ERR_SHAPE: return "FN_ERR_SHAPE: invalid shape or leading dimension";
+    case FN_ERR_DTYPE: return "FN_ERR_DTYPE: unknown or mismatched dtype";
+    case FN_ERR_ALIGN: return "FN_ERR_ALIGN: pointer or leading dimension breaks 16-byte alignment";
+    case FN_ERR_UNSUPPORTED: return "FN_ERR_UNSUPPORTED: request not implemented by this build";
+    case FN_ERR_VALUE: return "FN_ERR_VALUE: invalid eps, layout or path";
+    case FN_ERR_HIP: return "FN_ERR_HIP: HIP runtime error at launch";
+    case FN_ERR_ALIAS: return "FN_ERR_ALIAS: output overlaps an input";
+    case FN_ERR_SIZE: return "FN_ERR_SIZE: tensor extent beyond the kernels' 32-bit addressing";
+  }
+  return "unknown fn_status";
+}
+
+}  // extern "C"

@@ -1,0 +1,138 @@
+// fp32 fused norm-then-project kernel (small fp32 problems; exact fp32 products,
+// no reduced-precision matrix-core modes).
+//
+// A 256-thread workgroup owns a 64 x 64 output tile and walks K in steps of 16,
+// staging the activation and weight tiles in LDS.  The threads that stage an
+// activation row also accumulate its sum of squares (and sum, for LayerNorm)
+// from the values they just loaded, alongside the products (Cor. 1); the
+// deferred per-row scale (Prop. 2) is applied in the epilogue.  Thread (tx, ty)
+// computes rows ty + 16 i and packed columns tx + 16 j, so columns j = 0, 1 (and
+// 2, 3) are a GLU gate block and its up block.
+#include "fn_device.h"
+#include "fn_launch.h"
+
+namespace fn {
+
+template <int EPI>
+__global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, int M, int K, int lda,
+                                                  const float* __restrict__ ws, int NP, int KP,
+                                                  int ncols, float* __restrict__ y, int ldy,
+                                                  EpiArgs ep) {
+  constexpr int BM = 64, BN = 64, BK = 16;
+  __shared__ float As[BK][BM + 4];
+  __shared__ float Wsh[BK][BN];
+  __shared__ float row_ss[BM], row_sa[BM];
+
+  const int t = threadIdx.x;
+  const int tx = t & 15, ty = t >> 4;
+  const int m0 = blockIdx.y * BM, p0 = blockIdx.x * BN;
+
+  const int lr = t >> 2, lkq = (t & 3) * 4;       // activation staging: row, k quad
+  const int wk = t >> 4, wc = (t & 15) * 4;        // weight staging: k row, column quad
+  const bool lr_ok = m0 + lr < M;
+  const bool wc_ok = p0 + wc < NP;
+
+  float acc[4][4] = {};
+  float ss = 0.f, sa = 0.f;
+  for (int k0 = 0; k0 < K; k0 += BK) {
+    float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (lr_ok && k0 + lkq < K)
+      av = *reinterpret_cast<const float4*>(a + (int64_t)(m0 + lr) * lda + k0 + lkq);
+    ss = fmaf(av.x, av.x, ss);
+    ss = fmaf(av.y, av.y, ss);
+    ss = fmaf(av.z, av.z, ss);
+    ss = fmaf(av.w, av.w, ss);
+    sa += (av.x + av.y) + (av.z + av.w);
+    float4 wv = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (wc_ok) wv = *reinterpret_cast<const float4*>(ws + (int64_t)(k0 + wk) * NP + p0 + wc);
+    __syncthreads();
+    As[lkq + 0][lr] = av.x;
+    As[lkq + 1][lr] = av.y;
+    As[lkq + 2][lr] = av.z;
+    As[lkq + 3][lr] = av.w;
+    *reinterpret_cast<float4*>(&Wsh[wk][wc]) = wv;
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < BK; ++kk) {
+      float ar[4], wr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ar[i] = As[kk][ty + 16 * i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) wr[j] = Wsh[kk][tx + 16 * j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(ar[i], wr[j], acc[i][j]);
+    }
+  }
+  ss += __shfl_xor(ss, 1);
+  ss += __shfl_xor(ss, 2);
+  sa += __shfl_xor(sa, 1);
+  sa += __shfl_xor(sa, 2);
+  if ((t & 3) == 0) {
+    row_ss[lr] = ss;
+    row_sa[lr] = sa;
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = ty + 16 * i;
+    const int m = m0 + r;
+    if (m >= M) continue;
+    float s = 1.f, mu = 0.f;
+    if constexpr (EPI == EPI_RMS || EPI == EPI_GLU) {
+      s = rsqrtf(fmaf(row_ss[r], ep.inv_k, ep.eps));
+      if (EPI == EPI_RMS && ep.inv_rms && blockIdx.x == 0 && tx == 0) ep.inv_rms[m] = s;
+    } else if constexpr (EPI == EPI_LN) {
+      mu = row_sa[r] * ep.inv_k;
+      const float var = fmaxf(fmaf(row_ss[r], ep.inv_k, -mu * mu), 0.f);
+      s = rsqrtf(var + ep.eps);
+    }
+    float* yr = y + (int64_t)m * ldy;
+    if constexpr (epi_is_glu(EPI)) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int f = p0 / 2 + 16 * q + tx;
+        const float gate = acc[i][2 * q], up = acc[i][2 * q + 1];
+        if (f < ncols)
+          yr[f] = EPI == EPI_GLU ? silu(gate * s) * (up * s) : silu(gate) * up;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c = p0 + tx + 16 * j;
+        if (c >= ncols) continue;
+        float v = acc[i][j];
+        if constexpr (EPI == EPI_RMS) {
+          v *= s;
+          if (ep.bias) v += ep.bias[c];
+        } else if constexpr (EPI == EPI_LN) {
+          v = fmaf(fmaf(-mu, ep.colsum[c], v), s, ep.cstar ? ep.cstar[c] : 0.f);
+        }
+        yr[c] = v;
+      }
+    }
+  }
+}
+
+template <int EPI>
+static hipError_t launch_f32_epi(const F32Args& p) {
+  dim3 grid((p.NP + 63) / 64, (p.M + 63) / 64);
+  hipLaunchKernelGGL(f32_kernel<EPI>, grid, dim3(256), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP,
+                     p.KP, p.ncols, p.y, p.ldy, p.ep);
+  return hipGetLastError();
+}
+
+hipError_t launch_f32(const F32Args& p) {
+  switch (p.epi) {
+    case EPI_RMS: return launch_f32_epi<EPI_RMS>(p);
+    case EPI_GLU: return launch_f32_epi<EPI_GLU>(p);
+    case EPI_LN: return launch_f32_epi<EPI_LN>(p);
+    case EPI_NONE: return launch_f32_epi<EPI_NONE>(p);
+    case EPI_GLU_NOSCALE: return launch_f32_epi<EPI_GLU_NOSCALE>(p);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace fn

@@ -1,0 +1,149 @@
+// Device-side building blocks shared by the FlashNorm gfx950 kernels.
+//
+// Packed weight layout ("fragment-major"), written by fold_weights and read by
+// every bf16 kernel.  A logical column n is first mapped to a packed column p
+// (identity for a linear layer; for a GLU, gate feature f goes to
+// 32*(f/16) + f%16 and up feature f to 32*(f/16) + 16 + f%16, so a gate block of
+// 16 columns is immediately followed by its up block).  Packed columns are padded
+// to NP (a multiple of 16) and rows to KP (a multiple of 64) with zeros.  The
+// packed buffer is a sequence of 1 KiB fragments, column-block major:
+//   fragment (cb, kb) = columns [16 cb, 16 cb + 16) x rows [32 kb, 32 kb + 32),
+//   at byte offset (cb * KP/32 + kb) * 1024; inside it, lane L = 16 * ((k%32)/8) + p%16
+//   holds the 8 consecutive rows k..k+7 (k%8 == 0) of column p as 16 bytes.
+// That is exactly the per-lane operand of one v_mfma_f32_16x16x32_bf16, so a
+// wave moves a fragment global -> LDS -> registers with one 16-byte access per
+// lane, and a column block's whole K extent is one contiguous stream.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fn {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+
+constexpr int kFragBytes = 1024;  // one 16 x 32 bf16 operand fragment
+constexpr int kKB = 32;           // k extent of a fragment
+constexpr int kKPad = 64;         // packed K is padded to this
+constexpr int kNPad = 16;         // packed columns are padded to this
+constexpr int kDtypeF32 = 0;      // element type codes of the C ABI
+constexpr int kDtypeBf16 = 1;
+
+// dword 3 of a CDNA buffer resource: 32-bit raw data, no swizzle, range checked.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+// A voffset this large is outside every buffer the kernels build (all extents < 2^31),
+// so the load returns zeros.
+constexpr unsigned kOobOffset = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           kBufferRsrcWord3);
+}
+
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+
+// Buffer resource as four SGPRs, for the LDS-DMA loads issued through inline asm.
+__device__ __forceinline__ i32x4 make_rsrc_sgpr(const void* base, uint32_t bytes) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  i32x4 r;
+  r[0] = (int)(uint32_t)p;
+  r[1] = (int)(uint32_t)(p >> 32) & 0xffff;  // stride 0
+  r[2] = (int)bytes;                          // num_records (bytes)
+  r[3] = kBufferRsrcWord3;
+  r[0] = __builtin_amdgcn_readfirstlane(r[0]);
+  r[1] = __builtin_amdgcn_readfirstlane(r[1]);
+  r[2] = __builtin_amdgcn_readfirstlane(r[2]);
+  r[3] = __builtin_amdgcn_readfirstlane(r[3]);
+  return r;
+}
+
+// 16 bytes per lane from a range-checked buffer straight into LDS: lane i of the
+// wave writes lds_base + 16 * i; out-of-range lanes write zeros.  Issued through
+// inline asm so the compiler does not add a conservative wait for these writes
+// before unrelated LDS reads: the kernels order them with explicit vmcnt waits
+// and barriers.  lds_base must be wave-uniform.
+__device__ __forceinline__ void load_lds16(i32x4 rsrc, const void* lds_base, unsigned voffset) {
+  const unsigned m0 = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_base);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(m0), "v"(voffset), "s"(rsrc)
+               : "memory", "m0");
+}
+
+// 16 bytes per lane from a range-checked buffer into registers.
+__device__ __forceinline__ u32x4 load_buf16(__amdgpu_buffer_rsrc_t rsrc, unsigned voffset) {
+  return __builtin_amdgcn_raw_buffer_load_b128(rsrc, voffset, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding:
+// vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ float bf16_lo(unsigned w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(unsigned w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ unsigned f32_to_bf16_bits(float f) {
+  unsigned u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// sum of squares and plain sum of the 8 bf16 values of one operand fragment lane,
+// via packed bf16 dot products accumulated in fp32.
+__device__ __forceinline__ float sumsq8(const bf16x8& v, float acc) {
+  bf16x2 p0 = {v[0], v[1]}, p1 = {v[2], v[3]}, p2 = {v[4], v[5]}, p3 = {v[6], v[7]};
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p0, p0, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p1, p1, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p3, p3, acc, false);
+  return acc;
+}
+
+__device__ __forceinline__ float sum8(const bf16x8& v, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  bf16x2 p0 = {v[0], v[1]}, p1 = {v[2], v[3]}, p2 = {v[4], v[5]}, p3 = {v[6], v[7]};
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p0, one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p1, one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p2, one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(p3, one, acc, false);
+  return acc;
+}
+
+__device__ __forceinline__ float silu(float t) { return t / (1.0f + __expf(-t)); }
+
+// Epilogue kinds of the fused kernels.
+enum Epi : int {
+  EPI_RMS = 0,          // y = acc * s (+ bias)
+  EPI_GLU = 1,          // out = silu(s * gate) * (s * up)
+  EPI_LN = 2,           // y = (acc - mu * colsum) * rstd + c*
+  EPI_NONE = 3,         // y = acc                      (unfused baseline GEMM)
+  EPI_GLU_NOSCALE = 4,  // out = silu(gate) * up        (unfused baseline GEMM)
+};
+
+constexpr bool epi_is_glu(int e) { return e == EPI_GLU || e == EPI_GLU_NOSCALE; }
+constexpr bool epi_needs_ss(int e) { return e == EPI_RMS || e == EPI_GLU || e == EPI_LN; }
+
+struct EpiArgs {
+  float eps;
+  float inv_k;          // 1/K
+  const float* bias;    // EPI_RMS: optional [N]
+  const float* colsum;  // EPI_LN: [N]
+  const float* cstar;   // EPI_LN: optional [N]
+  float* inv_rms;       // EPI_RMS: optional [M]
+};
+
+}  // namespace fn

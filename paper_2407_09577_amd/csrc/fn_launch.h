@@ -1,0 +1,87 @@
+// Host-side launch interface between the C ABI (api.hip) and the kernel files.
+// Arguments reaching these functions have already been validated.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fn_device.h"
+
+namespace fn {
+
+enum Tile : int { TILE_AUTO = 0, TILE_256x256 = 1, TILE_128x128 = 2 };
+
+// Packed-layout geometry shared by the fold and the kernels.
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+// Packed column count: N for a linear layer, 2 * round_up(F, 16) for a GLU with N = 2F.
+inline int64_t packed_cols(int64_t N, int glu) {
+  return glu ? 2 * round_up(N / 2, kNPad) : round_up(N, kNPad);
+}
+inline int64_t packed_rows(int64_t K) { return round_up(K, kKPad); }
+
+struct PrefillArgs {
+  const __bf16* a;
+  int M, K, lda;
+  const __bf16* ws;
+  int NP, KP;
+  int ncols;  // logical output columns (N, or F for a GLU)
+  __bf16* y;
+  int ldy;
+  int epi;
+  int tile;
+  EpiArgs ep;
+  hipStream_t stream;
+};
+hipError_t launch_prefill_bf16(const PrefillArgs& p);
+
+struct DecodeArgs {
+  const __bf16* a;
+  int M, K, lda;
+  const __bf16* ws;
+  int NP, KP;
+  int ncols;
+  __bf16* y;
+  int ldy;
+  int epi;
+  EpiArgs ep;
+  hipStream_t stream;
+};
+hipError_t launch_decode_bf16(const DecodeArgs& p);
+
+struct F32Args {
+  const float* a;
+  int M, K, lda;
+  const float* ws;  // [KP][NP] row-major fp32, columns in packed order
+  int NP, KP;
+  int ncols;
+  float* y;
+  int ldy;
+  int epi;
+  EpiArgs ep;
+  hipStream_t stream;
+};
+hipError_t launch_f32(const F32Args& p);
+
+struct FoldArgs {
+  const void* W;
+  int64_t ldw;
+  int w_dtype;  // 0 fp32, 1 bf16
+  const float* g;
+  const float* beta;
+  int64_t K, N;
+  int glu;
+  void* ws;
+  int ws_dtype;
+  float* colsum;
+  float* cstar;
+  hipStream_t stream;
+};
+hipError_t launch_fold(const FoldArgs& p);
+hipError_t launch_unpack(const void* ws, int64_t K, int64_t N, int glu, int ws_dtype, void* out,
+                         int64_t ldo, hipStream_t stream);
+
+// Unfused baseline normalisation: x = RMSNorm(a; g) or LayerNorm(a; g, beta), dtype of a.
+hipError_t launch_norm_rows(const void* a, int M, int K, int lda, int dtype, const float* g,
+                            const float* beta, float eps, void* x, int ldx, hipStream_t stream);
+
+}  // namespace fn

@@ -1,0 +1,209 @@
+"""Thin Python binding of ``libflashnorm.so`` (the C ABI in ``include/flashnorm.h``).
+
+Argument marshalling only: tensors become device pointers, leading dimensions
+and dtype codes; outputs the caller does not pass are allocated with torch; the
+work is enqueued on the current torch stream (or the given one).  Every step of
+the computation runs in the library's HIP kernels.  If the library is not built
+this module raises on first use -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libflashnorm.so")
+
+FN_F32, FN_BF16 = 0, 1
+FN_LAYOUT_LINEAR, FN_LAYOUT_GLU = 0, 1
+FN_PATH_AUTO, FN_PATH_PREFILL, FN_PATH_DECODE = 0, 1, 2
+FN_DECODE_MAX_M = 16
+
+STATUS = {0: "FN_OK", -1: "FN_ERR_NULL", -2: "FN_ERR_SHAPE", -3: "FN_ERR_DTYPE", -4: "FN_ERR_ALIGN",
+          -5: "FN_ERR_UNSUPPORTED", -6: "FN_ERR_VALUE", -7: "FN_ERR_HIP", -8: "FN_ERR_ALIAS",
+          -9: "FN_ERR_SIZE"}
+
+_lib = None
+
+
+class FlashNormError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {_load().flashnorm_status_string(status).decode()}")
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    sig = {
+        "fold_weights_size": ([I64, I64, I, I], ctypes.c_size_t),
+        "fold_weights": ([P, I64, I, P, P, I64, I64, I, P, I, P, P, P], I),
+        "unpack_weights": ([P, I64, I64, I, I, P, I64, P], I),
+        "flashnorm_linear": ([P, I64, I64, I64, I, P, I64, F, P, P, I64, I, P, P], I),
+        "flashnorm_linear_ex": ([P, I64, I64, I64, I, P, I64, F, P, P, I64, I, P, I, P], I),
+        "flashnorm_glu": ([P, I64, I64, I64, I, P, I64, F, P, I64, I, P], I),
+        "flashnorm_glu_ex": ([P, I64, I64, I64, I, P, I64, F, P, I64, I, I, P], I),
+        "flashnorm_layernorm_linear": ([P, I64, I64, I64, I, P, P, P, I64, F, P, I64, I, P], I),
+        "flashnorm_layernorm_linear_ex": ([P, I64, I64, I64, I, P, P, P, I64, F, P, I64, I, I, P], I),
+        "baseline_rmsnorm_linear": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P], I),
+        "baseline_rmsnorm_glu": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P], I),
+        "baseline_layernorm_linear": ([P, I64, I64, I64, I, P, P, P, I64, F, P, P, I64, I, P], I),
+        "flashnorm_status_string": ([I], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def lib():
+    """The raw ctypes handle (for tests of the C ABI itself)."""
+    return _load()
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise FlashNormError(status, where)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return FN_BF16
+    if t.dtype == torch.float32:
+        return FN_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _torch_dtype(code: int) -> torch.dtype:
+    return torch.bfloat16 if code == FN_BF16 else torch.float32
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _ld(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a row-major 2-D tensor (unit column stride)")
+    return t.stride(0)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _vec(t, n, name):
+    if t is None:
+        return None
+    if t.dtype != torch.float32 or t.numel() != n or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous fp32 vector of {n} elements")
+    return t
+
+
+def fold_weights_size(K: int, N: int, layout: int = FN_LAYOUT_LINEAR, ws_dtype: int = FN_BF16) -> int:
+    return _load().fold_weights_size(K, N, layout, ws_dtype)
+
+
+def fold_weights(W: torch.Tensor, g, beta=None, layout: int = FN_LAYOUT_LINEAR, ws_dtype=None,
+                 colsum: bool = False, c_star: bool = False, stream=None):
+    """Fold g into W (and beta into c*) and pack.  W is the logical [K, N] weight
+    ([K, 2F] = [Wg | Wu] for a GLU).  g = None packs W unchanged.  Returns
+    (W_star, colsum or None, c_star or None); W_star is an opaque uint8 device buffer."""
+    K, N = W.shape
+    ws_code = _dt(W) if ws_dtype is None else (ws_dtype if isinstance(ws_dtype, int) else _dt(torch.empty(0, dtype=ws_dtype)))
+    nbytes = fold_weights_size(K, N, layout, ws_code)
+    if nbytes == 0:
+        raise ValueError("invalid fold geometry")
+    Ws = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
+    cs = torch.empty(N, dtype=torch.float32, device=W.device) if colsum else None
+    cb = torch.empty(N, dtype=torch.float32, device=W.device) if c_star else None
+    _check(_load().fold_weights(_ptr(W), _ld(W), _dt(W), _ptr(_vec(g, K, "g")), _ptr(_vec(beta, K, "beta")),
+                                K, N, layout, _ptr(Ws), ws_code, _ptr(cs), _ptr(cb), _stream(stream)),
+           "fold_weights")
+    return Ws, cs, cb
+
+
+def unpack_weights(W_star: torch.Tensor, K: int, N: int, layout: int = FN_LAYOUT_LINEAR,
+                   ws_dtype: int = FN_BF16, stream=None) -> torch.Tensor:
+    out = torch.zeros(K, N, dtype=_torch_dtype(ws_dtype), device=W_star.device)
+    _check(_load().unpack_weights(_ptr(W_star), K, N, layout, ws_dtype, _ptr(out), N, _stream(stream)),
+           "unpack_weights")
+    return out
+
+
+def flashnorm_linear(a: torch.Tensor, W_star: torch.Tensor, N: int, eps: float, bias=None, out=None,
+                     inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    M, K = a.shape
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    _check(_load().flashnorm_linear_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star), N, eps,
+                                       _ptr(_vec(bias, N, "bias")), _ptr(y), _ld(y), _dt(y),
+                                       _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
+           "flashnorm_linear")
+    return y
+
+
+def flashnorm_glu(a: torch.Tensor, W_star_gu: torch.Tensor, F: int, eps: float, out=None,
+                  path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    M, K = a.shape
+    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    _check(_load().flashnorm_glu_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star_gu), F, eps, _ptr(o), _ld(o),
+                                    _dt(o), path, _stream(stream)), "flashnorm_glu")
+    return o
+
+
+def flashnorm_layernorm_linear(a: torch.Tensor, W_star: torch.Tensor, colsum: torch.Tensor, c_star, N: int,
+                               eps: float, out=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    M, K = a.shape
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    _check(_load().flashnorm_layernorm_linear_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star),
+                                                 _ptr(_vec(colsum, N, "colsum")), _ptr(_vec(c_star, N, "c_star")),
+                                                 N, eps, _ptr(y), _ld(y), _dt(y), path, _stream(stream)),
+           "flashnorm_layernorm_linear")
+    return y
+
+
+def _ws(a, x_ws):
+    return x_ws if x_ws is not None else torch.empty_like(a, memory_format=torch.contiguous_format)
+
+
+def baseline_rmsnorm_linear(a, g, W_packed, N, eps, x_ws=None, out=None, path=FN_PATH_AUTO, stream=None):
+    M, K = a.shape
+    x = _ws(a, x_ws)
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    _check(_load().baseline_rmsnorm_linear(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed),
+                                           N, eps, _ptr(x), _ptr(y), _ld(y), path, _stream(stream)),
+           "baseline_rmsnorm_linear")
+    return y
+
+
+def baseline_rmsnorm_glu(a, g, W_packed_gu, F, eps, x_ws=None, out=None, path=FN_PATH_AUTO, stream=None):
+    M, K = a.shape
+    x = _ws(a, x_ws)
+    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    _check(_load().baseline_rmsnorm_glu(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed_gu),
+                                        F, eps, _ptr(x), _ptr(o), _ld(o), path, _stream(stream)),
+           "baseline_rmsnorm_glu")
+    return o
+
+
+def baseline_layernorm_linear(a, g, beta, W_packed, N, eps, x_ws=None, out=None, path=FN_PATH_AUTO,
+                              stream=None):
+    M, K = a.shape
+    x = _ws(a, x_ws)
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    _check(_load().baseline_layernorm_linear(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")),
+                                             _ptr(_vec(beta, K, "beta")), _ptr(W_packed), N, eps, _ptr(x),
+                                             _ptr(y), _ld(y), path, _stream(stream)),
+           "baseline_layernorm_linear")
+    return y

@@ -1,0 +1,141 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point the
+header declares, sizes the packed weights as documented, and rejects invalid
+arguments with the documented status before launching anything (so these run
+without a GPU: no call here reaches a kernel launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import __graft_entry__ as graft
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashnorm.h")
+
+
+@pytest.fixture(scope="module")
+def fnlib():
+    graft.ensure_built()
+    from paper_2407_09577_amd import flashnorm
+    return flashnorm
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\**([a-z_0-9]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for required in ("fold_weights", "flashnorm_linear", "flashnorm_glu", "flashnorm_layernorm_linear"):
+        assert required in names
+    assert len(names) >= 13
+
+
+def test_library_exports_every_declared_symbol(fnlib):
+    lib = ctypes.CDLL(fnlib.LIB_PATH)
+    missing = [n for n in _declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(fnlib):
+    lib = fnlib.lib()
+    for code, name in fnlib.STATUS.items():
+        assert lib.flashnorm_status_string(code).decode().startswith(name)
+    assert lib.flashnorm_status_string(12345).decode() == "unknown fn_status"
+
+
+def test_fold_weights_size(fnlib):
+    f = fnlib.fold_weights_size
+    # bf16: rows padded to 64, columns to 16; GLU: 2 * round_up(F, 16) columns
+    assert f(576, 1536, 0, 1) == 576 * 1536 * 2
+    assert f(4096, 22016, 1, 1) == 4096 * 22016 * 2
+    assert f(576, 576, 0, 0) == 576 * 576 * 4
+    assert f(8, 3, 0, 1) == 64 * 16 * 2
+    assert f(72, 2 * 9, 1, 1) == 128 * 32 * 2
+    assert f(0, 16, 0, 1) == 0 and f(16, 0, 0, 1) == 0
+    assert f(16, 7, 1, 1) == 0          # GLU needs an even column count
+    assert f(16, 16, 2, 1) == 0          # unknown layout
+    assert f(16, 16, 0, 7) == 0          # unknown dtype
+
+
+# Fake but aligned, non-null device addresses: validation never dereferences them.
+A, W, Y, X = 0x100000, 0x200000, 0x300000, 0x400000
+
+
+def _lin(lib, a=A, M=4, K=64, lda=64, adt=1, ws=W, N=32, eps=1e-6, y=Y, ldy=32, ydt=1, path=0):
+    return lib.flashnorm_linear_ex(a, M, K, lda, adt, ws, N, eps, None, y, ldy, ydt, None, path, None)
+
+
+def test_linear_validation(fnlib):
+    lib = fnlib.lib()
+    assert _lin(lib, M=-1) == -2
+    assert _lin(lib, K=0) == -2
+    assert _lin(lib, N=0) == -2
+    assert _lin(lib, lda=32) == -2                 # lda < K
+    assert _lin(lib, K=60, lda=64) == -2           # bf16 K % 8
+    assert _lin(lib, ldy=16) == -2                 # ldy < N
+    assert _lin(lib, a=0) == -1
+    assert _lin(lib, ws=0) == -1
+    assert _lin(lib, y=0) == -1
+    assert _lin(lib, a=A + 8) == -4                # 16-byte alignment
+    assert _lin(lib, lda=68, K=64) == -4           # row alignment (bf16: ld % 8)
+    assert _lin(lib, adt=5) == -3
+    assert _lin(lib, ydt=0) == -3                  # output dtype must match
+    assert _lin(lib, eps=-1.0) == -6
+    assert _lin(lib, eps=float("nan")) == -6
+    assert _lin(lib, eps=float("inf")) == -6
+    assert _lin(lib, path=7) == -6
+    assert _lin(lib, M=17, path=2) == -5           # decode path takes M <= 16
+    assert _lin(lib, adt=0, ydt=0, path=2) == -5   # decode path is bf16 only
+    assert _lin(lib, y=A + 64) == -8               # output overlaps the activations
+    assert _lin(lib, lda=1 << 22, K=64) == -9
+    # M == 0 is a no-op that never touches the device, even with null tensors
+    assert _lin(lib, M=0, a=0, y=0) == 0
+
+
+def test_glu_and_layernorm_validation(fnlib):
+    lib = fnlib.lib()
+    glu = lambda **kw: lib.flashnorm_glu_ex(kw.get("a", A), kw.get("M", 4), 64, 64, 1, kw.get("ws", W),
+                                            kw.get("F", 16), 1e-6, Y, kw.get("ldo", 16), 1, 0, None)
+    assert glu(F=0) == -2
+    assert glu(ws=0) == -1
+    assert glu(ldo=8) == -2
+    ln = lambda **kw: lib.flashnorm_layernorm_linear_ex(A, 4, 64, 64, 1, W, kw.get("colsum", X), None, 32,
+                                                        kw.get("eps", 1e-5), Y, 32, 1, 0, None)
+    assert ln(colsum=0) == -1
+    assert ln(eps=-1e-3) == -6
+
+
+def test_fold_validation(fnlib):
+    lib = fnlib.lib()
+    f = lambda **kw: lib.fold_weights(kw.get("W", A), kw.get("ldw", 32), kw.get("wdt", 1), kw.get("g", X),
+                                      kw.get("beta", None), kw.get("K", 64), kw.get("N", 32),
+                                      kw.get("layout", 0), kw.get("ws", W), kw.get("wsdt", 1),
+                                      kw.get("colsum", None), kw.get("cstar", None), None)
+    assert f(W=0) == -1
+    assert f(ws=0) == -1
+    assert f(ldw=16) == -2
+    assert f(N=31, layout=1, ldw=32) == -2
+    assert f(layout=3) == -6
+    assert f(wdt=4) == -3
+    assert f(cstar=X) == -1                        # c* needs beta
+    assert f(layout=1, colsum=X) == -5             # LayerNorm extras: linear layout only
+    assert f(ws=W + 4) == -4
+    assert f(ws=A + 16) == -8                      # packed output overlaps W
+    u = lambda **kw: lib.unpack_weights(kw.get("ws", W), 64, 32, 0, 1, kw.get("out", Y), kw.get("ldo", 32), None)
+    assert u(ws=0) == -1
+    assert u(ldo=8) == -2
+
+
+def test_baseline_validation(fnlib):
+    lib = fnlib.lib()
+    b = lambda **kw: lib.baseline_rmsnorm_linear(A, 4, 64, 64, 1, kw.get("g", X), W, 32, 1e-6,
+                                                 kw.get("xws", 0x500000), Y, 32, 0, None)
+    assert b(g=0) == -1
+    assert b(xws=0) == -1
+    assert b(xws=A) == -8                          # workspace overlaps the activations
+    assert lib.baseline_layernorm_linear(A, 4, 64, 64, 1, X, None, W, 32, 1e-5, 0x500000, Y, 32, 0, None) == -1

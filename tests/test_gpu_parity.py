@@ -1,0 +1,283 @@
+"""GPU parity: the HIP path, called through the C ABI, against the fp64 oracle.
+
+Metric (per output row m): e_m = max_n |y - r| / max_n |r|, gated on max_m e_m:
+<= 2e-2 for bf16 inputs and <= 1e-5 for fp32 (the stated tolerances), plus no
+NaN/Inf.  Row-normwise, because unit-variance outputs put many entries near zero
+where an element-wise relative error is meaningless, and so that the x20 outlier
+rows weigh as much as the others.  The bf16 error budget is dominated by the one
+rounding of W* = g W to bf16 and of the output (each ~2^-9 relative), expected
+around 3e-3 after averaging over K.
+
+Full-size workloads run in the launch configuration the benchmark times; where
+the fp64 oracle cannot compute every row in seconds, a fixed sample of rows
+(first, last, tile boundaries and random rows) is compared one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import __graft_entry__ as graft
+import oracle
+from paper_2407_09577_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+TOL = {torch.bfloat16: 2e-2, torch.float32: 1e-5}
+
+
+@pytest.fixture(scope="module")
+def fn():
+    graft.ensure_built()
+    from paper_2407_09577_amd import flashnorm
+    flashnorm.lib()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return flashnorm
+
+
+DEV = "cuda:0"
+
+
+def row_err(got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    assert np.isfinite(got).all(), "NaN/Inf in GPU output"
+    den = np.abs(ref).max(axis=1)
+    den = np.where(den == 0, 1.0, den)
+    return float(np.max(np.abs(got - ref).max(axis=1) / den))
+
+
+def to_np(t):
+    return t.detach().float().cpu().double().numpy()
+
+
+def sample_rows(M, n=48, seed=0):
+    rng = np.random.default_rng(seed)
+    fixed = [0, 1, 15, 16, 127, 128, 255, 256, M // 2, M - 2, M - 1]
+    rows = sorted(set([r for r in fixed if 0 <= r < M] + list(rng.choice(M, size=min(n, M), replace=False))))
+    return np.array(rows, dtype=np.int64)
+
+
+def padded_out(M, N, dtype, align=8):
+    ld = (N + align - 1) // align * align
+    return torch.empty(M, ld, dtype=dtype, device=DEV)[:, :N]
+
+
+def check_linear(fn, w, rows=None, path=0, bias=None):
+    a, W = w.a.to(DEV), w.W.to(DEV)
+    Ws, _, _ = fn.fold_weights(W, w.g.to(DEV))
+    y = padded_out(w.M, w.N, w.dtype)
+    b = bias.to(DEV) if bias is not None else None
+    fn.flashnorm_linear(a, Ws, w.N, w.eps, bias=b, out=y, path=path)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps, bias=bias, rows=rows)
+    got = to_np(y) if rows is None else to_np(y)[rows]
+    return row_err(got, ref)
+
+
+# ------------------------------------------------------------------ the five workloads
+def test_tiny_fp32_deferred_vs_standard(fn):
+    w = workloads.tiny_fp32()
+    assert check_linear(fn, w) <= TOL[torch.float32]
+
+
+def test_smollm2_prefill_full(fn):
+    w = workloads.smollm2_prefill()
+    err = check_linear(fn, w)
+    assert err <= TOL[torch.bfloat16], err
+
+
+def test_smollm2_outlier_rows(fn):
+    w = workloads.smollm2_prefill()
+    rows = w.outlier_rows.numpy()
+    assert check_linear(fn, w, rows=rows) <= TOL[torch.bfloat16]
+
+
+def test_llama7b_qkv_prefill_sampled(fn):
+    w = workloads.llama7b_qkv_prefill()
+    err = check_linear(fn, w, rows=sample_rows(w.M, n=24))
+    assert err <= TOL[torch.bfloat16], err
+
+
+@pytest.mark.parametrize("M", [1, 4, 16])
+def test_llama7b_swiglu_decode(fn, M):
+    w = workloads.llama7b_swiglu_decode(M=M)
+    a, W = w.a.to(DEV), w.W.to(DEV)
+    Ws, _, _ = fn.fold_weights(W, w.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    F = w.out_features
+    out = fn.flashnorm_glu(a, Ws, F, w.eps)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)
+    err = row_err(to_np(out), ref)
+    assert err <= TOL[torch.bfloat16], err
+
+
+def test_layernorm_linear_sampled(fn):
+    w = workloads.layernorm_linear()
+    a, W = w.a.to(DEV), w.W.to(DEV)
+    Ws, cs, cb = fn.fold_weights(W, w.g.to(DEV), beta=w.beta.to(DEV), colsum=True, c_star=True)
+    y = fn.flashnorm_layernorm_linear(a, Ws, cs, cb, w.N, w.eps)
+    torch.cuda.synchronize()
+    rows = sample_rows(w.M, n=24)
+    ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps, rows=rows)
+    err = row_err(to_np(y)[rows], ref)
+    assert err <= TOL[torch.bfloat16], err
+
+
+# ------------------------------------------------------------------ ragged and edge shapes
+@pytest.mark.parametrize("M,K,N", [(300, 200, 333), (17, 576, 576), (3, 72, 40), (513, 8, 20),
+                                   (1, 64, 16), (257, 136, 1000)])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_linear_ragged(fn, M, K, N, dtype):
+    w = workloads.make("linear", M, K, N, dtype=dtype, eps=1e-5, seed=M + K + N, outlier_frac=0.02)
+    bias = torch.randn(N, generator=torch.Generator().manual_seed(3))
+    assert check_linear(fn, w, bias=bias) <= TOL[dtype]
+    assert check_linear(fn, w) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("M", [1, 3, 16])
+@pytest.mark.parametrize("path", [1, 2])
+def test_linear_both_paths_few_rows(fn, M, path):
+    w = workloads.make("linear", M, 520, 208, eps=1e-6, seed=7 + M)
+    assert check_linear(fn, w, path=path) <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("M,K,F", [(70, 136, 45), (5, 264, 100), (16, 4096, 48), (200, 576, 96)])
+@pytest.mark.parametrize("path", [0, 1, 2])
+def test_glu_ragged(fn, M, K, F, path):
+    if path == 2 and M > 16:
+        pytest.skip("the decode path takes M <= 16")
+    w = workloads.make("glu", M, K, F, eps=1e-6, seed=M * K + F)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    out = padded_out(M, F, w.dtype)
+    fn.flashnorm_glu(w.a.to(DEV), Ws, F, w.eps, out=out, path=path)
+    torch.cuda.synchronize()
+    assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
+
+
+def test_glu_fp32(fn):
+    w = workloads.make("glu", 40, 96, 36, dtype=torch.float32, eps=1e-6, seed=5)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    out = padded_out(40, 36, torch.float32, align=4)
+    fn.flashnorm_glu(w.a.to(DEV), Ws, 36, w.eps, out=out)
+    torch.cuda.synchronize()
+    assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[torch.float32]
+
+
+@pytest.mark.parametrize("M,K,N,dtype,path", [(130, 200, 72, torch.bfloat16, 0), (9, 128, 40, torch.bfloat16, 2),
+                                              (9, 128, 40, torch.bfloat16, 1), (33, 96, 50, torch.float32, 0)])
+def test_layernorm_ragged(fn, M, K, N, dtype, path):
+    w = workloads.make("layernorm", M, K, N, dtype=dtype, eps=1e-5, seed=M + N, a_mean=0.5)
+    Ws, cs, cb = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), beta=w.beta.to(DEV), colsum=True, c_star=True)
+    y = padded_out(M, N, dtype, align=8 if dtype == torch.bfloat16 else 4)
+    fn.flashnorm_layernorm_linear(w.a.to(DEV), Ws, cs, cb, N, w.eps, out=y, path=path)
+    torch.cuda.synchronize()
+    ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps)
+    assert row_err(to_np(y), ref) <= TOL[dtype]
+
+
+def test_zero_rows_give_exact_zero(fn):
+    w = workloads.make("linear", 40, 128, 48, eps=1e-6, seed=11)
+    w.a[[0, 17, 39]] = 0
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    for path in (1, 0):
+        a = w.a.to(DEV) if path == 1 else w.a[:16].to(DEV)
+        y = fn.flashnorm_linear(a, Ws, 48, w.eps, path=path)
+        torch.cuda.synchronize()
+        assert torch.all(y[0] == 0)
+        if path == 1:
+            assert torch.all(y[17] == 0) and torch.all(y[39] == 0)
+
+
+def test_negative_g(fn):
+    w = workloads.make("linear", 64, 256, 96, eps=1e-6, seed=12)
+    w.g = w.g * torch.where(torch.arange(256) % 3 == 0, -1.0, 1.0)
+    assert check_linear(fn, w) <= TOL[torch.bfloat16]
+
+
+def test_layernorm_constant_rows_give_cstar(fn):
+    w = workloads.make("layernorm", 24, 128, 64, eps=1e-5, seed=13)
+    w.a[:] = 0.75
+    Ws, cs, cb = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), beta=w.beta.to(DEV), colsum=True, c_star=True)
+    y = fn.flashnorm_layernorm_linear(w.a.to(DEV), Ws, cs, cb, 64, w.eps)
+    torch.cuda.synchronize()
+    ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps)
+    assert row_err(to_np(y), ref) <= TOL[torch.bfloat16]
+
+
+def test_inv_rms_side_output(fn):
+    w = workloads.make("linear", 200, 256, 64, eps=1e-5, seed=14, outlier_frac=0.05)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    inv = torch.empty(200, dtype=torch.float32, device=DEV)
+    fn.flashnorm_linear(w.a.to(DEV), Ws, 64, w.eps, inv_rms=inv)
+    torch.cuda.synchronize()
+    a = w.a.double().numpy() if w.a.dtype == torch.float32 else w.a.float().double().numpy()
+    want = np.array([1.0 / oracle.rms(r, float(np.float32(w.eps))) for r in a])
+    np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=1e-5)
+
+
+# ------------------------------------------------------------------ fold, determinism, baselines
+@pytest.mark.parametrize("K,N,layout,dtype", [(200, 72, 0, torch.bfloat16), (136, 2 * 45, 1, torch.bfloat16),
+                                              (96, 40, 0, torch.float32), (64, 2 * 20, 1, torch.float32)])
+def test_fold_bitwise(fn, K, N, layout, dtype):
+    kind = "glu" if layout else "layernorm"
+    w = workloads.make(kind, 2, K, N // 2 if layout else N, dtype=dtype, seed=K + N)
+    want_extras = layout == 0
+    Ws, cs, cb = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), beta=w.beta.to(DEV) if want_extras else None,
+                                 layout=layout, colsum=want_extras, c_star=want_extras)
+    back = fn.unpack_weights(Ws, K, N, layout, fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32)
+    torch.cuda.synchronize()
+    storage = oracle.STORAGE_BF16 if dtype == torch.bfloat16 else oracle.STORAGE_F32
+    exp_ws, exp_cs, exp_cb = oracle.fold(w.W, w.g, w.beta if want_extras else None, storage=storage)
+    np.testing.assert_array_equal(back.double().cpu().numpy(), exp_ws)
+    if want_extras:
+        scale = np.abs(exp_ws).sum(axis=0)
+        assert np.all(np.abs(cs.cpu().double().numpy() - exp_cs) <= 1e-6 * scale + 1e-30)
+        bscale = np.abs(w.beta.double().numpy()[:, None] * w.W.double().numpy()).sum(axis=0)
+        assert np.all(np.abs(cb.cpu().double().numpy() - exp_cb) <= 1e-6 * bscale + 1e-30)
+
+
+def test_determinism_bitwise(fn):
+    w = workloads.make("linear", 1000, 576, 1536, eps=1e-5, seed=21)
+    a = w.a.to(DEV)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    y1 = fn.flashnorm_linear(a, Ws, w.N, w.eps)
+    y2 = fn.flashnorm_linear(a, Ws, w.N, w.eps)
+    d = workloads.make("glu", 16, 1024, 256, eps=1e-6, seed=22)
+    Wg, _, _ = fn.fold_weights(d.W.to(DEV), d.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    o1 = fn.flashnorm_glu(d.a.to(DEV), Wg, 256, d.eps)
+    o2 = fn.flashnorm_glu(d.a.to(DEV), Wg, 256, d.eps)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+
+
+@pytest.mark.parametrize("M", [8, 600])
+def test_baselines_match_oracle(fn, M):
+    lin = workloads.make("linear", M, 320, 200, eps=1e-5, seed=31)
+    Wp, _, _ = fn.fold_weights(lin.W.to(DEV), None)
+    y = fn.baseline_rmsnorm_linear(lin.a.to(DEV), lin.g.to(DEV), Wp, 200, lin.eps, out=padded_out(M, 200, lin.dtype))
+    glu = workloads.make("glu", M, 320, 72, eps=1e-6, seed=32)
+    Wgp, _, _ = fn.fold_weights(glu.W.to(DEV), None, layout=fn.FN_LAYOUT_GLU)
+    o = fn.baseline_rmsnorm_glu(glu.a.to(DEV), glu.g.to(DEV), Wgp, 72, glu.eps)
+    ln = workloads.make("layernorm", M, 320, 64, eps=1e-5, seed=33, a_mean=0.5)
+    Wlp, _, _ = fn.fold_weights(ln.W.to(DEV), None)
+    z = fn.baseline_layernorm_linear(ln.a.to(DEV), ln.g.to(DEV), ln.beta.to(DEV), Wlp, 64, ln.eps)
+    torch.cuda.synchronize()
+    assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
+    assert row_err(to_np(o), oracle.rmsnorm_swiglu(glu.a, glu.g, glu.W, glu.eps)) <= TOL[torch.bfloat16]
+    assert row_err(to_np(z), oracle.layernorm_linear(ln.a, ln.g, ln.beta, ln.W, ln.eps)) <= TOL[torch.bfloat16]
+
+
+def test_non_contiguous_activation_rows(fn):
+    # lda > K: the activations are a column slice of a wider buffer
+    w = workloads.make("linear", 150, 192, 80, eps=1e-5, seed=41)
+    big = torch.randn(150, 256).to(torch.bfloat16)
+    big[:, :192] = w.a
+    a = big.to(DEV)[:, :192]
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    for path in (1,):
+        y = fn.flashnorm_linear(a, Ws, 80, w.eps, path=path)
+        torch.cuda.synchronize()
+        assert row_err(to_np(y), oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
+    y = fn.flashnorm_linear(a[:12], Ws, 80, w.eps, path=2)
+    torch.cuda.synchronize()
+    assert row_err(to_np(y), oracle.rmsnorm_linear(w.a[:12], w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
