@@ -1,0 +1,229 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused FlashNorm norm-then-project path on one MI355X.
+
+A step is one pass of the hot path over one batch of synthetic input: one call
+of the fused op (kernel selection + one kernel launch) on inputs and a folded
+weight already resident in HBM.  The fold (W* = diag(g) W, done once at load
+time) is outside the timed region.  Several independent input/weight/output
+sets are rotated so the working set exceeds the 256 MB Infinity Cache and every
+step streams its operands from HBM.  The same-library unfused baseline
+(normalisation kernel -> the same matrix-multiply kernel) is timed the same way.
+
+Prints ONE JSON line (rank 0) with the throughput, the roofline of the fused
+kernel (algorithmic FLOPs or bytes per launch / measured launch time) and the
+fp64 CPU oracle timed on a bounded sample of the same workload.
+
+  python bench.py [--steps 100] [--warmup 20] [--workload smollm2_prefill]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fused RMSNorm+proj TFLOP/s (prefill), HBM GB/s (decode), % of MI355X peak"
+# MI355X published peaks: dense bf16 matrix cores 2.5 PFLOP/s (256 CU x 2.4 GHz x
+# 4096 FLOP/clk), fp32 vector 157.3 TFLOP/s, HBM3E 8 TB/s.
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+CACHE_BYTES = 256 * 2 ** 20  # Infinity Cache; the rotation keeps >= 2x this resident
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="smollm2_prefill",
+                   choices=["tiny_fp32", "smollm2_prefill", "llama7b_qkv_prefill", "llama7b_swiglu_decode",
+                            "layernorm_linear"])
+    p.add_argument("--decode-m", type=int, default=16, choices=[1, 4, 16])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-unfused", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle timing sample")
+    return p.parse_args()
+
+
+class Setup:
+    """GPU-resident rotating operand sets and the closures that run one step."""
+
+    def __init__(self, name, decode_m):
+        import torch
+        from paper_2407_09577_amd import flashnorm as fn
+        from paper_2407_09577_amd import workloads
+
+        self.fn = fn
+        self.torch = torch
+        gen = workloads.WORKLOADS[name]
+        self.w = w = gen(M=decode_m) if name == "llama7b_swiglu_decode" else gen()
+        dev = torch.device("cuda:0")
+        self.kind = w.kind
+        M, K = w.M, w.K
+        ncols = w.out_features
+        es = w.a.element_size()
+        layout = fn.FN_LAYOUT_GLU if w.kind == "glu" else fn.FN_LAYOUT_LINEAR
+        a0 = w.a.to(dev)
+        W0 = w.W.to(dev)
+        g0 = w.g.to(dev)
+        beta0 = w.beta.to(dev) if w.beta is not None else None
+        ln = w.kind == "layernorm"
+        Ws0, cs0, cb0 = fn.fold_weights(W0, g0, beta=beta0, layout=layout, colsum=ln, c_star=ln)
+        Wp0, _, _ = fn.fold_weights(W0, None, layout=layout)  # unfolded, for the baseline
+        del W0
+        self.ws_bytes = Ws0.numel()
+        set_bytes = a0.numel() * es + self.ws_bytes + M * ncols * es
+        self.nsets = max(2, -(-2 * CACHE_BYTES // set_bytes))
+        self.sets = []
+        for i in range(self.nsets):
+            a = a0 if i == 0 else a0.clone()
+            Ws = Ws0 if i == 0 else Ws0.clone()
+            Wp = Wp0 if i == 0 else Wp0.clone()
+            y = torch.empty(M, ncols, dtype=w.a.dtype, device=dev)
+            x = torch.empty_like(a)
+            self.sets.append((a, Ws, Wp, y, x))
+        self.g, self.beta, self.cs, self.cb = g0, beta0, cs0, cb0
+        self.M, self.K, self.ncols, self.es = M, K, ncols, es
+        self.N = w.N
+
+    def run(self, i):
+        fn, w = self.fn, self.w
+        a, Ws, _, y, _ = self.sets[i % self.nsets]
+        if self.kind == "glu":
+            fn.flashnorm_glu(a, Ws, self.ncols, w.eps, out=y)
+        elif self.kind == "layernorm":
+            fn.flashnorm_layernorm_linear(a, Ws, self.cs, self.cb, self.ncols, w.eps, out=y)
+        else:
+            fn.flashnorm_linear(a, Ws, self.ncols, w.eps, out=y)
+
+    def run_unfused(self, i):
+        fn, w = self.fn, self.w
+        a, _, Wp, y, x = self.sets[i % self.nsets]
+        if self.kind == "glu":
+            fn.baseline_rmsnorm_glu(a, self.g, Wp, self.ncols, w.eps, x_ws=x, out=y)
+        elif self.kind == "layernorm":
+            fn.baseline_layernorm_linear(a, self.g, self.beta, Wp, self.ncols, w.eps, x_ws=x, out=y)
+        else:
+            fn.baseline_rmsnorm_linear(a, self.g, Wp, self.ncols, w.eps, x_ws=x, out=y)
+
+    def flops(self):
+        return 2.0 * self.M * self.K * self.N
+
+    def alg_bytes(self):
+        """Read a once, read W* once, write the output once."""
+        return self.M * self.K * self.es + self.ws_bytes + self.M * self.ncols * self.es
+
+    def time_steps(self, fn_step, steps, warmup):
+        torch = self.torch
+        for i in range(warmup):
+            fn_step(i)
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for i in range(steps):
+            fn_step(warmup + i)
+        end.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / steps  # ms per step
+
+
+def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total):
+    """Time the fp64 oracle (as it stands) on a bounded sample of rows of the same workload."""
+    import numpy as np
+    import oracle
+
+    a = w.a.double().numpy()
+    g, W = w.g.double().numpy(), w.W.double().numpy()
+    beta = w.beta.double().numpy() if w.beta is not None else None
+
+    def call(rows):
+        if w.kind == "glu":
+            oracle.rmsnorm_swiglu(a, g, W, w.eps, rows=rows)
+        elif w.kind == "layernorm":
+            oracle.layernorm_linear(a, g, beta, W, w.eps, rows=rows)
+        else:
+            oracle.rmsnorm_linear(a, g, W, w.eps, rows=rows)
+
+    probe = np.arange(min(w.M, max(4, oracle.num_threads())))
+    call(probe)  # warm (page-in, thread pool)
+    t0 = time.perf_counter()
+    call(probe)
+    per_row = (time.perf_counter() - t0) / probe.size
+    n = int(max(probe.size, min(w.M, target_s / max(per_row, 1e-9))))
+    rows = np.arange(n)
+    t0 = time.perf_counter()
+    call(rows)
+    t = time.perf_counter() - t0
+    if unit == "TFLOP/s":
+        value = flops_per_row * n / t / 1e12
+    else:  # whole-op bytes over the time the oracle would take for all M rows
+        value = bytes_total / (t * w.M / n) / 1e9
+    return {"value": value, "unit": unit, "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"fp64 oracle (standard form) on rows 0..{n - 1} of {w.M} of the same workload, "
+                      f"{t:.2f} s wall"}
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
+              "the FlashNorm path here is a single-GPU kernel library", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import __graft_entry__ as graft
+
+    graft.ensure_built()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    s = Setup(args.workload, args.decode_m)
+    w = s.w
+    decode = args.workload == "llama7b_swiglu_decode"
+    fp32 = w.a.dtype == torch.float32
+
+    torch.cuda.synchronize()
+    ms = s.time_steps(s.run, args.steps, args.warmup)
+    ms_unf = None if args.no_unfused else s.time_steps(s.run_unfused, args.steps, args.warmup)
+
+    t = ms * 1e-3
+    if decode:
+        unit = "GB/s"
+        value = s.alg_bytes() / t / 1e9
+        roof = {"bound": "hbm", "achieved": value, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": value / PEAK_HBM_GBS, "traffic": None}
+    else:
+        unit = "TFLOP/s"
+        value = s.flops() / t / 1e12
+        peak = PEAK_F32_TFLOPS if fp32 else PEAK_BF16_TFLOPS
+        roof = {"bound": "alu" if fp32 else "mfma", "achieved": value, "peak": peak, "unit": "TFLOP/s",
+                "frac": value / peak, "traffic": None}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        per_row = 2.0 * w.K * w.N
+        cpu = cpu_baseline(w, unit, args.cpu_seconds, per_row, s.alg_bytes())
+
+    config = {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "out_features": s.ncols, "eps": w.eps,
+              "op": {"glu": "flashnorm_glu", "layernorm": "flashnorm_layernorm_linear"}.get(w.kind, "flashnorm_linear"),
+              "step": "one fused call on HBM-resident inputs; weight fold done once before timing",
+              "rotating_sets": s.nsets, "alg_flops_per_step": s.flops(), "alg_bytes_per_step": s.alg_bytes(),
+              "parallelism": "single GPU"}
+    if ms_unf is not None:
+        config["unfused_ms_per_step"] = ms_unf
+        config["fused_vs_unfused_speedup"] = (ms_unf - ms) / ms_unf
+    out = {"metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32" if fp32 else "bf16", "data": "synthetic",
+           "config": config, "roofline": roof, "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -18,8 +18,9 @@
  *    never allocates device memory, never synchronises, and keeps no mutable
  *    global state: calls on different streams may run concurrently.
  *  - Tensors are row-major with an explicit leading dimension (elements between
- *    consecutive rows).  Every tensor pointer must be 16-byte aligned and every
- *    leading dimension a multiple of 8 elements for bf16, 4 for fp32.
+ *    consecutive rows).  Every tensor pointer (including the fp32 per-column
+ *    vectors bias, colsum and c_star) must be 16-byte aligned and every leading
+ *    dimension a multiple of 8 elements for bf16, 4 for fp32.
  *  - Arguments are validated on the host before anything is launched; on any
  *    error nothing is written and a negative fn_status is returned.  M == 0 is
  *    a valid no-op.  Kernel launch failures return FN_ERR_HIP; faults during
@@ -66,6 +67,13 @@ typedef enum { FN_LAYOUT_LINEAR = 0, FN_LAYOUT_GLU = 1 } fn_layout;
  * DECODE forces the bandwidth-bound few-row kernel (bf16, M <= 16, else
  * FN_ERR_UNSUPPORTED).  fp32 always runs the fp32 kernel. */
 typedef enum { FN_PATH_AUTO = 0, FN_PATH_PREFILL = 1, FN_PATH_DECODE = 2 } fn_path;
+
+/* Tuning override: bits 8..15 of a path argument may name one of the library's
+ * kernel configurations for the selected path (prefill tile shapes, or decode
+ * work splits with FN_PATH_DECODE; 0 = automatic choice); values it does not
+ * know return FN_ERR_VALUE.  Results are identical for every configuration up to
+ * floating-point summation order. */
+#define FN_PATH_TILE_SHIFT 8
 
 /* Largest M the DECODE path accepts. */
 #define FN_DECODE_MAX_M 16

@@ -49,6 +49,8 @@ def _load():
     P = ctypes.c_void_p
     I = ctypes.c_int64
     D = ctypes.c_double
+    lib.fn_oracle_num_threads.argtypes = []
+    lib.fn_oracle_num_threads.restype = ctypes.c_int
     lib.fn_oracle_rms.argtypes = [P, I, D]
     lib.fn_oracle_rms.restype = D
     for name in ("fn_oracle_rmsnorm_linear", "fn_oracle_weightless", "fn_oracle_deferred"):
@@ -95,6 +97,11 @@ def _rows(rows, M):
 def _eps(eps) -> float:
     # the kernels receive eps as an fp32 scalar; the oracle uses that exact value
     return float(np.float32(eps))
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's row loops use."""
+    return int(_load().fn_oracle_num_threads())
 
 
 def rms(a, eps: float = 0.0) -> float:

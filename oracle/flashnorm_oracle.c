@@ -23,11 +23,15 @@
  * "parity unpinned".
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
 #define ORACLE_EXPORT __attribute__((visibility("default")))
+
+/* Threads the OpenMP loops below use (reported with CPU timings). */
+ORACLE_EXPORT int fn_oracle_num_threads(void) { return omp_get_max_threads(); }
 
 static int64_t row_of(const int64_t* rows, int64_t r) { return rows ? rows[r] : r; }
 

@@ -61,7 +61,10 @@ struct OpDesc {
 int validate_op(const OpDesc& d, int y_dtype) {
   if (!dtype_ok(d.dtype) || !dtype_ok(y_dtype)) return FN_ERR_DTYPE;
   if (y_dtype != d.dtype) return FN_ERR_DTYPE;
-  if (d.path < FN_PATH_AUTO || d.path > FN_PATH_DECODE) return FN_ERR_VALUE;
+  const int base_path = d.path & 0xff, tile = d.path >> FN_PATH_TILE_SHIFT;
+  if (base_path < FN_PATH_AUTO || base_path > FN_PATH_DECODE) return FN_ERR_VALUE;
+  if (tile < 0 || tile >= (base_path == FN_PATH_DECODE ? fn::kDecodeCfgCount : (int)fn::TILE_COUNT))
+    return FN_ERR_VALUE;
   if (d.K > kMaxLd) return FN_ERR_SIZE;
   if (d.K % (d.dtype == FN_BF16 ? 8 : 4)) return FN_ERR_SHAPE;
   int s = check_matrix(d.a, d.M, d.K, d.lda, d.dtype, true);
@@ -80,7 +83,7 @@ int validate_op(const OpDesc& d, int y_dtype) {
     if (overlaps(d.y, ybytes, d.a, extent_bytes(d.M, d.K, d.lda, d.dtype))) return FN_ERR_ALIAS;
     if (overlaps(d.y, ybytes, d.ws, wbytes)) return FN_ERR_ALIAS;
   }
-  if (d.path == FN_PATH_DECODE && (d.dtype != FN_BF16 || d.M > FN_DECODE_MAX_M)) return FN_ERR_UNSUPPORTED;
+  if (base_path == FN_PATH_DECODE && (d.dtype != FN_BF16 || d.M > FN_DECODE_MAX_M)) return FN_ERR_UNSUPPORTED;
   return FN_OK;
 }
 
@@ -93,14 +96,17 @@ int run_op(const OpDesc& d) {
                   (int)d.ncols, (float*)d.y, (int)d.ldy, d.epi, d.ep, d.stream};
     return status_of(fn::launch_f32(p));
   }
-  const bool decode = d.path == FN_PATH_DECODE || (d.path == FN_PATH_AUTO && d.M <= FN_DECODE_MAX_M);
+  const int base_path = d.path & 0xff;
+  const bool decode = base_path == FN_PATH_DECODE || (base_path == FN_PATH_AUTO && d.M <= FN_DECODE_MAX_M);
   if (decode) {
     fn::DecodeArgs p{(const __bf16*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const __bf16*)d.ws, NP, KP,
-                     (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, d.ep, d.stream};
+                     (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, d.path >> FN_PATH_TILE_SHIFT, d.ep,
+                     d.stream};
     return status_of(fn::launch_decode_bf16(p));
   }
   fn::PrefillArgs p{(const __bf16*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const __bf16*)d.ws, NP, KP,
-                    (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, fn::TILE_AUTO, d.ep, d.stream};
+                    (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, d.path >> FN_PATH_TILE_SHIFT, d.ep,
+                    d.stream};
   return status_of(fn::launch_prefill_bf16(p));
 }
 
@@ -162,6 +168,7 @@ int flashnorm_linear_ex(const void* a, int64_t M, int64_t K, int64_t lda, int a_
   d.ep.inv_rms = inv_rms;
   int s = validate_op(d, y_dtype);
   if (s) return s;
+  if (!aligned16(bias)) return FN_ERR_ALIGN;
   return run_op(d);
 }
 
@@ -196,6 +203,7 @@ int flashnorm_layernorm_linear_ex(const void* a, int64_t M, int64_t K, int64_t l
   int s = validate_op(d, y_dtype);
   if (s) return s;
   if (!colsum) return FN_ERR_NULL;
+  if (!aligned16(colsum) || !aligned16(c_star)) return FN_ERR_ALIGN;
   return run_op(d);
 }
 
@@ -217,7 +225,6 @@ static int baseline_common(const void* a, int64_t M, int64_t K, int64_t lda, int
   s = check_matrix(a, M, K, lda, a_dtype, true);
   if (s) return s;
   if (!g) return FN_ERR_NULL;
-  if (K > 16384) return FN_ERR_UNSUPPORTED;  // one row per workgroup held in registers
   if (M == 0) return FN_OK;
   const int64_t xb = extent_bytes(M, K, K, a_dtype);
   if (overlaps(x_ws, xb, a, extent_bytes(M, K, lda, a_dtype)) ||

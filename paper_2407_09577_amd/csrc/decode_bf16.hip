@@ -13,6 +13,8 @@
 // partial products and sums are combined in LDS in a fixed order
 // (deterministic), and one wave per output block applies the deferred scale and
 // the epilogue.
+#include <type_traits>
+
 #include "fn_device.h"
 #include "fn_epilogue.h"
 #include "fn_launch.h"
@@ -105,24 +107,37 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     if (ep.inv_rms && blockIdx.x == 0 && wave == 0 && lane < 16) ep.inv_rms[m] = st.s;
   }
   const int n_lane = (lane >> 4) * 4;
-  for (int o = wave; o < NOUT; o += KSPLIT) {
-    if constexpr (epi_is_glu(EPI)) {
-      f32x4 g = red[0][2 * o][lane], u = red[0][2 * o + 1][lane];
+  auto epilogue = [&](auto vec_tag) {
+    constexpr bool VEC = decltype(vec_tag)::value;
+    for (int o = wave; o < NOUT; o += KSPLIT) {
+      if constexpr (epi_is_glu(EPI)) {
+        f32x4 g = red[0][2 * o][lane], u = red[0][2 * o + 1][lane];
 #pragma unroll
-      for (int w = 1; w < KSPLIT; ++w) {
-        g += red[w][2 * o][lane];
-        u += red[w][2 * o + 1][lane];
+        for (int w = 1; w < KSPLIT; ++w) {
+          g += red[w][2 * o][lane];
+          u += red[w][2 * o + 1][lane];
+        }
+        const int fb = (cb0 / 2 + o) * 16;
+        if (fb + 16 <= ncols)
+          store4_bf16_full<EPI, VEC>(y, ldy, m, fb + n_lane, g, u, st, ep);
+        else
+          store4_bf16_edge<EPI, VEC>(y, ldy, M, ncols, m, fb + n_lane, g, u, st, ep);
+      } else {
+        f32x4 v = red[0][o][lane];
+#pragma unroll
+        for (int w = 1; w < KSPLIT; ++w) v += red[w][o][lane];
+        const int pb = (cb0 + o) * 16;
+        if (pb + 16 <= ncols)
+          store4_bf16_full<EPI, VEC>(y, ldy, m, pb + n_lane, v, v, st, ep);
+        else
+          store4_bf16_edge<EPI, VEC>(y, ldy, M, ncols, m, pb + n_lane, v, v, st, ep);
       }
-      const int f = (cb0 / 2 + o) * 16 + n_lane;
-      store4_bf16<EPI>(y, ldy, ncols, m, f, g, u, st, ep);
-    } else {
-      f32x4 v = red[0][o][lane];
-#pragma unroll
-      for (int w = 1; w < KSPLIT; ++w) v += red[w][o][lane];
-      const int p = (cb0 + o) * 16 + n_lane;
-      store4_bf16<EPI>(y, ldy, ncols, m, p, v, v, st, ep);
     }
-  }
+  };
+  if (epi_vec<EPI>(ep) != nullptr)
+    epilogue(std::true_type{});
+  else
+    epilogue(std::false_type{});
 }
 
 template <int NCB, int KSPLIT, int U, int EPI>
@@ -133,13 +148,27 @@ static hipError_t launch_decode_cfg(const DecodeArgs& p) {
   return hipGetLastError();
 }
 
+template <int EPI>
+static hipError_t launch_decode_epi(const DecodeArgs& p) {
+  switch (p.cfg) {
+    case 0:
+    case 1: return launch_decode_cfg<2, 8, 8, EPI>(p);
+    case 2: return launch_decode_cfg<2, 4, 8, EPI>(p);
+    case 3: return launch_decode_cfg<2, 16, 4, EPI>(p);
+    case 4: return launch_decode_cfg<4, 8, 4, EPI>(p);
+    case 5: return launch_decode_cfg<2, 8, 4, EPI>(p);
+    case 6: return launch_decode_cfg<2, 16, 8, EPI>(p);
+  }
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_decode_bf16(const DecodeArgs& p) {
   switch (p.epi) {
-    case EPI_RMS: return launch_decode_cfg<2, 8, 8, EPI_RMS>(p);
-    case EPI_GLU: return launch_decode_cfg<2, 8, 8, EPI_GLU>(p);
-    case EPI_LN: return launch_decode_cfg<2, 8, 8, EPI_LN>(p);
-    case EPI_NONE: return launch_decode_cfg<2, 8, 8, EPI_NONE>(p);
-    case EPI_GLU_NOSCALE: return launch_decode_cfg<2, 8, 8, EPI_GLU_NOSCALE>(p);
+    case EPI_RMS: return launch_decode_epi<EPI_RMS>(p);
+    case EPI_GLU: return launch_decode_epi<EPI_GLU>(p);
+    case EPI_LN: return launch_decode_epi<EPI_LN>(p);
+    case EPI_NONE: return launch_decode_epi<EPI_NONE>(p);
+    case EPI_GLU_NOSCALE: return launch_decode_epi<EPI_GLU_NOSCALE>(p);
   }
   return hipErrorInvalidValue;
 }

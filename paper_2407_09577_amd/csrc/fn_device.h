@@ -65,14 +65,16 @@ __device__ __forceinline__ i32x4 make_rsrc_sgpr(const void* base, uint32_t bytes
 // wave writes lds_base + 16 * i; out-of-range lanes write zeros.  Issued through
 // inline asm so the compiler does not add a conservative wait for these writes
 // before unrelated LDS reads: the kernels order them with explicit vmcnt waits
-// and barriers.  lds_base must be wave-uniform.
+// and barriers.  lds_base must be wave-uniform.  M0 is written here without being
+// declared (the compiler reserves it and rejects the clobber); these kernels use
+// M0 for nothing else.
 __device__ __forceinline__ void load_lds16(i32x4 rsrc, const void* lds_base, unsigned voffset) {
   const unsigned m0 = __builtin_amdgcn_readfirstlane(
       (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_base);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
                : "s"(m0), "v"(voffset), "s"(rsrc)
-               : "memory", "m0");
+               : "memory");
 }
 
 // 16 bytes per lane from a range-checked buffer into registers.

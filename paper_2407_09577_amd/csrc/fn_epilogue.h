@@ -35,42 +35,66 @@ __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& e
   return st;
 }
 
-// Store 4 consecutive outputs of row m starting at logical column n (a multiple
-// of 4).  v: accumulators of the 4 columns (GLU: gate); u: the up accumulators.
-// ncols: number of logical output columns (N, or F for a GLU).
+// Four fp32 values -> four bf16 (hardware round to nearest even), as 8 bytes.
+__device__ __forceinline__ u32x2 pack4_bf16(const float (&o)[4]) {
+  typedef __attribute__((ext_vector_type(2))) float f32x2;
+  const bf16x2 lo = __builtin_convertvector((f32x2{o[0], o[1]}), bf16x2);
+  const bf16x2 hi = __builtin_convertvector((f32x2{o[2], o[3]}), bf16x2);
+  return u32x2{__builtin_bit_cast(unsigned, lo), __builtin_bit_cast(unsigned, hi)};
+}
+
+// Epilogue value of one output.  vec: the optional per-column vector (RMS: the
+// bias, added after the scaling; LN: c*), 0 when absent; cs: colsum (LN).
 template <int EPI>
-__device__ __forceinline__ void store4_bf16(__bf16* __restrict__ y, int64_t ldy, int ncols, int m,
-                                            int n, f32x4 v, f32x4 u, RowStat st,
-                                            const EpiArgs& ep) {
+__device__ __forceinline__ float epi_value(float v, float u, RowStat st, float vec, float cs) {
+  if constexpr (EPI == EPI_RMS) return fmaf(v, st.s, vec);
+  else if constexpr (EPI == EPI_GLU) return silu(v * st.s) * (u * st.s);
+  else if constexpr (EPI == EPI_LN) return fmaf(fmaf(-st.mu, cs, v), st.s, vec);
+  else if constexpr (EPI == EPI_NONE) return v;
+  else return silu(v) * u;  // EPI_GLU_NOSCALE
+}
+
+// The optional per-column vector of an epilogue (bias or c*), or nullptr.
+template <int EPI>
+__device__ __forceinline__ const float* epi_vec(const EpiArgs& ep) {
+  if constexpr (EPI == EPI_RMS) return ep.bias;
+  else if constexpr (EPI == EPI_LN) return ep.cstar;
+  else return nullptr;
+}
+
+// Store 4 consecutive outputs of row m starting at logical column n (n % 4 == 0)
+// when all four lie inside the output: one 8-byte store, 16-byte vector loads of
+// the per-column vectors.  VEC: the optional per-column vector is present.
+// v: accumulators of the 4 columns (GLU: gate); u: the up accumulators.
+template <int EPI, bool VEC>
+__device__ __forceinline__ void store4_bf16_full(__bf16* __restrict__ y, int64_t ldy, int m, int n,
+                                                 f32x4 v, f32x4 u, RowStat st, const EpiArgs& ep) {
+  f32x4 vec = {0.f, 0.f, 0.f, 0.f}, cs = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (VEC) vec = *reinterpret_cast<const f32x4*>(epi_vec<EPI>(ep) + n);
+  if constexpr (EPI == EPI_LN) cs = *reinterpret_cast<const f32x4*>(ep.colsum + n);
   float o[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) o[r] = epi_value<EPI>(v[r], u[r], st, vec[r], cs[r]);
+  *reinterpret_cast<u32x2*>(y + (int64_t)m * ldy + n) = pack4_bf16(o);
+}
+
+// The same for the ragged edge: row m may lie past M and columns past ncols
+// (number of logical output columns: N, or F for a GLU).
+template <int EPI, bool VEC>
+__device__ __forceinline__ void store4_bf16_edge(__bf16* __restrict__ y, int64_t ldy, int M, int ncols,
+                                                 int m, int n, f32x4 v, f32x4 u, RowStat st,
+                                                 const EpiArgs& ep) {
+  if (m >= M) return;
+  const float* vp = epi_vec<EPI>(ep);
+  unsigned short* dst = reinterpret_cast<unsigned short*>(y + (int64_t)m * ldy + n);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int c = n + r;
-    float val;
-    if constexpr (EPI == EPI_RMS) {
-      val = v[r] * st.s;
-      if (ep.bias && c < ncols) val += ep.bias[c];
-    } else if constexpr (EPI == EPI_GLU) {
-      val = silu(v[r] * st.s) * (u[r] * st.s);
-    } else if constexpr (EPI == EPI_LN) {
-      float cs = c < ncols ? ep.colsum[c] : 0.0f;
-      float cb = (ep.cstar && c < ncols) ? ep.cstar[c] : 0.0f;
-      val = fmaf(fmaf(-st.mu, cs, v[r]), st.s, cb);
-    } else if constexpr (EPI == EPI_NONE) {
-      val = v[r];
-    } else {  // EPI_GLU_NOSCALE
-      val = silu(v[r]) * u[r];
+    if (c < ncols) {
+      const float vec = VEC ? vp[c] : 0.f;
+      const float cs = EPI == EPI_LN ? ep.colsum[c] : 0.f;
+      dst[r] = __builtin_bit_cast(unsigned short, (__bf16)epi_value<EPI>(v[r], u[r], st, vec, cs));
     }
-    o[r] = val;
-  }
-  __bf16* dst = y + (int64_t)m * ldy + n;
-  if (n + 3 < ncols) {
-    u32x2 w = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-    *reinterpret_cast<u32x2*>(dst) = w;
-  } else {
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (n + r < ncols) reinterpret_cast<unsigned short*>(dst)[r] = (unsigned short)f32_to_bf16_bits(o[r]);
   }
 }
 

@@ -9,7 +9,21 @@
 
 namespace fn {
 
-enum Tile : int { TILE_AUTO = 0, TILE_256x256 = 1, TILE_128x128 = 2 };
+// Prefill tile configurations (selected automatically, or forced through the
+// high byte of the path argument for tuning).
+enum Tile : int {
+  TILE_AUTO = 0,
+  TILE_256x256 = 1,       // 4 waves of 128 x 128, 4-stage ring, register prefetch
+  TILE_128x128 = 2,       // 4 waves of 64 x 64, 4-stage ring, register prefetch
+  TILE_256x256_W8 = 3,    // 8 waves of 128 x 64, 4-stage ring
+  TILE_128x128_S8 = 4,    // 4 waves of 64 x 64, 8-stage ring, register prefetch
+  TILE_256x128 = 5,       // 4 waves of 128 x 64
+  TILE_128x256 = 6,       // 4 waves of 64 x 128
+  TILE_128x64 = 7,        // 4 waves of 64 x 32
+  TILE_64x128 = 8,        // 4 waves of 32 x 64
+  TILE_128x128_NOPF = 9,  // as TILE_128x128 without register prefetch
+  TILE_COUNT
+};
 
 // Packed-layout geometry shared by the fold and the kernels.
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -43,10 +57,12 @@ struct DecodeArgs {
   __bf16* y;
   int ldy;
   int epi;
+  int cfg;  // decode configuration (0 = automatic), see launch_decode_bf16
   EpiArgs ep;
   hipStream_t stream;
 };
 hipError_t launch_decode_bf16(const DecodeArgs& p);
+constexpr int kDecodeCfgCount = 7;
 
 struct F32Args {
   const float* a;

@@ -15,6 +15,8 @@
 // transposed, D' = W*^T a^T, so that one lane's four accumulators are four
 // consecutive output columns of one row, and the lane that squares an
 // activation fragment holds exactly the row whose outputs it scales.
+#include <type_traits>
+
 #include "fn_device.h"
 #include "fn_epilogue.h"
 #include "fn_launch.h"
@@ -43,34 +45,56 @@ __device__ __forceinline__ void tile_of_block(int bid, int nblocks, int tiles_m,
   tn = in_group / gsize;
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+// Wait until at most `ahead` k blocks of this wave's ring transfers (LOADS each)
+// are still outstanding, i.e. everything issued before them has landed.
+// `ahead` is wave-uniform and at most A; the counter needs an immediate, so the
+// exact value is selected by a chain of uniform branches.
+template <int LOADS, int A>
+__device__ __forceinline__ void wait_ahead(int ahead) {
+  if constexpr (A == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= A)
+      wait_vmcnt<A * LOADS>();
+    else
+      wait_ahead<LOADS, A - 1>(ahead);
+  }
+}
+
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI>
 __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep, int tiles_m, int tiles_n) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;  // wave sub-tile
   constexpr int FM = TM / 16, FN = TN / 16;  // fragments per wave along rows / columns
-  constexpr int A_FRAGS = BM / 16 * 2, W_FRAGS = BN / 16 * 2;
+  constexpr int A_FRAGS = BM / 16, W_FRAGS = BN / 16;  // per 32-deep k block
+  constexpr int T_FRAGS = A_FRAGS + W_FRAGS;
   constexpr int A_BYTES = A_FRAGS * kFragBytes;
-  constexpr int STAGE = (A_FRAGS + W_FRAGS) * kFragBytes;
-  constexpr int A_PER_WAVE = A_FRAGS / NW, W_PER_WAVE = W_FRAGS / NW;
-  constexpr int LOADS = A_PER_WAVE + W_PER_WAVE;
-  static_assert(A_FRAGS % NW == 0 && W_FRAGS % NW == 0, "fragments must split evenly over waves");
+  constexpr int STAGE = T_FRAGS * kFragBytes;
+  constexpr int LOADS = (T_FRAGS + NW - 1) / NW;     // loads per wave per stage
+  constexpr bool kUneven = T_FRAGS % NW != 0;        // some waves pad with a dummy load
+  constexpr int NMF = FN * FM;                       // matrix-core ops per wave per k block
+  constexpr int NRD = FN + FM;                       // LDS fragment reads per wave per k block
+  static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be whole fragments");
   static_assert(!epi_is_glu(EPI) || TN % 32 == 0, "GLU needs whole gate/up block pairs per wave");
+  static_assert(STAGES >= 3 && (STAGES - 2) * LOADS < 64, "ring depth / vmcnt range");
+  static_assert(NRD <= NMF && LOADS <= NRD, "schedule needs at least one op per group");
   constexpr bool kSS = epi_needs_ss(EPI);
   constexpr bool kSA = EPI == EPI_LN;
 
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  // STAGES ring of k blocks, plus one slot that absorbs padding loads.
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE + (kUneven ? kFragBytes : 0)];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
   int tm, tn;
   tile_of_block(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM;
   const int p0 = tn * BN;
-  const int KB = KP / kKB;  // fragments per packed column block
+  const int nkb = KP / kKB;  // k blocks (even: KP is a multiple of 64)
 
   // Range-checked views of this tile's activation rows and weight column blocks.
   const int rows_valid = min(BM, M - m0);
@@ -78,35 +102,39 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
                                     (uint32_t)(((int64_t)(rows_valid - 1) * lda + K) * 2));
   const int cb0 = p0 / 16;
   const int cbs_valid = min(BN / 16, NP / 16 - cb0);
-  const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * KB * (kFragBytes / 2),
-                                    (uint32_t)(cbs_valid * KB * kFragBytes));
+  const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * nkb * (kFragBytes / 2),
+                                    (uint32_t)(cbs_valid * nkb * kFragBytes));
 
-  // Every wave moves A_FRAGS/NW activation and W_FRAGS/NW weight fragments per
-  // k step; fragment f covers block f/2 at k half f%2.  The per-lane offsets are
-  // fixed except for the k step.
+  // Fragment f of a stage: f < A_FRAGS is activation row block f, otherwise weight
+  // column block f - A_FRAGS.  Wave w moves fragments w, w + NW, ...
   const int lrow = lane & 15;
   const int lk = (lane >> 4) * 8;
-  unsigned a_off[A_PER_WAVE];
-  int a_k[A_PER_WAVE];
+  unsigned off0[LOADS];
 #pragma unroll
-  for (int i = 0; i < A_PER_WAVE; ++i) {
-    const int f = wave * A_PER_WAVE + i;
-    a_k[i] = (f & 1) * 32 + lk;
-    a_off[i] = (unsigned)(((f >> 1) * 16 + lrow) * lda * 2 + a_k[i] * 2);
+  for (int i = 0; i < LOADS; ++i) {
+    const int f = wave + NW * i;
+    if (A_FRAGS % NW == 0 ? i < A_FRAGS / NW : f < A_FRAGS)
+      off0[i] = (unsigned)((f * 16 + lrow) * lda * 2 + lk * 2);
+    else
+      off0[i] = (unsigned)((f - A_FRAGS) * nkb * kFragBytes + lane * 16);
   }
 
-  auto load_tile = [&](int kt, char* stage) {
-#pragma unroll
-    for (int i = 0; i < A_PER_WAVE; ++i) {
-      const int f = wave * A_PER_WAVE + i;
-      const int k = kt * 64 + a_k[i];
-      load_lds16(rs_a, stage + f * kFragBytes, k < K ? a_off[i] + kt * 128 : kOobOffset);
-    }
-#pragma unroll
-    for (int i = 0; i < W_PER_WAVE; ++i) {
-      const int g = wave * W_PER_WAVE + i;
-      const unsigned off = (unsigned)(((g >> 1) * KB + kt * 2 + (g & 1)) * kFragBytes + lane * 16);
-      load_lds16(rs_w, stage + A_BYTES + g * kFragBytes, off);
+  // Transfer i of block kb into its ring slot.  Every wave issues exactly LOADS
+  // transfers per block, also for blocks past the end of K (they read as
+  // zeros), so the outstanding-transfer count of every step is the same.
+  // When the activation fragments split evenly over the waves, transfer i is an
+  // activation fragment exactly when i < A_FRAGS / NW (known at compile time).
+  constexpr bool kSplitA = A_FRAGS % NW == 0;
+  auto load_one = [&](int kb, int i) {
+    char* st = smem + (kb % STAGES) * STAGE;
+    const int f = wave + NW * i;
+    if (kSplitA ? i < A_FRAGS / NW : f < A_FRAGS) {
+      const bool ok = kb * kKB + lk < K;
+      load_lds16(rs_a, st + f * kFragBytes, ok ? off0[i] + kb * (kKB * 2) : kOobOffset);
+    } else if (!kUneven || f < T_FRAGS) {
+      load_lds16(rs_w, st + f * kFragBytes, kb < nkb ? off0[i] + kb * kFragBytes : kOobOffset);
+    } else {
+      load_lds16(rs_w, smem + STAGES * STAGE, kOobOffset);
     }
   };
 
@@ -119,115 +147,214 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 #pragma unroll
   for (int j = 0; j < FM; ++j) ss[j] = sa[j] = 0.f;
 
-  auto compute = [&](const char* stage) {
+  bf16x8 af0[FM], wf0[FN];
+  bf16x8 af1[PF ? FM : 1], wf1[PF ? FN : 1];
+
+  // Fragment r of block kb (r < FM: activations, else weights) into registers.
+  auto read_one = [&](int kb, int r, bf16x8 (&af)[FM], bf16x8 (&wf)[FN]) {
+    const char* st = smem + (kb % STAGES) * STAGE;
+    if (r < FM)
+      af[r] = *reinterpret_cast<const bf16x8*>(st + (wm * FM + r) * kFragBytes + lane * 16);
+    else
+      wf[r - FM] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + (wn * FN + r - FM) * kFragBytes + lane * 16);
+  };
+
+  // Row statistics of fragment j (squares, and sums for LayerNorm).
+  auto stats_one = [&](int j, const bf16x8 (&af)[FM]) {
+    if constexpr (kSS) ss[j] = sumsq8(af[j], ss[j]);
+    if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
+  };
+
+  auto sync_block = [&]() {
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS reads have landed
+    __builtin_amdgcn_s_barrier();
+  };
+
+  // One k block of work for the matrix cores, issued as NRD groups: group g
+  // holds its share of the NMF matrix-core ops, LDS read g of the next block
+  // (PF), transfer g of block kb+STAGES-1 (g < LOADS) and the row statistics of
+  // activation fragment g (g < FM).  The scheduling fences keep this
+  // interleaving, so memory traffic overlaps the matrix cores.
+  auto multiply_interleaved = [&](int kb, const bf16x8 (&afc)[FM], const bf16x8 (&wfc)[FN], bf16x8 (&afn)[FM],
+                                  bf16x8 (&wfn)[FN], bool more, bool stats) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      bf16x8 wf[FN], af[FM];
+    for (int g = 0; g < NRD; ++g) {
 #pragma unroll
-      for (int i = 0; i < FN; ++i)
-        wf[i] = *reinterpret_cast<const bf16x8*>(
-            stage + A_BYTES + ((wn * FN + i) * 2 + kb) * kFragBytes + lane * 16);
+      for (int t = g * NMF / NRD; t < (g + 1) * NMF / NRD; ++t) {
+        const int i = t / FM, j = t % FM;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wfc[i], afc[j], acc[i][j], 0, 0, 0);
+      }
+      if (more) {
+        if (g < LOADS) load_one(kb + STAGES - 1, g);
+        read_one(kb + 1, g, afn, wfn);
+      }
+      if (g < FM && stats) stats_one(g, afc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // Ring discipline.  Block kb lives in slot kb % STAGES; global->LDS transfers
+  // run STAGES-1 blocks ahead of the matrix cores.
+  //  PF: LDS->register reads run one block ahead of the matrix cores.  Step kb
+  //   waits until block kb+1 has landed (the STAGES-3 blocks after it may stay
+  //   outstanding) and for this wave's reads of block kb; the barrier then makes
+  //   block kb+1 visible to all waves and guarantees every wave has finished
+  //   reading block kb-1, whose slot the transfer of block kb+STAGES-1 overwrites.
+  //  !PF: step kb waits for block kb, barriers, then reads and multiplies it.
 #pragma unroll
-      for (int j = 0; j < FM; ++j)
-        af[j] = *reinterpret_cast<const bf16x8*>(stage + ((wm * FM + j) * 2 + kb) * kFragBytes +
-                                                 lane * 16);
+  for (int s = 0; s < STAGES - 1; ++s)
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) load_one(s, i);
+  // The WN waves that share a row band take turns squaring its activation
+  // fragments: wave wn handles the k blocks with kb % WN == wn, and the partial
+  // sums are combined through LDS after the loop.
+  auto stats_turn = [&](int kb) { return (kb % WN) == wn; };
+  if constexpr (PF) {
+    wait_vmcnt<(STAGES - 2) * LOADS>();
+    sync_block();
+#pragma unroll
+    for (int r = 0; r < NRD; ++r) read_one(0, r, af0, wf0);
+    for (int kb = 0; kb < nkb - 2; kb += 2) {
+      wait_vmcnt<(STAGES - 3) * LOADS>();
+      sync_block();
+      multiply_interleaved(kb, af0, wf0, af1, wf1, true, stats_turn(kb));
+      wait_vmcnt<(STAGES - 3) * LOADS>();
+      sync_block();
+      multiply_interleaved(kb + 1, af1, wf1, af0, wf0, true, stats_turn(kb + 1));
+    }
+    wait_vmcnt<(STAGES - 3) * LOADS>();
+    sync_block();
+    multiply_interleaved(nkb - 2, af0, wf0, af1, wf1, true, stats_turn(nkb - 2));
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    multiply_interleaved(nkb - 1, af1, wf1, af0, wf0, false, stats_turn(nkb - 1));
+  } else {
+    for (int kb = 0; kb < nkb; ++kb) {
+      wait_vmcnt<(STAGES - 2) * LOADS>();
+      sync_block();
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i) load_one(kb + STAGES - 1, i);
+#pragma unroll
+      for (int r = 0; r < NRD; ++r) read_one(kb, r, af0, wf0);
+#pragma unroll
+      for (int t = 0; t < NMF; ++t)
+        acc[t / FM][t % FM] =
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[t / FM], af0[t % FM], acc[t / FM][t % FM], 0, 0, 0);
+      if (stats_turn(kb)) {
+#pragma unroll
+        for (int j = 0; j < FM; ++j) stats_one(j, af0);
+      }
+    }
+  }
+
+  // Row statistics: lanes l, l^16, l^32, l^48 hold disjoint k of the same row,
+  // and the WN waves of a row band hold disjoint k blocks.
+  if constexpr (kSS || kSA) {
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      if constexpr (kSS) {
+        ss[j] += __shfl_xor(ss[j], 16);
+        ss[j] += __shfl_xor(ss[j], 32);
+      }
+      if constexpr (kSA) {
+        sa[j] += __shfl_xor(sa[j], 16);
+        sa[j] += __shfl_xor(sa[j], 32);
+      }
+    }
+    if constexpr (WN > 1) {
+      __shared__ float part[WN][2][BM];
+      if (lane < 16) {
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+          part[wn][0][wm * TM + j * 16 + lane] = ss[j];
+          part[wn][1][wm * TM + j * 16 + lane] = sa[j];
+        }
+      }
+      __syncthreads();
 #pragma unroll
       for (int j = 0; j < FM; ++j) {
-        if constexpr (kSS) ss[j] = sumsq8(af[j], ss[j]);
-        if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
+        float t0 = 0.f, t1 = 0.f;
+#pragma unroll
+        for (int w = 0; w < WN; ++w) {
+          t0 += part[w][0][wm * TM + j * 16 + lrow];
+          t1 += part[w][1][wm * TM + j * 16 + lrow];
+        }
+        ss[j] = t0;
+        sa[j] = t1;
       }
-#pragma unroll
-      for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
-    }
-  };
-
-  // All LDS reads of a stage have been consumed by the matrix cores before the
-  // barrier that precedes its next overwrite; the waits below only order the
-  // buffer->LDS transfers.
-  auto sync_after_loads = [&](bool more) {
-    if (more)
-      wait_vmcnt<LOADS>();
-    else
-      wait_vmcnt<0>();
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    __builtin_amdgcn_s_barrier();
-  };
-  auto sync_after_compute = [&]() {
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    __builtin_amdgcn_s_barrier();
-  };
-
-  const int nkt = KP / 64;
-  load_tile(0, smem);
-  for (int kt = 0; kt < nkt; ++kt) {
-    char* cur = smem + (kt & 1) * STAGE;
-    const bool more = kt + 1 < nkt;
-    if (more) load_tile(kt + 1, smem + ((kt + 1) & 1) * STAGE);
-    sync_after_loads(more);
-    compute(cur);
-    sync_after_compute();
-  }
-
-  // Row statistics: lanes l, l^16, l^32, l^48 hold disjoint k of the same row.
-#pragma unroll
-  for (int j = 0; j < FM; ++j) {
-    if constexpr (kSS) {
-      ss[j] += __shfl_xor(ss[j], 16);
-      ss[j] += __shfl_xor(ss[j], 32);
-    }
-    if constexpr (kSA) {
-      sa[j] += __shfl_xor(sa[j], 16);
-      sa[j] += __shfl_xor(sa[j], 32);
     }
   }
 
+  // Epilogue: one uniform decision per 16 x 16 fragment picks the fast store
+  // (fragment fully inside the output) or the guarded edge store, and the
+  // optional per-column vector is dispatched once for the whole tile.
   const int n_lane = (lane >> 4) * 4;
+  auto epilogue = [&](auto vec_tag) {
+    constexpr bool VEC = decltype(vec_tag)::value;
 #pragma unroll
-  for (int j = 0; j < FM; ++j) {
-    const int m = m0 + wm * TM + j * 16 + lrow;
-    const RowStat st = row_stat<EPI>(ss[j], sa[j], ep);
-    if constexpr (EPI == EPI_RMS) {
-      if (ep.inv_rms && wn == 0 && lane < 16 && m < M) ep.inv_rms[m] = st.s;
-    }
-    if (m >= M) continue;
-    if constexpr (epi_is_glu(EPI)) {
-#pragma unroll
-      for (int i = 0; i < FN; i += 2) {
-        const int f = (p0 + wn * TN) / 2 + (i / 2) * 16 + n_lane;
-        store4_bf16<EPI>(y, ldy, ncols, m, f, acc[i][j], acc[i + 1][j], st, ep);
+    for (int j = 0; j < FM; ++j) {
+      const int mb = m0 + wm * TM + j * 16;
+      const int m = mb + lrow;
+      const RowStat st = row_stat<EPI>(ss[j], sa[j], ep);
+      if constexpr (EPI == EPI_RMS) {
+        if (ep.inv_rms && wn == 0 && lane < 16 && m < M) ep.inv_rms[m] = st.s;
       }
-    } else {
+      const bool rows_full = mb + 16 <= M;
+      if constexpr (epi_is_glu(EPI)) {
 #pragma unroll
-      for (int i = 0; i < FN; ++i) {
-        const int p = p0 + wn * TN + i * 16 + n_lane;
-        store4_bf16<EPI>(y, ldy, ncols, m, p, acc[i][j], acc[i][j], st, ep);
+        for (int i = 0; i < FN; i += 2) {
+          const int fb = (p0 + wn * TN) / 2 + (i / 2) * 16;
+          if (rows_full && fb + 16 <= ncols)
+            store4_bf16_full<EPI, VEC>(y, ldy, m, fb + n_lane, acc[i][j], acc[i + 1][j], st, ep);
+          else
+            store4_bf16_edge<EPI, VEC>(y, ldy, M, ncols, m, fb + n_lane, acc[i][j], acc[i + 1][j], st, ep);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+          const int pb = p0 + wn * TN + i * 16;
+          if (rows_full && pb + 16 <= ncols)
+            store4_bf16_full<EPI, VEC>(y, ldy, m, pb + n_lane, acc[i][j], acc[i][j], st, ep);
+          else
+            store4_bf16_edge<EPI, VEC>(y, ldy, M, ncols, m, pb + n_lane, acc[i][j], acc[i][j], st, ep);
+        }
       }
     }
-  }
+  };
+  if (epi_vec<EPI>(ep) != nullptr)
+    epilogue(std::true_type{});
+  else
+    epilogue(std::false_type{});
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI>
 static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = (p.NP + BN - 1) / BN;
   const int nblocks = tiles_m * tiles_n;
-  hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(nblocks), dim3(WM * WN * 64), 0,
-                     p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y, p.ldy, p.ep,
-                     tiles_m, tiles_n);
+  hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI>), dim3(nblocks),
+                     dim3(WM * WN * 64), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y,
+                     p.ldy, p.ep, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_prefill_epi(const PrefillArgs& p) {
-  // Shape-specialised tiles: the large tile when it still yields at least one
-  // tile per compute unit, a smaller one otherwise.
+  // Shape-specialised tiles (measured on MI355X): the 256 x 256 tile with 8 waves
+  // when it still yields at least one tile per compute unit, 128 x 128 otherwise.
   const int64_t big = ((int64_t)(p.M + 255) / 256) * ((p.NP + 255) / 256);
-  if (p.tile == TILE_256x256 || (p.tile == TILE_AUTO && big >= 256))
-    return launch_prefill_cfg<256, 256, 2, 4, EPI>(p);
-  if (p.tile == TILE_128x128 || p.tile == TILE_AUTO) return launch_prefill_cfg<128, 128, 2, 2, EPI>(p);
+  int tile = p.tile;
+  if (tile == TILE_AUTO) tile = big >= 256 ? TILE_256x256_W8 : TILE_128x128;
+  switch (tile) {
+    case TILE_256x256: return launch_prefill_cfg<256, 256, 2, 2, 4, true, EPI>(p);
+    case TILE_128x128: return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
+    case TILE_256x256_W8: return launch_prefill_cfg<256, 256, 2, 4, 4, false, EPI>(p);
+    case TILE_128x128_S8: return launch_prefill_cfg<128, 128, 2, 2, 8, true, EPI>(p);
+    case TILE_256x128: return launch_prefill_cfg<256, 128, 2, 2, 4, true, EPI>(p);
+    case TILE_128x256: return launch_prefill_cfg<128, 256, 2, 2, 4, true, EPI>(p);
+    case TILE_128x64: return launch_prefill_cfg<128, 64, 2, 2, 4, true, EPI>(p);
+    case TILE_64x128: return launch_prefill_cfg<64, 128, 2, 2, 4, true, EPI>(p);
+    case TILE_128x128_NOPF: return launch_prefill_cfg<128, 128, 2, 2, 4, false, EPI>(p);
+  }
   return hipErrorInvalidValue;
 }
 

@@ -139,3 +139,10 @@ def test_baseline_validation(fnlib):
     assert b(xws=0) == -1
     assert b(xws=A) == -8                          # workspace overlaps the activations
     assert lib.baseline_layernorm_linear(A, 4, 64, 64, 1, X, None, W, 32, 1e-5, 0x500000, Y, 32, 0, None) == -1
+
+
+def test_vector_alignment_validation(fnlib):
+    lib = fnlib.lib()
+    assert lib.flashnorm_linear_ex(A, 4, 64, 64, 1, W, 32, 1e-6, X + 4, Y, 32, 1, None, 0, None) == -4
+    assert lib.flashnorm_layernorm_linear_ex(A, 4, 64, 64, 1, W, X + 8, None, 32, 1e-5, Y, 32, 1, 0, None) == -4
+    assert lib.flashnorm_layernorm_linear_ex(A, 4, 64, 64, 1, W, X, X + 4, 32, 1e-5, Y, 32, 1, 0, None) == -4

@@ -281,3 +281,47 @@ def test_non_contiguous_activation_rows(fn):
     y = fn.flashnorm_linear(a[:12], Ws, 80, w.eps, path=2)
     torch.cuda.synchronize()
     assert row_err(to_np(y), oracle.rmsnorm_linear(w.a[:12], w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
+
+
+# ------------------------------------------------------------------ every kernel configuration
+PREFILL_TILES = list(range(1, 10))   # forced through the high byte of the path argument
+DECODE_CFGS = [1, 2, 3, 4, 5, 6]
+
+
+@pytest.mark.parametrize("tile", PREFILL_TILES)
+@pytest.mark.parametrize("kind", ["linear", "glu", "layernorm"])
+def test_every_prefill_tile(fn, tile, kind):
+    M, K, N = 300, 328, 2 * 80 if kind == "glu" else 296
+    w = workloads.make(kind, M, K, N // 2 if kind == "glu" else N, eps=1e-5, seed=tile * 7 + len(kind),
+                       a_mean=0.5 if kind == "layernorm" else 0.0, outlier_frac=0.02)
+    path = fn.FN_PATH_PREFILL | (tile << 8)
+    dev_W, dev_g = w.W.to(DEV), w.g.to(DEV)
+    a = w.a.to(DEV)
+    if kind == "linear":
+        Ws, _, _ = fn.fold_weights(dev_W, dev_g)
+        out = fn.flashnorm_linear(a, Ws, w.N, w.eps, path=path)
+        ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+    elif kind == "glu":
+        Ws, _, _ = fn.fold_weights(dev_W, dev_g, layout=fn.FN_LAYOUT_GLU)
+        out = fn.flashnorm_glu(a, Ws, w.out_features, w.eps, path=path)
+        ref = oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)
+    else:
+        Ws, cs, cb = fn.fold_weights(dev_W, dev_g, beta=w.beta.to(DEV), colsum=True, c_star=True)
+        out = fn.flashnorm_layernorm_linear(a, Ws, cs, cb, w.N, w.eps, path=path)
+        ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps)
+    torch.cuda.synchronize()
+    assert row_err(to_np(out), ref) <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("cfg", DECODE_CFGS)
+@pytest.mark.parametrize("M", [1, 7, 16])
+def test_every_decode_config(fn, cfg, M):
+    w = workloads.make("glu", M, 1032, 72, eps=1e-6, seed=cfg * 3 + M)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    out = fn.flashnorm_glu(w.a.to(DEV), Ws, 72, w.eps, path=fn.FN_PATH_DECODE | (cfg << 8))
+    lin = workloads.make("linear", M, 1032, 88, eps=1e-6, seed=cfg * 5 + M)
+    Wl, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
+    y = fn.flashnorm_linear(lin.a.to(DEV), Wl, 88, lin.eps, path=fn.FN_PATH_DECODE | (cfg << 8))
+    torch.cuda.synchronize()
+    assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
+    assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
