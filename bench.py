@@ -47,6 +47,10 @@ def parse_args():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-unfused", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle timing sample")
+    p.add_argument("--eager", action="store_true",
+                   help="launch every step from Python instead of replaying a captured HIP graph")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 256 MiB device copy (known traffic) for counter calibration")
     return p.parse_args()
 
 
@@ -118,17 +122,31 @@ class Setup:
         """Read a once, read W* once, write the output once."""
         return self.M * self.K * self.es + self.ws_bytes + self.M * self.ncols * self.es
 
-    def time_steps(self, fn_step, steps, warmup):
+    def time_steps(self, fn_step, steps, warmup, graph=True):
+        """Average ms per step over `steps` steps, HIP events on the launch stream.
+        graph=True captures the steps into one HIP graph and times its replay, so
+        small kernels are not limited by Python launch overhead."""
         torch = self.torch
         for i in range(warmup):
             fn_step(i)
         torch.cuda.synchronize()
+        g = None
+        if graph:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(steps):
+                    fn_step(warmup + i)
+            g.replay()  # warm replay
+            torch.cuda.synchronize()
         stream = torch.cuda.current_stream()
         start = torch.cuda.Event(enable_timing=True)
         end = torch.cuda.Event(enable_timing=True)
         start.record(stream)
-        for i in range(steps):
-            fn_step(warmup + i)
+        if g is not None:
+            g.replay()
+        else:
+            for i in range(steps):
+                fn_step(warmup + i)
         end.record(stream)
         torch.cuda.synchronize()
         return start.elapsed_time(end) / steps  # ms per step
@@ -158,20 +176,40 @@ def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total):
     per_row = (time.perf_counter() - t0) / probe.size
     n = int(max(probe.size, min(w.M, target_s / max(per_row, 1e-9))))
     rows = np.arange(n)
+    reps = 0
     t0 = time.perf_counter()
-    call(rows)
-    t = time.perf_counter() - t0
+    while True:  # the whole workload may take far less than the target: repeat it
+        call(rows)
+        reps += 1
+        if n < w.M or time.perf_counter() - t0 >= target_s:
+            break
+    t = (time.perf_counter() - t0) / reps
     if unit == "TFLOP/s":
         value = flops_per_row * n / t / 1e12
     else:  # whole-op bytes over the time the oracle would take for all M rows
         value = bytes_total / (t * w.M / n) / 1e9
+    what = f"all {w.M} rows, {reps} repetitions" if n == w.M else f"rows 0..{n - 1} of {w.M}"
     return {"value": value, "unit": unit, "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"fp64 oracle (standard form) on rows 0..{n - 1} of {w.M} of the same workload, "
-                      f"{t:.2f} s wall"}
+            "sample": f"fp64 oracle (standard form) on {what} of the same workload, {t * reps:.1f} s wall"}
+
+
+def copy_calibration():
+    """A plain device copy of known size: FETCH_SIZE/WRITE_SIZE read for it calibrate the counters."""
+    import torch
+    n = 256 * 2 ** 20
+    x = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "dispatches": 5}), flush=True)
 
 
 def main():
     args = parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
               "the FlashNorm path here is a single-GPU kernel library", file=sys.stderr)
@@ -189,8 +227,9 @@ def main():
     fp32 = w.a.dtype == torch.float32
 
     torch.cuda.synchronize()
-    ms = s.time_steps(s.run, args.steps, args.warmup)
-    ms_unf = None if args.no_unfused else s.time_steps(s.run_unfused, args.steps, args.warmup)
+    graph = not args.eager
+    ms = s.time_steps(s.run, args.steps, args.warmup, graph)
+    ms_unf = None if args.no_unfused else s.time_steps(s.run_unfused, args.steps, args.warmup, graph)
 
     t = ms * 1e-3
     if decode:
@@ -205,6 +244,13 @@ def main():
         roof = {"bound": "alu" if fp32 else "mfma", "achieved": value, "peak": peak, "unit": "TFLOP/s",
                 "frac": value / peak, "traffic": None}
 
+    # HBM traffic per launch from the committed rocprofv3 counter summary of this
+    # workload, only if it was taken with the current kernel sources.
+    from paper_2407_09577_amd import profiling
+    prof = profiling.read_summary(args.workload if not decode else f"{args.workload}_m{args.decode_m}")
+    if prof is not None:
+        roof["traffic"] = float(prof["traffic_bytes_per_launch"])
+
     cpu = None
     if not args.no_cpu_baseline:
         per_row = 2.0 * w.K * w.N
@@ -213,8 +259,11 @@ def main():
     config = {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "out_features": s.ncols, "eps": w.eps,
               "op": {"glu": "flashnorm_glu", "layernorm": "flashnorm_layernorm_linear"}.get(w.kind, "flashnorm_linear"),
               "step": "one fused call on HBM-resident inputs; weight fold done once before timing",
+              "launch": "HIP graph replay of the timed steps" if graph else "eager launches from Python",
               "rotating_sets": s.nsets, "alg_flops_per_step": s.flops(), "alg_bytes_per_step": s.alg_bytes(),
               "parallelism": "single GPU"}
+    if prof is not None:
+        config["traffic_profile"] = prof["path"]
     if ms_unf is not None:
         config["unfused_ms_per_step"] = ms_unf
         config["fused_vs_unfused_speedup"] = (ms_unf - ms) / ms_unf

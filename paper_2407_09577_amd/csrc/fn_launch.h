@@ -22,6 +22,9 @@ enum Tile : int {
   TILE_128x64 = 7,        // 4 waves of 64 x 32
   TILE_64x128 = 8,        // 4 waves of 32 x 64
   TILE_128x128_NOPF = 9,  // as TILE_128x128 without register prefetch
+  TILE_PP_256x256 = 10,   // ping-pong: 2 groups of 4 waves of 128 x 64
+  TILE_PP_256x128 = 11,   // ping-pong: 2 groups of 4 waves of 128 x 32
+  TILE_PP_128x256 = 12,   // ping-pong: 2 groups of 4 waves of 64 x 64
   TILE_COUNT
 };
 

@@ -284,7 +284,7 @@ def test_non_contiguous_activation_rows(fn):
 
 
 # ------------------------------------------------------------------ every kernel configuration
-PREFILL_TILES = list(range(1, 10))   # forced through the high byte of the path argument
+PREFILL_TILES = list(range(1, 13))   # forced through the high byte of the path argument
 DECODE_CFGS = [1, 2, 3, 4, 5, 6]
 
 
@@ -325,3 +325,38 @@ def test_every_decode_config(fn, cfg, M):
     torch.cuda.synchronize()
     assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
     assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
+
+
+def test_graph_replay_matches_eager(fn):
+    # the benchmark times HIP-graph replays: every replay, with eager work and
+    # synchronisations in between, must reproduce the eager result bit for bit
+    lin = workloads.make("linear", 520, 576, 384, eps=1e-5, seed=51)
+    glu = workloads.make("glu", 8, 1024, 96, eps=1e-6, seed=52)
+    ln = workloads.make("layernorm", 300, 256, 128, eps=1e-5, seed=53, a_mean=0.5)
+    Wl, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
+    Wg, _, _ = fn.fold_weights(glu.W.to(DEV), glu.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    Wn, cs, cb = fn.fold_weights(ln.W.to(DEV), ln.g.to(DEV), beta=ln.beta.to(DEV), colsum=True, c_star=True)
+    al, ag, an = lin.a.to(DEV), glu.a.to(DEV), ln.a.to(DEV)
+    yl = torch.empty(520, 384, dtype=torch.bfloat16, device=DEV)
+    yg = torch.empty(8, 96, dtype=torch.bfloat16, device=DEV)
+    yn = torch.empty(300, 128, dtype=torch.bfloat16, device=DEV)
+
+    def step():
+        fn.flashnorm_linear(al, Wl, 384, lin.eps, out=yl)
+        fn.flashnorm_glu(ag, Wg, 96, glu.eps, out=yg)
+        fn.flashnorm_layernorm_linear(an, Wn, cs, cb, 128, ln.eps, out=yn)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (yl, yg, yn)]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for it in range(4):
+        for t in (yl, yg, yn):
+            t.fill_(float("nan"))              # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want in zip((yl, yg, yn), ref):
+            assert torch.equal(got.view(torch.int16), want.view(torch.int16)), f"replay {it}"
