@@ -71,9 +71,15 @@ __device__ __forceinline__ i32x4 make_rsrc_sgpr(const void* base, uint32_t bytes
 __device__ __forceinline__ void load_lds16(i32x4 rsrc, const void* lds_base, unsigned voffset) {
   const unsigned m0 = __builtin_amdgcn_readfirstlane(
       (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_base);
+  // The descriptor is wave-uniform; re-assert it so it is allocated to SGPRs.
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane(rsrc[0]);
+  r[1] = __builtin_amdgcn_readfirstlane(rsrc[1]);
+  r[2] = __builtin_amdgcn_readfirstlane(rsrc[2]);
+  r[3] = __builtin_amdgcn_readfirstlane(rsrc[3]);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
-               : "s"(m0), "v"(voffset), "s"(rsrc)
+               : "s"(m0), "v"(voffset), "s"(r)
                : "memory");
 }
 

@@ -24,25 +24,51 @@
 namespace fn {
 
 // Workgroup id -> output tile.  Consecutive workgroup ids are dispatched to the
-// 8 XCDs in turn, so ids are first regrouped such that each XCD receives a
-// contiguous range of logical tiles; logical tiles are then ordered in groups
-// of kGroupM tile rows so tiles running together on one XCD share activation
-// rows and weight columns in that XCD's L2.
+// 8 XCDs in turn, and each XCD has its own L2.  The tile grid is cut into 8
+// rectangular regions (the factorisation of 8 that keeps a region's activation
+// rows plus weight columns smallest), ids are regrouped so each XCD receives one
+// region, and inside a region tiles run in groups of kGroupM tile rows, so the
+// tiles resident on one XCD share activation rows and weight columns in its L2.
 constexpr int kXcds = 8;
 constexpr int kGroupM = 4;
 
 __device__ __forceinline__ void tile_of_block(int bid, int nblocks, int tiles_m, int tiles_n,
                                               int& tm, int& tn) {
-  const int q = nblocks / kXcds, r = nblocks % kXcds;
-  const int x = bid % kXcds, i = bid / kXcds;
-  const int logical = x * q + min(x, r) + i;
-  const int per_group = kGroupM * tiles_n;
-  const int group = logical / per_group;
-  const int first_m = group * kGroupM;
-  const int gsize = min(tiles_m - first_m, kGroupM);
-  const int in_group = logical - group * per_group;
-  tm = first_m + in_group % gsize;
-  tn = in_group / gsize;
+  // Region grid rm x rn (rm * rn = 8), derived from the tile counts alone, so
+  // every workgroup computes the same grid.
+  int rm = 1, best = 0x7fffffff;
+#pragma unroll
+  for (int c = 1; c <= kXcds; c *= 2) {
+    const int mm = (tiles_m + c - 1) / c, nn = (tiles_n + kXcds / c - 1) / (kXcds / c);
+    if (c <= tiles_m && kXcds / c <= tiles_n && mm + nn < best) {
+      best = mm + nn;
+      rm = c;
+    }
+  }
+  const int rn = kXcds / rm;
+  if (best == 0x7fffffff || nblocks % kXcds != 0 || tiles_m % rm != 0 || tiles_n % rn != 0) {
+    // Small or uneven grids: contiguous ranges per XCD, grouped by tile rows.
+    const int q = nblocks / kXcds, r = nblocks % kXcds;
+    const int x = bid % kXcds, i = bid / kXcds;
+    const int logical = x * q + min(x, r) + i;
+    const int per_group = kGroupM * tiles_n;
+    const int group = logical / per_group;
+    const int first_m = group * kGroupM;
+    const int gsize = min(tiles_m - first_m, kGroupM);
+    const int in_group = logical - group * per_group;
+    tm = first_m + in_group % gsize;
+    tn = in_group / gsize;
+    return;
+  }
+  const int x = bid % kXcds, i = bid / kXcds;  // XCD x runs its region's tiles in order i
+  const int sm = tiles_m / rm, sn = tiles_n / rn;  // region size in tiles
+  const int gm = min(kGroupM, sm);
+  const int per_group = gm * sn;
+  const int group = i / per_group, in_group = i % per_group;
+  const int first_m = group * gm;
+  const int gsize = min(sm - first_m, gm);
+  tm = (x / rn) * sm + first_m + in_group % gsize;
+  tn = (x % rn) * sn + in_group / gsize;
 }
 
 // Wait until at most `ahead` k blocks of this wave's ring transfers (LOADS each)
@@ -125,7 +151,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // When the activation fragments split evenly over the waves, transfer i is an
   // activation fragment exactly when i < A_FRAGS / NW (known at compile time).
   constexpr bool kSplitA = A_FRAGS % NW == 0;
-  auto load_one = [&](int kb, int i) {
+  auto load_one = [&](int kb, int i) __attribute__((always_inline)) {
     char* st = smem + (kb % STAGES) * STAGE;
     const int f = wave + NW * i;
     if (kSplitA ? i < A_FRAGS / NW : f < A_FRAGS) {
@@ -151,7 +177,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   bf16x8 af1[PF ? FM : 1], wf1[PF ? FN : 1];
 
   // Fragment r of block kb (r < FM: activations, else weights) into registers.
-  auto read_one = [&](int kb, int r, bf16x8 (&af)[FM], bf16x8 (&wf)[FN]) {
+  auto read_one = [&](int kb, int r, bf16x8 (&af)[FM], bf16x8 (&wf)[FN]) __attribute__((always_inline)) {
     const char* st = smem + (kb % STAGES) * STAGE;
     if (r < FM)
       af[r] = *reinterpret_cast<const bf16x8*>(st + (wm * FM + r) * kFragBytes + lane * 16);
@@ -160,12 +186,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   };
 
   // Row statistics of fragment j (squares, and sums for LayerNorm).
-  auto stats_one = [&](int j, const bf16x8 (&af)[FM]) {
+  auto stats_one = [&](int j, const bf16x8 (&af)[FM]) __attribute__((always_inline)) {
     if constexpr (kSS) ss[j] = sumsq8(af[j], ss[j]);
     if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
   };
 
-  auto sync_block = [&]() {
+  auto sync_block = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS reads have landed
     __builtin_amdgcn_s_barrier();
   };
@@ -175,8 +201,13 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // (PF), transfer g of block kb+STAGES-1 (g < LOADS) and the row statistics of
   // activation fragment g (g < FM).  The scheduling fences keep this
   // interleaving, so memory traffic overlaps the matrix cores.
-  auto multiply_interleaved = [&](int kb, const bf16x8 (&afc)[FM], const bf16x8 (&wfc)[FN], bf16x8 (&afn)[FM],
-                                  bf16x8 (&wfn)[FN], bool more, bool stats) {
+  // Row statistics are split across the WN waves of a row band at compile time:
+  // the wave with column index WNC squares activation fragments j = WNC + WN t,
+  // over the whole of K, so no wave branches on whose turn it is.
+  auto multiply_interleaved = [&](auto wnc, int kb, const bf16x8 (&afc)[FM], const bf16x8 (&wfc)[FN],
+                                  bf16x8 (&afn)[FM], bf16x8 (&wfn)[FN], bool more)
+                                  __attribute__((always_inline)) {
+    constexpr int WNC = decltype(wnc)::value;
 #pragma unroll
     for (int g = 0; g < NRD; ++g) {
 #pragma unroll
@@ -188,7 +219,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         if (g < LOADS) load_one(kb + STAGES - 1, g);
         read_one(kb + 1, g, afn, wfn);
       }
-      if (g < FM && stats) stats_one(g, afc);
+      if (WNC + WN * g < FM) stats_one(WNC + WN * g, afc);  // resolved when unrolled
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -205,49 +236,58 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   for (int s = 0; s < STAGES - 1; ++s)
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) load_one(s, i);
-  // The WN waves that share a row band take turns squaring its activation
-  // fragments: wave wn handles the k blocks with kb % WN == wn, and the partial
-  // sums are combined through LDS after the loop.
-  auto stats_turn = [&](int kb) { return (kb % WN) == wn; };
-  if constexpr (PF) {
-    wait_vmcnt<(STAGES - 2) * LOADS>();
-    sync_block();
-#pragma unroll
-    for (int r = 0; r < NRD; ++r) read_one(0, r, af0, wf0);
-    for (int kb = 0; kb < nkb - 2; kb += 2) {
-      wait_vmcnt<(STAGES - 3) * LOADS>();
-      sync_block();
-      multiply_interleaved(kb, af0, wf0, af1, wf1, true, stats_turn(kb));
-      wait_vmcnt<(STAGES - 3) * LOADS>();
-      sync_block();
-      multiply_interleaved(kb + 1, af1, wf1, af0, wf0, true, stats_turn(kb + 1));
-    }
-    wait_vmcnt<(STAGES - 3) * LOADS>();
-    sync_block();
-    multiply_interleaved(nkb - 2, af0, wf0, af1, wf1, true, stats_turn(nkb - 2));
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    multiply_interleaved(nkb - 1, af1, wf1, af0, wf0, false, stats_turn(nkb - 1));
-  } else {
-    for (int kb = 0; kb < nkb; ++kb) {
+  auto mainloop = [&](auto wnc) __attribute__((always_inline)) {
+    constexpr int WNC = decltype(wnc)::value;
+    if constexpr (PF) {
       wait_vmcnt<(STAGES - 2) * LOADS>();
       sync_block();
 #pragma unroll
-      for (int i = 0; i < LOADS; ++i) load_one(kb + STAGES - 1, i);
+      for (int r = 0; r < NRD; ++r) read_one(0, r, af0, wf0);
+      for (int kb = 0; kb < nkb - 2; kb += 2) {
+        wait_vmcnt<(STAGES - 3) * LOADS>();
+        sync_block();
+        multiply_interleaved(wnc, kb, af0, wf0, af1, wf1, true);
+        wait_vmcnt<(STAGES - 3) * LOADS>();
+        sync_block();
+        multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true);
+      }
+      wait_vmcnt<(STAGES - 3) * LOADS>();
+      sync_block();
+      multiply_interleaved(wnc, nkb - 2, af0, wf0, af1, wf1, true);
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      multiply_interleaved(wnc, nkb - 1, af1, wf1, af0, wf0, false);
+    } else {
+      for (int kb = 0; kb < nkb; ++kb) {
+        wait_vmcnt<(STAGES - 2) * LOADS>();
+        sync_block();
 #pragma unroll
-      for (int r = 0; r < NRD; ++r) read_one(kb, r, af0, wf0);
+        for (int i = 0; i < LOADS; ++i) load_one(kb + STAGES - 1, i);
 #pragma unroll
-      for (int t = 0; t < NMF; ++t)
-        acc[t / FM][t % FM] =
-            __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[t / FM], af0[t % FM], acc[t / FM][t % FM], 0, 0, 0);
-      if (stats_turn(kb)) {
+        for (int r = 0; r < NRD; ++r) read_one(kb, r, af0, wf0);
 #pragma unroll
-        for (int j = 0; j < FM; ++j) stats_one(j, af0);
+        for (int t = 0; t < NMF; ++t)
+          acc[t / FM][t % FM] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[t / FM], af0[t % FM], acc[t / FM][t % FM], 0, 0, 0);
+#pragma unroll
+        for (int j = WNC; j < FM; j += WN) stats_one(j, af0);
       }
     }
+  };
+  // One copy of the main loop per column-wave index (wave-uniform dispatch); a
+  // single copy when there are no row statistics to split.
+  static_assert(WN <= 4, "mainloop dispatch covers up to 4 column waves");
+  if constexpr (!kSS && !kSA) {
+    mainloop(std::integral_constant<int, 0>{});
+  } else switch (wn) {
+    case 0: mainloop(std::integral_constant<int, 0>{}); break;
+    case 1: if constexpr (WN > 1) mainloop(std::integral_constant<int, 1>{}); break;
+    case 2: if constexpr (WN > 2) mainloop(std::integral_constant<int, 2>{}); break;
+    default: if constexpr (WN > 3) mainloop(std::integral_constant<int, 3>{}); break;
   }
 
-  // Row statistics: lanes l, l^16, l^32, l^48 hold disjoint k of the same row,
-  // and the WN waves of a row band hold disjoint k blocks.
+  // Row statistics: lanes l, l^16, l^32, l^48 hold disjoint k of the same row.
+  // Each fragment's totals live in the one wave of the row band that squared it;
+  // they reach the other WN-1 waves through LDS.
   if constexpr (kSS || kSA) {
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
@@ -261,25 +301,21 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       }
     }
     if constexpr (WN > 1) {
-      __shared__ float part[WN][2][BM];
+      __shared__ float row_tot[2][BM];
       if (lane < 16) {
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
-          part[wn][0][wm * TM + j * 16 + lane] = ss[j];
-          part[wn][1][wm * TM + j * 16 + lane] = sa[j];
+          if (j % WN == wn) {
+            row_tot[0][wm * TM + j * 16 + lane] = ss[j];
+            row_tot[1][wm * TM + j * 16 + lane] = sa[j];
+          }
         }
       }
       __syncthreads();
 #pragma unroll
       for (int j = 0; j < FM; ++j) {
-        float t0 = 0.f, t1 = 0.f;
-#pragma unroll
-        for (int w = 0; w < WN; ++w) {
-          t0 += part[w][0][wm * TM + j * 16 + lrow];
-          t1 += part[w][1][wm * TM + j * 16 + lrow];
-        }
-        ss[j] = t0;
-        sa[j] = t1;
+        ss[j] = row_tot[0][wm * TM + j * 16 + lrow];
+        sa[j] = row_tot[1][wm * TM + j * 16 + lrow];
       }
     }
   }
@@ -288,7 +324,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // (fragment fully inside the output) or the guarded edge store, and the
   // optional per-column vector is dispatched once for the whole tile.
   const int n_lane = (lane >> 4) * 4;
-  auto epilogue = [&](auto vec_tag) {
+  auto epilogue = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
@@ -389,7 +425,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
     off0[i] = f < A_FRAGS ? (unsigned)((f * 16 + lrow) * lda * 2 + lk * 2)
                           : (unsigned)((f - A_FRAGS) * nkb * kFragBytes + lane * 16);
   }
-  auto load_half = [&](int kb) {
+  auto load_half = [&](int kb) __attribute__((always_inline)) {
     char* st = smem + (kb % STAGES) * STAGE;
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
@@ -413,7 +449,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
   for (int j = 0; j < FM; ++j) ss[j] = sa[j] = 0.f;
   bf16x8 af[FM], wf[FN];
 
-  auto read_block = [&](int kb) {
+  auto read_block = [&](int kb) __attribute__((always_inline)) {
     const char* st = smem + (kb % STAGES) * STAGE;
 #pragma unroll
     for (int j = 0; j < FM; ++j)
@@ -423,7 +459,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
       wf[i] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + (wn * FN + i) * kFragBytes + lane * 16);
   };
   // The 4 waves of a group share its rows and take turns squaring them.
-  auto multiply = [&](int kb) {
+  auto multiply = [&](int kb) __attribute__((always_inline)) {
     const bool stats = (kb % WN) == wn;
 #pragma unroll
     for (int i = 0; i < FN; ++i) {
@@ -439,7 +475,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
       }
     }
   };
-  auto barrier = [&]() {
+  auto barrier = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
   };
@@ -501,7 +537,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
   }
 
   const int n_lane = (lane >> 4) * 4;
-  auto epilogue = [&](auto vec_tag) {
+  auto epilogue = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
