@@ -52,7 +52,9 @@ typedef enum {
   FN_ERR_VALUE = -6,       /* eps negative or not finite; unknown layout or path */
   FN_ERR_HIP = -7,         /* the HIP runtime reported an error while launching */
   FN_ERR_ALIAS = -8,       /* the output overlaps an input */
-  FN_ERR_SIZE = -9         /* a tensor exceeds the 32-bit byte extents the kernels address */
+  FN_ERR_SIZE = -9         /* a tensor exceeds the 32-bit byte extents the kernels address
+                              (leading dimensions and K above 2^21, M or N above 2^30,
+                              or a packed weight buffer of 2^31 bytes or more) */
 } fn_status;
 
 typedef enum { FN_F32 = 0, FN_BF16 = 1 } fn_dtype;
@@ -80,7 +82,8 @@ typedef enum { FN_PATH_AUTO = 0, FN_PATH_PREFILL = 1, FN_PATH_DECODE = 2 } fn_pa
 
 /* Bytes of the packed weight buffer that fold_weights writes for a logical
  * weight with K rows and N columns (N = 2F for FN_LAYOUT_GLU) stored as
- * ws_dtype.  Returns 0 for invalid arguments.  Host only; no device work. */
+ * ws_dtype.  Returns 0 for invalid arguments and for buffers of 2^31 bytes or
+ * more (FN_ERR_SIZE).  Host only; no device work. */
 size_t fold_weights_size(int64_t K, int64_t N, int layout, int ws_dtype);
 
 /* Fold the normalisation weights into the linear layer, once, offline

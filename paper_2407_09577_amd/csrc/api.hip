@@ -13,6 +13,13 @@ using fn::EpiArgs;
 
 constexpr int64_t kMaxLd = int64_t(1) << 21;    // leading dimensions, K (keeps tile extents < 2^31)
 constexpr int64_t kMaxRows = int64_t(1) << 30;  // M, N
+// Packed weight buffer: the matrix-core kernels address it with 32-bit byte
+// offsets and use offsets >= 2^31 as out-of-range (zero-returning) loads.
+constexpr int64_t kMaxPackedBytes = (int64_t(1) << 31) - 1;
+
+int64_t packed_bytes(int64_t K, int64_t N, bool glu, int64_t elem) {
+  return fn::packed_rows(K) * fn::packed_cols(N, glu) * elem;
+}
 
 bool dtype_ok(int d) { return d == FN_F32 || d == FN_BF16; }
 int64_t elem_size(int d) { return d == FN_BF16 ? 2 : 4; }
@@ -72,6 +79,8 @@ int validate_op(const OpDesc& d, int y_dtype) {
   if (d.ncols <= 0 || d.ncols > kMaxRows) return FN_ERR_SHAPE;
   s = check_matrix(d.y, d.M, d.ncols, d.ldy, d.dtype, true);
   if (s) return s;
+  if (packed_bytes(d.K, d.glu ? 2 * d.ncols : d.ncols, d.glu, elem_size(d.dtype)) > kMaxPackedBytes)
+    return FN_ERR_SIZE;
   if (!d.ws) return FN_ERR_NULL;
   if (!aligned16(d.ws)) return FN_ERR_ALIGN;
   s = check_eps(d.ep.eps);
@@ -125,7 +134,8 @@ size_t fold_weights_size(int64_t K, int64_t N, int layout, int ws_dtype) {
   if (K <= 0 || N <= 0 || K > kMaxLd || N > kMaxRows || !dtype_ok(ws_dtype)) return 0;
   if (layout != FN_LAYOUT_LINEAR && layout != FN_LAYOUT_GLU) return 0;
   if (layout == FN_LAYOUT_GLU && N % 2) return 0;
-  return (size_t)(fn::packed_rows(K) * fn::packed_cols(N, layout == FN_LAYOUT_GLU) * elem_size(ws_dtype));
+  const int64_t bytes = packed_bytes(K, N, layout == FN_LAYOUT_GLU, elem_size(ws_dtype));
+  return bytes > kMaxPackedBytes ? 0 : (size_t)bytes;
 }
 
 int fold_weights(const void* W, int64_t ldw, int w_dtype, const float* g, const float* beta, int64_t K,
@@ -135,6 +145,7 @@ int fold_weights(const void* W, int64_t ldw, int w_dtype, const float* g, const 
   if (layout != FN_LAYOUT_LINEAR && layout != FN_LAYOUT_GLU) return FN_ERR_VALUE;
   if (K <= 0 || N <= 0 || ldw < N || (layout == FN_LAYOUT_GLU && N % 2)) return FN_ERR_SHAPE;
   if (K > kMaxLd || N > kMaxRows) return FN_ERR_SIZE;
+  if (packed_bytes(K, N, layout == FN_LAYOUT_GLU, elem_size(ws_dtype)) > kMaxPackedBytes) return FN_ERR_SIZE;
   if (!W || !W_star) return FN_ERR_NULL;
   if (c_star && !beta) return FN_ERR_NULL;
   if (layout == FN_LAYOUT_GLU && (colsum || c_star)) return FN_ERR_UNSUPPORTED;
@@ -152,6 +163,7 @@ int unpack_weights(const void* W_star, int64_t K, int64_t N, int layout, int ws_
   if (layout != FN_LAYOUT_LINEAR && layout != FN_LAYOUT_GLU) return FN_ERR_VALUE;
   if (K <= 0 || N <= 0 || ldo < N || (layout == FN_LAYOUT_GLU && N % 2)) return FN_ERR_SHAPE;
   if (K > kMaxLd || N > kMaxRows) return FN_ERR_SIZE;
+  if (packed_bytes(K, N, layout == FN_LAYOUT_GLU, elem_size(ws_dtype)) > kMaxPackedBytes) return FN_ERR_SIZE;
   if (!W_star || !out) return FN_ERR_NULL;
   if (!aligned16(W_star) || (reinterpret_cast<uintptr_t>(out) % elem_size(ws_dtype))) return FN_ERR_ALIGN;
   const int64_t wsb = (int64_t)fold_weights_size(K, N, layout, ws_dtype);

@@ -40,9 +40,11 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
   const int KB = KP / kKB;
 
   const __amdgpu_buffer_rsrc_t rs_a = make_rsrc(a, (uint32_t)(((int64_t)(M - 1) * lda + K) * 2));
-  const int cbs_valid = min(NCB, NP / 16 - cb0);
+  // Column blocks past the packed width (last workgroup only) read the next k
+  // block's fragments, or zeros past the end; their outputs are never stored.
+  const int npb = NP / 16;
   const __amdgpu_buffer_rsrc_t rs_w =
-      make_rsrc(ws + (int64_t)cb0 * KB * (kFragBytes / 2), (uint32_t)(cbs_valid * KB * kFragBytes));
+      make_rsrc(ws + (int64_t)cb0 * (kFragBytes / 2), (uint32_t)(((int64_t)KB * npb - cb0) * kFragBytes));
 
   const int lrow = lane & 15;
   const int lk = (lane >> 4) * 8;
@@ -64,7 +66,7 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
       af[u] = load_buf16(rs_a, (kb_ok && row_ok && k < K) ? a_row_off + (unsigned)k * 2 : kOobOffset);
 #pragma unroll
       for (int c = 0; c < NCB; ++c)
-        wf[u][c] = load_buf16(rs_w, kb_ok ? (unsigned)((c * KB + kb) * kFragBytes + lane * 16) : kOobOffset);
+        wf[u][c] = load_buf16(rs_w, kb_ok ? (unsigned)((kb * npb + c) * kFragBytes + lane * 16) : kOobOffset);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -152,12 +154,18 @@ template <int EPI>
 static hipError_t launch_decode_epi(const DecodeArgs& p) {
   switch (p.cfg) {
     case 0:
+    case 3: return launch_decode_cfg<2, 2, 8, EPI>(p);
     case 1: return launch_decode_cfg<2, 8, 8, EPI>(p);
     case 2: return launch_decode_cfg<2, 4, 8, EPI>(p);
-    case 3: return launch_decode_cfg<2, 16, 4, EPI>(p);
-    case 4: return launch_decode_cfg<4, 8, 4, EPI>(p);
-    case 5: return launch_decode_cfg<2, 8, 4, EPI>(p);
-    case 6: return launch_decode_cfg<2, 16, 8, EPI>(p);
+    case 4: return launch_decode_cfg<2, 2, 4, EPI>(p);
+    case 5: return launch_decode_cfg<2, 2, 16, EPI>(p);
+    case 6: return launch_decode_cfg<2, 1, 8, EPI>(p);
+    case 7: return launch_decode_cfg<2, 1, 16, EPI>(p);
+    case 8: return launch_decode_cfg<4, 2, 8, EPI>(p);
+    case 9: return launch_decode_cfg<4, 1, 8, EPI>(p);
+    case 10: return launch_decode_cfg<2, 4, 2, EPI>(p);
+    case 11: return launch_decode_cfg<4, 4, 4, EPI>(p);
+    case 12: return launch_decode_cfg<2, 1, 4, EPI>(p);
   }
   return hipErrorInvalidValue;
 }

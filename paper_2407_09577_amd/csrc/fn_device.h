@@ -6,13 +6,16 @@
 // 32*(f/16) + f%16 and up feature f to 32*(f/16) + 16 + f%16, so a gate block of
 // 16 columns is immediately followed by its up block).  Packed columns are padded
 // to NP (a multiple of 16) and rows to KP (a multiple of 64) with zeros.  The
-// packed buffer is a sequence of 1 KiB fragments, column-block major:
+// packed buffer is a sequence of 1 KiB fragments, k-block major:
 //   fragment (cb, kb) = columns [16 cb, 16 cb + 16) x rows [32 kb, 32 kb + 32),
-//   at byte offset (cb * KP/32 + kb) * 1024; inside it, lane L = 16 * ((k%32)/8) + p%16
+//   at byte offset (kb * NP/16 + cb) * 1024; inside it, lane L = 16 * ((k%32)/8) + p%16
 //   holds the 8 consecutive rows k..k+7 (k%8 == 0) of column p as 16 bytes.
 // That is exactly the per-lane operand of one v_mfma_f32_16x16x32_bf16, so a
 // wave moves a fragment global -> LDS -> registers with one 16-byte access per
-// lane, and a column block's whole K extent is one contiguous stream.
+// lane.  All column blocks of one 32-row k block are contiguous, so workgroups
+// that advance through K together read one contiguous region at a time (spread
+// over every HBM channel), and a prefill tile's weight columns for one k block
+// are one contiguous run.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -96,8 +99,6 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-__device__ __forceinline__ float bf16_lo(unsigned w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(unsigned w) { return __uint_as_float(w & 0xffff0000u); }
 
 // fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ unsigned f32_to_bf16_bits(float f) {
@@ -119,6 +120,26 @@ __device__ __forceinline__ float sumsq8(const bf16x8& v, float acc) {
   acc = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, acc, false);
   acc = __builtin_amdgcn_fdot2_f32_bf16(p3, p3, acc, false);
   return acc;
+}
+
+// bf16 halves of a 32-bit word, widened exactly to fp32.
+__device__ __forceinline__ float bf16_lo(unsigned w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(unsigned w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Pair q (elements 2q, 2q+1) of an 8-element fragment: acc + v[2q]^2 + v[2q+1]^2,
+// and acc + v[2q] + v[2q+1].  The bf16 values are widened exactly to fp32 (a
+// shift and a mask) and accumulated with plain fp32 multiply-adds: unlike the
+// bf16 dot instructions, these issue alongside the matrix-core ops of the
+// other waves on the SIMD instead of taking matrix-core issue cycles.
+__device__ __forceinline__ float sumsq2(const bf16x8& v, int q, float acc) {
+  const unsigned w = __builtin_bit_cast(u32x4, v)[q];
+  const float lo = bf16_lo(w), hi = bf16_hi(w);
+  return fmaf(hi, hi, fmaf(lo, lo, acc));
+}
+
+__device__ __forceinline__ float sum2(const bf16x8& v, int q, float acc) {
+  const unsigned w = __builtin_bit_cast(u32x4, v)[q];
+  return acc + bf16_lo(w) + bf16_hi(w);
 }
 
 __device__ __forceinline__ float sum8(const bf16x8& v, float acc) {

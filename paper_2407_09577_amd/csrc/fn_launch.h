@@ -25,6 +25,8 @@ enum Tile : int {
   TILE_PP_256x256 = 10,   // ping-pong: 2 groups of 4 waves of 128 x 64
   TILE_PP_256x128 = 11,   // ping-pong: 2 groups of 4 waves of 128 x 32
   TILE_PP_128x256 = 12,   // ping-pong: 2 groups of 4 waves of 64 x 64
+  TILE_256x256_W8_PF = 13,  // 8 waves of 128 x 64, 4-stage ring, register prefetch
+  TILE_256x256_W8_PF5 = 14, // 8 waves of 128 x 64, 5-stage ring, register prefetch
   TILE_COUNT
 };
 
@@ -65,7 +67,7 @@ struct DecodeArgs {
   hipStream_t stream;
 };
 hipError_t launch_decode_bf16(const DecodeArgs& p);
-constexpr int kDecodeCfgCount = 7;
+constexpr int kDecodeCfgCount = 13;
 
 struct F32Args {
   const float* a;

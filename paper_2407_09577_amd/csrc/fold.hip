@@ -50,12 +50,12 @@ __device__ __forceinline__ double load_w(const void* W, int64_t idx, int w_dtype
 // fragment-major bf16 layout.
 __global__ void fold_pack_bf16_kernel(const void* __restrict__ W, int64_t ldw, int w_dtype,
                                       const float* __restrict__ g, int64_t K, int64_t N, int glu,
-                                      int64_t KB, int64_t nchunks, u32x4* __restrict__ out) {
+                                      int64_t NPB, int64_t nchunks, u32x4* __restrict__ out) {
   const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= nchunks) return;
   const int64_t frag = c / 64;
   const int lane = (int)(c % 64);
-  const int64_t cb = frag / KB, kb = frag % KB;
+  const int64_t kb = frag / NPB, cb = frag % NPB;
   const int64_t p = cb * 16 + (lane & 15);
   const int64_t k0 = kb * kKB + (lane >> 4) * 8;
   const int64_t n = logical_col(p, N, glu);
@@ -88,8 +88,7 @@ __global__ void fold_pack_f32_kernel(const void* __restrict__ W, int64_t ldw, in
 __device__ __forceinline__ double packed_at(const void* ws, int ws_dtype, int64_t k, int64_t p,
                                             int64_t KP, int64_t NP) {
   if (ws_dtype == kDtypeBf16) {
-    const int64_t KB = KP / kKB;
-    const int64_t off = ((p / 16) * KB + k / kKB) * 512 + (((k % kKB) / 8) * 16 + p % 16) * 8 + k % 8;
+    const int64_t off = ((k / kKB) * (NP / 16) + p / 16) * 512 + (((k % kKB) / 8) * 16 + p % 16) * 8 + k % 8;
     const unsigned short b = reinterpret_cast<const unsigned short*>(ws)[off];
     return (double)__uint_as_float((unsigned)b << 16);
   }
@@ -120,8 +119,7 @@ __global__ void unpack_kernel(const void* __restrict__ ws, int ws_dtype, int64_t
   const int64_t n = logical_col(p, N, glu);
   if (n < 0) return;
   if (ws_dtype == kDtypeBf16) {
-    const int64_t KB = KP / kKB;
-    const int64_t off = ((p / 16) * KB + k / kKB) * 512 + (((k % kKB) / 8) * 16 + p % 16) * 8 + k % 8;
+    const int64_t off = ((k / kKB) * (NP / 16) + p / 16) * 512 + (((k % kKB) / 8) * 16 + p % 16) * 8 + k % 8;
     reinterpret_cast<unsigned short*>(out)[k * ldo + n] = reinterpret_cast<const unsigned short*>(ws)[off];
   } else {
     reinterpret_cast<float*>(out)[k * ldo + n] = reinterpret_cast<const float*>(ws)[k * NP + p];
@@ -135,7 +133,7 @@ hipError_t launch_fold(const FoldArgs& p) {
   if (p.ws_dtype == kDtypeBf16) {
     const int64_t nchunks = KP * NP / 8;
     hipLaunchKernelGGL(fold_pack_bf16_kernel, dim3(blocks_for(nchunks, 256)), dim3(256), 0, p.stream, p.W,
-                       p.ldw, p.w_dtype, p.g, p.K, p.N, p.glu, KP / kKB, nchunks,
+                       p.ldw, p.w_dtype, p.g, p.K, p.N, p.glu, NP / 16, nchunks,
                        reinterpret_cast<u32x4*>(p.ws));
   } else {
     hipLaunchKernelGGL(fold_pack_f32_kernel, dim3(blocks_for(KP * NP, 256)), dim3(256), 0, p.stream, p.W,

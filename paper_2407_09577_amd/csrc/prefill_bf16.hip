@@ -6,12 +6,12 @@
 // memory traffic).
 //
 // Work decomposition.  A workgroup owns a BM x BN output tile (BM activation
-// rows x BN packed weight columns) and walks K in steps of 64.  Each step moves
-// the activation tile (BM/16 x 2 fragments) and the weight tile (BN/16 x 2
-// fragments) straight from HBM into LDS with range-checked buffer loads (rows
-// past M, columns past N and k past K read as zero), double buffered, so the
-// loads of step t+1 are in flight while the matrix cores work on step t.  The
-// WM x WN waves each own a (BM/WM) x (BN/WN) sub-tile.  The matrix multiply runs
+// rows x BN packed weight columns) and walks K in blocks of 32.  Each block's
+// activation fragments (BM/16) and weight fragments (BN/16) move straight from
+// HBM into an LDS ring of STAGES blocks with range-checked buffer loads (rows
+// past M, columns past N and k past K read as zero), issued several blocks
+// ahead of the matrix cores.  The WM x WN waves each own a (BM/WM) x (BN/WN)
+// sub-tile.  The matrix multiply runs
 // transposed, D' = W*^T a^T, so that one lane's four accumulators are four
 // consecutive output columns of one row, and the lane that squares an
 // activation fragment holds exactly the row whose outputs it scales.
@@ -127,14 +127,17 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   const i32x4 rs_a = make_rsrc_sgpr(a + (int64_t)m0 * lda,
                                     (uint32_t)(((int64_t)(rows_valid - 1) * lda + K) * 2));
   const int cb0 = p0 / 16;
-  const int cbs_valid = min(BN / 16, NP / 16 - cb0);
-  const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * nkb * (kFragBytes / 2),
-                                    (uint32_t)(cbs_valid * nkb * kFragBytes));
+  const int npb = NP / 16;  // column blocks per k block of the packed weight
+  const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * (kFragBytes / 2),
+                                    (uint32_t)(((int64_t)nkb * npb - cb0) * kFragBytes));
 
   // Fragment f of a stage: f < A_FRAGS is activation row block f, otherwise weight
   // column block f - A_FRAGS.  Wave w moves fragments w, w + NW, ...
   const int lrow = lane & 15;
   const int lk = (lane >> 4) * 8;
+  // Weight column blocks past the packed width (last column tile only) read the
+  // next k block's fragments, or zeros past the buffer's end; the columns they
+  // feed lie beyond every output column and are never stored.
   unsigned off0[LOADS];
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
@@ -142,7 +145,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     if (A_FRAGS % NW == 0 ? i < A_FRAGS / NW : f < A_FRAGS)
       off0[i] = (unsigned)((f * 16 + lrow) * lda * 2 + lk * 2);
     else
-      off0[i] = (unsigned)((f - A_FRAGS) * nkb * kFragBytes + lane * 16);
+      off0[i] = (unsigned)((f - A_FRAGS) * kFragBytes + lane * 16);
   }
 
   // Transfer i of block kb into its ring slot.  Every wave issues exactly LOADS
@@ -158,7 +161,8 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       const bool ok = kb * kKB + lk < K;
       load_lds16(rs_a, st + f * kFragBytes, ok ? off0[i] + kb * (kKB * 2) : kOobOffset);
     } else if (!kUneven || f < T_FRAGS) {
-      load_lds16(rs_w, st + f * kFragBytes, kb < nkb ? off0[i] + kb * kFragBytes : kOobOffset);
+      load_lds16(rs_w, st + f * kFragBytes,
+                 kb < nkb ? off0[i] + (unsigned)(kb * npb) * kFragBytes : kOobOffset);
     } else {
       load_lds16(rs_w, smem + STAGES * STAGE, kOobOffset);
     }
@@ -185,10 +189,15 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       wf[r - FM] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + (wn * FN + r - FM) * kFragBytes + lane * 16);
   };
 
-  // Row statistics of fragment j (squares, and sums for LayerNorm).
+  // Row statistics of fragment j (squares, and sums for LayerNorm), whole or
+  // one element pair q at a time.
   auto stats_one = [&](int j, const bf16x8 (&af)[FM]) __attribute__((always_inline)) {
     if constexpr (kSS) ss[j] = sumsq8(af[j], ss[j]);
     if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
+  };
+  auto stats_pair = [&](int j, int q, const bf16x8 (&af)[FM]) __attribute__((always_inline)) {
+    if constexpr (kSS) ss[j] = sumsq2(af[j], q, ss[j]);
+    if constexpr (kSA) sa[j] = sum2(af[j], q, sa[j]);
   };
 
   auto sync_block = [&]() __attribute__((always_inline)) {
@@ -198,12 +207,14 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 
   // One k block of work for the matrix cores, issued as NRD groups: group g
   // holds its share of the NMF matrix-core ops, LDS read g of the next block
-  // (PF), transfer g of block kb+STAGES-1 (g < LOADS) and the row statistics of
-  // activation fragment g (g < FM).  The scheduling fences keep this
-  // interleaving, so memory traffic overlaps the matrix cores.
+  // (PF), transfer g of block kb+STAGES (g < LOADS) and a share of the row
+  // statistics.  The scheduling fences keep this interleaving, so memory
+  // traffic overlaps the matrix cores.
   // Row statistics are split across the WN waves of a row band at compile time:
   // the wave with column index WNC squares activation fragments j = WNC + WN t,
-  // over the whole of K, so no wave branches on whose turn it is.
+  // over the whole of K, so no wave branches on whose turn it is.  Its NOWN
+  // fragments x 4 element pairs are dealt round-robin over the groups, so
+  // consecutive accumulations into one row total sit groups apart.
   auto multiply_interleaved = [&](auto wnc, int kb, const bf16x8 (&afc)[FM], const bf16x8 (&wfc)[FN],
                                   bf16x8 (&afn)[FM], bf16x8 (&wfn)[FN], bool more)
                                   __attribute__((always_inline)) {
@@ -216,42 +227,49 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wfc[i], afc[j], acc[i][j], 0, 0, 0);
       }
       if (more) {
-        if (g < LOADS) load_one(kb + STAGES - 1, g);
+        if (g < LOADS) load_one(kb + STAGES, g);
         read_one(kb + 1, g, afn, wfn);
       }
-      if (WNC + WN * g < FM) stats_one(WNC + WN * g, afc);  // resolved when unrolled
+      constexpr int NOWN = (FM - WNC + WN - 1) / WN;
+#pragma unroll
+      for (int idx = g; idx < NOWN * 4; idx += NRD)  // resolved when unrolled
+        stats_pair(WNC + WN * (idx % NOWN), idx / NOWN, afc);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // Ring discipline.  Block kb lives in slot kb % STAGES; global->LDS transfers
-  // run STAGES-1 blocks ahead of the matrix cores.
-  //  PF: LDS->register reads run one block ahead of the matrix cores.  Step kb
-  //   waits until block kb+1 has landed (the STAGES-3 blocks after it may stay
-  //   outstanding) and for this wave's reads of block kb; the barrier then makes
-  //   block kb+1 visible to all waves and guarantees every wave has finished
-  //   reading block kb-1, whose slot the transfer of block kb+STAGES-1 overwrites.
-  //  !PF: step kb waits for block kb, barriers, then reads and multiplies it.
+  // Ring discipline.  Block kb lives in slot kb % STAGES.
+  //  PF: LDS->register reads run one block ahead of the matrix cores, and
+  //   global->LDS transfers STAGES blocks ahead.  Before step kb every wave
+  //   waits until its transfers of block kb+1 have landed (those of the
+  //   STAGES-2 blocks after it may stay outstanding) and for its own reads of
+  //   block kb; the barrier then makes block kb+1 visible to all waves and
+  //   guarantees that every wave has finished reading block kb, whose slot the
+  //   transfer of block kb+STAGES issued during step kb overwrites.
+  //  !PF: transfers run STAGES-1 blocks ahead; step kb waits for block kb,
+  //   barriers (every wave is done with block kb-1, whose slot block
+  //   kb+STAGES-1 takes), then reads and multiplies block kb.
+  static_assert(!PF || (STAGES - 1) * LOADS < 64, "vmcnt range");
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
+  for (int s = 0; s < (PF ? STAGES : STAGES - 1); ++s)
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) load_one(s, i);
   auto mainloop = [&](auto wnc) __attribute__((always_inline)) {
     constexpr int WNC = decltype(wnc)::value;
     if constexpr (PF) {
-      wait_vmcnt<(STAGES - 2) * LOADS>();
+      wait_vmcnt<(STAGES - 1) * LOADS>();
       sync_block();
 #pragma unroll
       for (int r = 0; r < NRD; ++r) read_one(0, r, af0, wf0);
       for (int kb = 0; kb < nkb - 2; kb += 2) {
-        wait_vmcnt<(STAGES - 3) * LOADS>();
+        wait_vmcnt<(STAGES - 2) * LOADS>();
         sync_block();
         multiply_interleaved(wnc, kb, af0, wf0, af1, wf1, true);
-        wait_vmcnt<(STAGES - 3) * LOADS>();
+        wait_vmcnt<(STAGES - 2) * LOADS>();
         sync_block();
         multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true);
       }
-      wait_vmcnt<(STAGES - 3) * LOADS>();
+      wait_vmcnt<(STAGES - 2) * LOADS>();
       sync_block();
       multiply_interleaved(wnc, nkb - 2, af0, wf0, af1, wf1, true);
       __builtin_amdgcn_s_waitcnt(0xc07f);
@@ -301,7 +319,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       }
     }
     if constexpr (WN > 1) {
-      __shared__ float row_tot[2][BM];
+      // The totals reuse the ring: wait for this wave's last (zero-filling)
+      // transfers, and for every wave to finish reading the last block.
+      static_assert(STAGES * STAGE >= 2 * BM * (int)sizeof(float), "ring too small for row totals");
+      float (*row_tot)[BM] = reinterpret_cast<float (*)[BM]>(smem);
+      wait_vmcnt<0>();
+      __syncthreads();
       if (lane < 16) {
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
@@ -410,9 +433,9 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
   const i32x4 rs_a = make_rsrc_sgpr(a + (int64_t)m0 * lda,
                                     (uint32_t)(((int64_t)(rows_valid - 1) * lda + K) * 2));
   const int cb0 = p0 / 16;
-  const int cbs_valid = min(BN / 16, NP / 16 - cb0);
-  const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * nkb * (kFragBytes / 2),
-                                    (uint32_t)(cbs_valid * nkb * kFragBytes));
+  const int npb = NP / 16;  // column blocks per k block of the packed weight
+  const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * (kFragBytes / 2),
+                                    (uint32_t)(((int64_t)nkb * npb - cb0) * kFragBytes));
 
   const int lrow = lane & 15;
   const int lk = (lane >> 4) * 8;
@@ -423,7 +446,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
   for (int i = 0; i < LOADS; ++i) {
     const int f = wm * HALF + wn + WN * i;
     off0[i] = f < A_FRAGS ? (unsigned)((f * 16 + lrow) * lda * 2 + lk * 2)
-                          : (unsigned)((f - A_FRAGS) * nkb * kFragBytes + lane * 16);
+                          : (unsigned)((f - A_FRAGS) * kFragBytes + lane * 16);
   }
   auto load_half = [&](int kb) __attribute__((always_inline)) {
     char* st = smem + (kb % STAGES) * STAGE;
@@ -434,7 +457,8 @@ __global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
         const bool ok = kb * kKB + lk < K;
         load_lds16(rs_a, st + f * kFragBytes, ok ? off0[i] + kb * (kKB * 2) : kOobOffset);
       } else {
-        load_lds16(rs_w, st + f * kFragBytes, kb < nkb ? off0[i] + kb * kFragBytes : kOobOffset);
+        load_lds16(rs_w, st + f * kFragBytes,
+                   kb < nkb ? off0[i] + (unsigned)(kb * npb) * kFragBytes : kOobOffset);
       }
     }
   };
@@ -599,10 +623,11 @@ static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
 template <int EPI>
 static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   // Shape-specialised tiles (measured on MI355X): the 256 x 256 tile with 8 waves
-  // when it still yields at least one tile per compute unit, 128 x 128 otherwise.
+  // and register prefetch when it still yields at least one tile per compute
+  // unit, 128 x 128 otherwise.
   const int64_t big = ((int64_t)(p.M + 255) / 256) * ((p.NP + 255) / 256);
   int tile = p.tile;
-  if (tile == TILE_AUTO) tile = big >= 256 ? TILE_256x256_W8 : TILE_128x128;
+  if (tile == TILE_AUTO) tile = big >= 256 ? TILE_256x256_W8_PF : TILE_128x128;
   switch (tile) {
     case TILE_256x256: return launch_prefill_cfg<256, 256, 2, 2, 4, true, EPI>(p);
     case TILE_128x128: return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
@@ -616,6 +641,8 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
     case TILE_PP_256x256: return launch_pingpong_cfg<256, 256, 4, EPI>(p);
     case TILE_PP_256x128: return launch_pingpong_cfg<256, 128, 4, EPI>(p);
     case TILE_PP_128x256: return launch_pingpong_cfg<128, 256, 4, EPI>(p);
+    case TILE_256x256_W8_PF: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI>(p);
+    case TILE_256x256_W8_PF5: return launch_prefill_cfg<256, 256, 2, 4, 5, true, EPI>(p);
   }
   return hipErrorInvalidValue;
 }

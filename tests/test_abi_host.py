@@ -60,6 +60,10 @@ def test_fold_weights_size(fnlib):
     assert f(16, 7, 1, 1) == 0          # GLU needs an even column count
     assert f(16, 16, 2, 1) == 0          # unknown layout
     assert f(16, 16, 0, 7) == 0          # unknown dtype
+    # packed buffers of 2^31 bytes or more are beyond the kernels' 32-bit offsets
+    assert f(1 << 15, (1 << 15) - 16, 0, 1) == (1 << 15) * ((1 << 15) - 16) * 2
+    assert f(1 << 15, 1 << 15, 0, 1) == 0
+    assert f(1 << 15, 1 << 14, 0, 0) == 0
 
 
 # Fake but aligned, non-null device addresses: validation never dereferences them.
@@ -93,6 +97,7 @@ def test_linear_validation(fnlib):
     assert _lin(lib, adt=0, ydt=0, path=2) == -5   # decode path is bf16 only
     assert _lin(lib, y=A + 64) == -8               # output overlaps the activations
     assert _lin(lib, lda=1 << 22, K=64) == -9
+    assert _lin(lib, K=1 << 15, lda=1 << 15, N=1 << 15, ldy=1 << 15) == -9   # 2 GiB packed weight
     # M == 0 is a no-op that never touches the device, even with null tensors
     assert _lin(lib, M=0, a=0, y=0) == 0
 
@@ -126,6 +131,7 @@ def test_fold_validation(fnlib):
     assert f(layout=1, colsum=X) == -5             # LayerNorm extras: linear layout only
     assert f(ws=W + 4) == -4
     assert f(ws=A + 16) == -8                      # packed output overlaps W
+    assert f(K=1 << 15, N=1 << 15, ldw=1 << 15) == -9
     u = lambda **kw: lib.unpack_weights(kw.get("ws", W), 64, 32, 0, 1, kw.get("out", Y), kw.get("ldo", 32), None)
     assert u(ws=0) == -1
     assert u(ldo=8) == -2

@@ -284,8 +284,8 @@ def test_non_contiguous_activation_rows(fn):
 
 
 # ------------------------------------------------------------------ every kernel configuration
-PREFILL_TILES = list(range(1, 13))   # forced through the high byte of the path argument
-DECODE_CFGS = [1, 2, 3, 4, 5, 6]
+PREFILL_TILES = list(range(1, 15))   # forced through the high byte of the path argument
+DECODE_CFGS = list(range(1, 13))
 
 
 @pytest.mark.parametrize("tile", PREFILL_TILES)
