@@ -4,15 +4,16 @@
 // once (Sec. 6 and App. "End-to-end validation": decode is memory-bound and
 // wants its own kernel instead of a padded prefill tile).  A workgroup owns NCB
 // packed column blocks of 16 columns (for a GLU, whole gate/up block pairs) and
-// its KSPLIT waves split K: wave w takes the 32-row fragments w, w + KSPLIT, ...
-// so the waves of one workgroup read adjacent 1 KiB fragments.  Each fragment is
-// one 16-byte load per lane, fed directly to a 16x16x32 bf16 matrix-core op
-// together with the matching 16-row activation fragment (rows >= M read as
-// zero), so the arithmetic costs nothing next to the stream.  The squares of
-// the activation fragments are summed on the way (Cor. 1), the per-wave
-// partial products and sums are combined in LDS in a fixed order
-// (deterministic), and one wave per output block applies the deferred scale and
-// the epilogue.
+// its KSPLIT waves split K: wave w takes the 32-row k blocks w, w + KSPLIT, ...
+// Each weight fragment is one 16-byte load per lane (non-temporal: it is read
+// exactly once), fed directly to a 16x16x32 bf16 matrix-core op together with
+// the matching 16-row activation fragment (rows >= M read as zero), so the
+// arithmetic costs nothing next to the stream.  Loads go in sets of U k blocks,
+// optionally double buffered so the next set is in flight while the current
+// one is consumed.  The squares of the activation fragments are summed on the
+// way (Cor. 1); with several waves the partial products and sums are combined
+// in LDS in a fixed order (deterministic), and the lanes holding a row's
+// totals apply the deferred scale and the epilogue.
 #include <type_traits>
 
 #include "fn_device.h"
@@ -21,7 +22,7 @@
 
 namespace fn {
 
-template <int NCB, int KSPLIT, int U, int EPI>
+template <int NCB, int KSPLIT, int U, bool DB, int CPOL, int EPI>
 __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep) {
@@ -30,9 +31,10 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
   constexpr int NOUT = epi_is_glu(EPI) ? NCB / 2 : NCB;  // output blocks per workgroup
   static_assert(!epi_is_glu(EPI) || NCB % 2 == 0, "GLU needs gate/up block pairs");
 
-  __shared__ f32x4 red[KSPLIT][NCB][64];
-  __shared__ float red_ss[KSPLIT][16];
-  __shared__ float red_sa[KSPLIT][16];
+  // Per-wave partials for the cross-wave combine (unused with one wave).
+  __shared__ f32x4 red[KSPLIT > 1 ? KSPLIT : 1][NCB][64];
+  __shared__ float red_ss[KSPLIT > 1 ? KSPLIT : 1][16];
+  __shared__ float red_sa[KSPLIT > 1 ? KSPLIT : 1][16];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -56,8 +58,10 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
   for (int c = 0; c < NCB; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
   float ss = 0.f, sa = 0.f;
 
-  for (int kb0 = wave; kb0 < KB; kb0 += KSPLIT * U) {
-    u32x4 af[U], wf[U][NCB];
+  // One set = U k blocks of this wave (kb, kb + KSPLIT, ...): U activation
+  // fragments and U x NCB weight fragments, one 16-byte load per lane each.
+  // Blocks past K read as zeros.
+  auto load_set = [&](int kb0, u32x4 (&af)[U], u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kb = kb0 + KSPLIT * u;
@@ -66,8 +70,10 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
       af[u] = load_buf16(rs_a, (kb_ok && row_ok && k < K) ? a_row_off + (unsigned)k * 2 : kOobOffset);
 #pragma unroll
       for (int c = 0; c < NCB; ++c)
-        wf[u][c] = load_buf16(rs_w, kb_ok ? (unsigned)((kb * npb + c) * kFragBytes + lane * 16) : kOobOffset);
+        wf[u][c] = load_buf16<CPOL>(rs_w, kb_ok ? (unsigned)((kb * npb + c) * kFragBytes + lane * 16) : kOobOffset);
     }
+  };
+  auto compute_set = [&](const u32x4 (&af)[U], const u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bf16x8 av = __builtin_bit_cast(bf16x8, af[u]);
@@ -77,6 +83,31 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
       for (int c = 0; c < NCB; ++c)
         acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[u][c]), av,
                                                           acc[c], 0, 0, 0);
+    }
+  };
+
+  constexpr int STEP = KSPLIT * U;  // k blocks per set across the workgroup
+  if constexpr (DB) {
+    // Double-buffered register sets: the next set's loads are issued before the
+    // current set is consumed, so every wave keeps a full set in flight.  Sets
+    // past K are issued as zero-returning loads, which keeps the loop uniform.
+    u32x4 af0[U], wf0[U][NCB], af1[U], wf1[U][NCB];
+    load_set(wave, af0, wf0);
+    for (int kb0 = wave; kb0 < KB; kb0 += 2 * STEP) {
+      load_set(kb0 + STEP, af1, wf1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_set(af0, wf0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_set(kb0 + 2 * STEP, af0, wf0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_set(af1, wf1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+    for (int kb0 = wave; kb0 < KB; kb0 += STEP) {
+      u32x4 af[U], wf[U][NCB];
+      load_set(kb0, af, wf);
+      compute_set(af, wf);
     }
   }
 
@@ -88,46 +119,53 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     sa += __shfl_xor(sa, 16);
     sa += __shfl_xor(sa, 32);
   }
+  // Combine the waves' partial products and row sums (a fixed order).  With a
+  // single wave per workgroup every lane already holds its row's totals.
+  if constexpr (KSPLIT > 1) {
 #pragma unroll
-  for (int c = 0; c < NCB; ++c) red[wave][c][lane] = acc[c];
-  if (lane < 16) {
-    red_ss[wave][lane] = ss;
-    red_sa[wave][lane] = sa;
+    for (int c = 0; c < NCB; ++c) red[wave][c][lane] = acc[c];
+    if (lane < 16) {
+      red_ss[wave][lane] = ss;
+      red_sa[wave][lane] = sa;
+    }
+    __syncthreads();
   }
-  __syncthreads();
+  auto total = [&](int c) __attribute__((always_inline)) {
+    if constexpr (KSPLIT == 1) return acc[c];
+    f32x4 v = red[0][c][lane];
+#pragma unroll
+    for (int w = 1; w < KSPLIT; ++w) v += red[w][c][lane];
+    return v;
+  };
 
   const int m = lrow;
   if (m >= M) return;
-  float ss_t = 0.f, sa_t = 0.f;
+  float ss_t = ss, sa_t = sa;
+  if constexpr (KSPLIT > 1) {
+    ss_t = sa_t = 0.f;
 #pragma unroll
-  for (int w = 0; w < KSPLIT; ++w) {
-    ss_t += red_ss[w][m];
-    sa_t += red_sa[w][m];
+    for (int w = 0; w < KSPLIT; ++w) {
+      ss_t += red_ss[w][m];
+      sa_t += red_sa[w][m];
+    }
   }
   const RowStat st = row_stat<EPI>(ss_t, sa_t, ep);
   if constexpr (EPI == EPI_RMS) {
     if (ep.inv_rms && blockIdx.x == 0 && wave == 0 && lane < 16) ep.inv_rms[m] = st.s;
   }
   const int n_lane = (lane >> 4) * 4;
-  auto epilogue = [&](auto vec_tag) {
+  auto epilogue = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
     for (int o = wave; o < NOUT; o += KSPLIT) {
       if constexpr (epi_is_glu(EPI)) {
-        f32x4 g = red[0][2 * o][lane], u = red[0][2 * o + 1][lane];
-#pragma unroll
-        for (int w = 1; w < KSPLIT; ++w) {
-          g += red[w][2 * o][lane];
-          u += red[w][2 * o + 1][lane];
-        }
+        const f32x4 g = total(2 * o), u = total(2 * o + 1);
         const int fb = (cb0 / 2 + o) * 16;
         if (fb + 16 <= ncols)
           store4_bf16_full<EPI, VEC>(y, ldy, m, fb + n_lane, g, u, st, ep);
         else
           store4_bf16_edge<EPI, VEC>(y, ldy, M, ncols, m, fb + n_lane, g, u, st, ep);
       } else {
-        f32x4 v = red[0][o][lane];
-#pragma unroll
-        for (int w = 1; w < KSPLIT; ++w) v += red[w][o][lane];
+        const f32x4 v = total(o);
         const int pb = (cb0 + o) * 16;
         if (pb + 16 <= ncols)
           store4_bf16_full<EPI, VEC>(y, ldy, m, pb + n_lane, v, v, st, ep);
@@ -142,30 +180,34 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     epilogue(std::false_type{});
 }
 
-template <int NCB, int KSPLIT, int U, int EPI>
+template <int NCB, int KSPLIT, int U, int EPI, bool DB = false, int CPOL = 0>
 static hipError_t launch_decode_cfg(const DecodeArgs& p) {
   const int nblocks = (p.NP / 16 + NCB - 1) / NCB;
-  hipLaunchKernelGGL((decode_bf16_kernel<NCB, KSPLIT, U, EPI>), dim3(nblocks), dim3(KSPLIT * 64), 0,
+  hipLaunchKernelGGL((decode_bf16_kernel<NCB, KSPLIT, U, DB, CPOL, EPI>), dim3(nblocks), dim3(KSPLIT * 64), 0,
                      p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y, p.ldy, p.ep);
   return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_decode_epi(const DecodeArgs& p) {
+  // Configurations (NCB column blocks per workgroup, KSPLIT waves, U k blocks
+  // per load set, double-buffered sets, non-temporal weight loads).  Measured on
+  // MI355X (Llama-7B SwiGLU decode, 180 MB of weights): one wave per workgroup,
+  // two blocks per set, double buffered, non-temporal is the fastest for M = 1..16.
   switch (p.cfg) {
     case 0:
-    case 3: return launch_decode_cfg<2, 2, 8, EPI>(p);
-    case 1: return launch_decode_cfg<2, 8, 8, EPI>(p);
-    case 2: return launch_decode_cfg<2, 4, 8, EPI>(p);
-    case 4: return launch_decode_cfg<2, 2, 4, EPI>(p);
-    case 5: return launch_decode_cfg<2, 2, 16, EPI>(p);
-    case 6: return launch_decode_cfg<2, 1, 8, EPI>(p);
-    case 7: return launch_decode_cfg<2, 1, 16, EPI>(p);
-    case 8: return launch_decode_cfg<4, 2, 8, EPI>(p);
-    case 9: return launch_decode_cfg<4, 1, 8, EPI>(p);
-    case 10: return launch_decode_cfg<2, 4, 2, EPI>(p);
-    case 11: return launch_decode_cfg<4, 4, 4, EPI>(p);
-    case 12: return launch_decode_cfg<2, 1, 4, EPI>(p);
+    case 1: return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT>(p);
+    case 2: return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT>(p);
+    case 3: return launch_decode_cfg<2, 2, 2, EPI, true, kCachePolicyNT>(p);
+    case 4: return launch_decode_cfg<2, 2, 4, EPI, true, kCachePolicyNT>(p);
+    case 5: return launch_decode_cfg<2, 1, 8, EPI, true, kCachePolicyNT>(p);
+    case 6: return launch_decode_cfg<4, 1, 2, EPI, true, kCachePolicyNT>(p);
+    case 7: return launch_decode_cfg<4, 1, 4, EPI, true, kCachePolicyNT>(p);
+    case 8: return launch_decode_cfg<2, 2, 8, EPI, false, kCachePolicyNT>(p);
+    case 9: return launch_decode_cfg<2, 2, 8, EPI>(p);
+    case 10: return launch_decode_cfg<2, 4, 4, EPI, true, kCachePolicyNT>(p);
+    case 11: return launch_decode_cfg<8, 1, 2, EPI, true, kCachePolicyNT>(p);
+    case 12: return launch_decode_cfg<2, 1, 1, EPI, true, kCachePolicyNT>(p);
   }
   return hipErrorInvalidValue;
 }

@@ -86,9 +86,14 @@ __device__ __forceinline__ void load_lds16(i32x4 rsrc, const void* lds_base, uns
                : "memory");
 }
 
+// Cache-policy operand of the buffer loads: the non-temporal hint, for data
+// streamed exactly once (the decode weight stream).
+constexpr int kCachePolicyNT = 2;
+
 // 16 bytes per lane from a range-checked buffer into registers.
+template <int CPOL = 0>
 __device__ __forceinline__ u32x4 load_buf16(__amdgpu_buffer_rsrc_t rsrc, unsigned voffset) {
-  return __builtin_amdgcn_raw_buffer_load_b128(rsrc, voffset, 0, 0);
+  return __builtin_amdgcn_raw_buffer_load_b128(rsrc, voffset, 0, CPOL);
 }
 
 // s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding:
