@@ -16,17 +16,17 @@ enum Tile : int {
   TILE_256x256 = 1,       // 4 waves of 128 x 128, 4-stage ring, register prefetch
   TILE_128x128 = 2,       // 4 waves of 64 x 64, 4-stage ring, register prefetch
   TILE_256x256_W8 = 3,    // 8 waves of 128 x 64, 4-stage ring
-  TILE_128x128_S8 = 4,    // 4 waves of 64 x 64, 8-stage ring, register prefetch
+  TILE_128x96_W8 = 4,     // 8 waves of 32 x 48, register prefetch (GLU: 128 x 128)
   TILE_256x128 = 5,       // 4 waves of 128 x 64
   TILE_128x256 = 6,       // 4 waves of 64 x 128
   TILE_128x64 = 7,        // 4 waves of 64 x 32
   TILE_64x128 = 8,        // 4 waves of 32 x 64
   TILE_128x128_NOPF = 9,  // as TILE_128x128 without register prefetch
-  TILE_PP_256x256 = 10,   // ping-pong: 2 groups of 4 waves of 128 x 64
-  TILE_PP_256x128 = 11,   // ping-pong: 2 groups of 4 waves of 128 x 32
-  TILE_PP_128x256 = 12,   // ping-pong: 2 groups of 4 waves of 64 x 64
-  TILE_256x256_W8_PF = 13,  // 8 waves of 128 x 64, 4-stage ring, register prefetch
-  TILE_256x256_W8_PF5 = 14, // 8 waves of 128 x 64, 5-stage ring, register prefetch
+  TILE_256x256_W8_PF = 10,   // 8 waves of 128 x 64, 4-stage ring, register prefetch
+  TILE_256x256_W8_PF5 = 11,  // 8 waves of 128 x 64, 5-stage ring, register prefetch
+  TILE_128x128_W8 = 12,      // 8 waves of 64 x 32, register prefetch
+  TILE_128x128_W8T = 13,     // 8 waves of 32 x 64, register prefetch
+  TILE_128x96 = 14,          // 4 waves of 64 x 48, register prefetch (GLU: 128 x 128)
   TILE_COUNT
 };
 

@@ -385,230 +385,6 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     epilogue(std::false_type{});
 }
 
-// Ping-pong variant: 8 waves in two groups of 4 (group g = wave / 4 owns the
-// rows [g * BM/2, (g+1) * BM/2) of the tile; each wave a (BM/2) x (BN/4)
-// sub-tile).  Waves 0..3 and 4..7 sit on the same four SIMDs, one of each group
-// per SIMD.  The groups run half a step apart: in every interval one group's
-// waves run their matrix-core ops while the other group's waves read the next
-// k block from LDS into registers and issue their half of the global->LDS
-// transfers, so each SIMD's matrix core is fed by alternating waves.  A
-// workgroup barrier ends every interval.
-//   interval 2b  : group 0 reads block b (+ transfers block b+S-1), group 1 multiplies block b-1
-//   interval 2b+1: group 0 multiplies block b, group 1 reads block b (+ its transfers)
-// Block b+S-1 goes to the slot of block b-1, which group 1 finished reading in
-// interval 2b-1.  Before the barrier ending interval 2b+1 every wave waits until
-// its transfers of block b+1 have landed (S-2 later blocks may stay in flight).
-template <int BM, int BN, int STAGES, int EPI>
-__global__ __launch_bounds__(512, 1) void prefill_pingpong_kernel(
-    const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
-    int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep, int tiles_m, int tiles_n) {
-  constexpr int WM = 2, WN = 4;
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 16, FN = TN / 16;
-  constexpr int A_FRAGS = BM / 16, W_FRAGS = BN / 16;
-  constexpr int T_FRAGS = A_FRAGS + W_FRAGS;
-  constexpr int A_BYTES = A_FRAGS * kFragBytes;
-  constexpr int STAGE = T_FRAGS * kFragBytes;
-  constexpr int HALF = T_FRAGS / 2;     // fragments each group transfers per block
-  constexpr int LOADS = HALF / WN;      // transfers per wave per block
-  static_assert(HALF % WN == 0 && A_FRAGS % WN == 0, "transfers must split evenly over a group");
-  static_assert(!epi_is_glu(EPI) || TN % 32 == 0, "GLU needs whole gate/up block pairs per wave");
-  static_assert(STAGES >= 3 && (STAGES - 2) * LOADS < 64, "ring depth / vmcnt range");
-  constexpr bool kSS = epi_needs_ss(EPI);
-  constexpr bool kSA = EPI == EPI_LN;
-
-  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
-
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave / WN, wn = wave % WN;  // wm is the group
-
-  int tm, tn;
-  tile_of_block(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM;
-  const int p0 = tn * BN;
-  const int nkb = KP / kKB;
-
-  const int rows_valid = min(BM, M - m0);
-  const i32x4 rs_a = make_rsrc_sgpr(a + (int64_t)m0 * lda,
-                                    (uint32_t)(((int64_t)(rows_valid - 1) * lda + K) * 2));
-  const int cb0 = p0 / 16;
-  const int npb = NP / 16;  // column blocks per k block of the packed weight
-  const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * (kFragBytes / 2),
-                                    (uint32_t)(((int64_t)nkb * npb - cb0) * kFragBytes));
-
-  const int lrow = lane & 15;
-  const int lk = (lane >> 4) * 8;
-  // Group g moves stage fragments f = g * HALF + wn + WN * i (i < LOADS); f <
-  // A_FRAGS is an activation row block, otherwise a weight column block.
-  unsigned off0[LOADS];
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    const int f = wm * HALF + wn + WN * i;
-    off0[i] = f < A_FRAGS ? (unsigned)((f * 16 + lrow) * lda * 2 + lk * 2)
-                          : (unsigned)((f - A_FRAGS) * kFragBytes + lane * 16);
-  }
-  auto load_half = [&](int kb) __attribute__((always_inline)) {
-    char* st = smem + (kb % STAGES) * STAGE;
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int f = wm * HALF + wn + WN * i;
-      if (wm * HALF + WN * i < A_FRAGS) {  // wave-uniform
-        const bool ok = kb * kKB + lk < K;
-        load_lds16(rs_a, st + f * kFragBytes, ok ? off0[i] + kb * (kKB * 2) : kOobOffset);
-      } else {
-        load_lds16(rs_w, st + f * kFragBytes,
-                   kb < nkb ? off0[i] + (unsigned)(kb * npb) * kFragBytes : kOobOffset);
-      }
-    }
-  };
-
-  f32x4 acc[FN][FM];
-#pragma unroll
-  for (int i = 0; i < FN; ++i)
-#pragma unroll
-    for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float ss[FM], sa[FM];
-#pragma unroll
-  for (int j = 0; j < FM; ++j) ss[j] = sa[j] = 0.f;
-  bf16x8 af[FM], wf[FN];
-
-  auto read_block = [&](int kb) __attribute__((always_inline)) {
-    const char* st = smem + (kb % STAGES) * STAGE;
-#pragma unroll
-    for (int j = 0; j < FM; ++j)
-      af[j] = *reinterpret_cast<const bf16x8*>(st + (wm * FM + j) * kFragBytes + lane * 16);
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-      wf[i] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + (wn * FN + i) * kFragBytes + lane * 16);
-  };
-  // The 4 waves of a group share its rows and take turns squaring them.
-  auto multiply = [&](int kb) __attribute__((always_inline)) {
-    const bool stats = (kb % WN) == wn;
-#pragma unroll
-    for (int i = 0; i < FN; ++i) {
-#pragma unroll
-      for (int j = 0; j < FM; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
-      if (stats) {
-#pragma unroll
-        for (int j = i; j < FM; j += FN) {
-          if constexpr (kSS) ss[j] = sumsq8(af[j], ss[j]);
-          if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
-        }
-      }
-    }
-  };
-  auto barrier = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    __builtin_amdgcn_s_barrier();
-  };
-
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s) load_half(s);
-  wait_vmcnt<(STAGES - 2) * LOADS>();
-  barrier();
-  // Interval k: a wave of group g is at phase k - g; an even phase 2b reads block b
-  // (and transfers block b+STAGES-1), an odd phase 2b+1 multiplies block b.  One
-  // call site each keeps the accumulators in place.
-  for (int k = 0; k <= 2 * nkb; ++k) {
-    const int phase = k - wm;
-    if (phase >= 0) {
-      const int b = phase >> 1;
-      if ((phase & 1) == 0) {
-        if (b < nkb) {
-          load_half(b + STAGES - 1);
-          read_block(b);
-        }
-      } else {
-        multiply(b);
-      }
-    }
-    if (k & 1) wait_vmcnt<(STAGES - 2) * LOADS>();  // block (k+1)/2 has landed
-    barrier();
-  }
-
-  // Row statistics: combine lanes, then the 4 waves of each group through LDS.
-  if constexpr (kSS || kSA) {
-    __shared__ float part[WN][2][BM];
-#pragma unroll
-    for (int j = 0; j < FM; ++j) {
-      if constexpr (kSS) {
-        ss[j] += __shfl_xor(ss[j], 16);
-        ss[j] += __shfl_xor(ss[j], 32);
-      }
-      if constexpr (kSA) {
-        sa[j] += __shfl_xor(sa[j], 16);
-        sa[j] += __shfl_xor(sa[j], 32);
-      }
-      if (lane < 16) {
-        part[wn][0][wm * TM + j * 16 + lane] = ss[j];
-        part[wn][1][wm * TM + j * 16 + lane] = sa[j];
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < FM; ++j) {
-      float t0 = 0.f, t1 = 0.f;
-#pragma unroll
-      for (int w = 0; w < WN; ++w) {
-        t0 += part[w][0][wm * TM + j * 16 + lrow];
-        t1 += part[w][1][wm * TM + j * 16 + lrow];
-      }
-      ss[j] = t0;
-      sa[j] = t1;
-    }
-  }
-
-  const int n_lane = (lane >> 4) * 4;
-  auto epilogue = [&](auto vec_tag) __attribute__((always_inline)) {
-    constexpr bool VEC = decltype(vec_tag)::value;
-#pragma unroll
-    for (int j = 0; j < FM; ++j) {
-      const int mb = m0 + wm * TM + j * 16;
-      const int m = mb + lrow;
-      const RowStat st = row_stat<EPI>(ss[j], sa[j], ep);
-      if constexpr (EPI == EPI_RMS) {
-        if (ep.inv_rms && wn == 0 && lane < 16 && m < M) ep.inv_rms[m] = st.s;
-      }
-      const bool rows_full = mb + 16 <= M;
-      if constexpr (epi_is_glu(EPI)) {
-#pragma unroll
-        for (int i = 0; i < FN; i += 2) {
-          const int fb = (p0 + wn * TN) / 2 + (i / 2) * 16;
-          if (rows_full && fb + 16 <= ncols)
-            store4_bf16_full<EPI, VEC>(y, ldy, m, fb + n_lane, acc[i][j], acc[i + 1][j], st, ep);
-          else
-            store4_bf16_edge<EPI, VEC>(y, ldy, M, ncols, m, fb + n_lane, acc[i][j], acc[i + 1][j], st, ep);
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < FN; ++i) {
-          const int pb = p0 + wn * TN + i * 16;
-          if (rows_full && pb + 16 <= ncols)
-            store4_bf16_full<EPI, VEC>(y, ldy, m, pb + n_lane, acc[i][j], acc[i][j], st, ep);
-          else
-            store4_bf16_edge<EPI, VEC>(y, ldy, M, ncols, m, pb + n_lane, acc[i][j], acc[i][j], st, ep);
-        }
-      }
-    }
-  };
-  if (epi_vec<EPI>(ep) != nullptr)
-    epilogue(std::true_type{});
-  else
-    epilogue(std::false_type{});
-}
-
-template <int BM, int BN, int STAGES, int EPI>
-static hipError_t launch_pingpong_cfg(const PrefillArgs& p) {
-  const int tiles_m = (p.M + BM - 1) / BM;
-  const int tiles_n = (p.NP + BN - 1) / BN;
-  hipLaunchKernelGGL((prefill_pingpong_kernel<BM, BN, STAGES, EPI>), dim3(tiles_m * tiles_n), dim3(512), 0,
-                     p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y, p.ldy, p.ep, tiles_m,
-                     tiles_n);
-  return hipGetLastError();
-}
-
 template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI>
 static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
   const int tiles_m = (p.M + BM - 1) / BM;
@@ -620,29 +396,47 @@ static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
   return hipGetLastError();
 }
 
+// Shape-specialised tile choice (measured on MI355X).  The 256 x 256 tile with 8
+// waves and register prefetch when it still yields at least one tile per compute
+// unit.  Otherwise 128-row tiles with 8 waves, 128 or 96 columns wide, whichever
+// fills the 256 compute units best (whole rounds of tiles); 96 is not used for a
+// GLU, whose wave tiles must hold whole gate/up block pairs.
+static int auto_tile(int M, int NP, bool glu) {
+  constexpr int kCUs = 256;
+  const int64_t big = ((int64_t)(M + 255) / 256) * ((NP + 255) / 256);
+  if (big >= kCUs) return TILE_256x256_W8_PF;
+  if (glu) return TILE_128x128_W8T;
+  const int64_t t128 = ((int64_t)(M + 127) / 128) * ((NP + 127) / 128);
+  const int64_t t96 = ((int64_t)(M + 127) / 128) * ((NP + 95) / 96);
+  // fill = tiles / (CUs x rounds); compare t96 * rounds128 against t128 * rounds96.
+  const int64_t r128 = (t128 + kCUs - 1) / kCUs, r96 = (t96 + kCUs - 1) / kCUs;
+  return t96 * r128 > t128 * r96 ? TILE_128x96_W8 : TILE_128x128_W8T;
+}
+
 template <int EPI>
 static hipError_t launch_prefill_epi(const PrefillArgs& p) {
-  // Shape-specialised tiles (measured on MI355X): the 256 x 256 tile with 8 waves
-  // and register prefetch when it still yields at least one tile per compute
-  // unit, 128 x 128 otherwise.
-  const int64_t big = ((int64_t)(p.M + 255) / 256) * ((p.NP + 255) / 256);
   int tile = p.tile;
-  if (tile == TILE_AUTO) tile = big >= 256 ? TILE_256x256_W8_PF : TILE_128x128;
+  if (tile == TILE_AUTO) tile = auto_tile(p.M, p.NP, epi_is_glu(EPI));
   switch (tile) {
     case TILE_256x256: return launch_prefill_cfg<256, 256, 2, 2, 4, true, EPI>(p);
     case TILE_128x128: return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
     case TILE_256x256_W8: return launch_prefill_cfg<256, 256, 2, 4, 4, false, EPI>(p);
-    case TILE_128x128_S8: return launch_prefill_cfg<128, 128, 2, 2, 8, true, EPI>(p);
+    case TILE_128x96_W8:
+      if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
+      else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI>(p);
     case TILE_256x128: return launch_prefill_cfg<256, 128, 2, 2, 4, true, EPI>(p);
     case TILE_128x256: return launch_prefill_cfg<128, 256, 2, 2, 4, true, EPI>(p);
     case TILE_128x64: return launch_prefill_cfg<128, 64, 2, 2, 4, true, EPI>(p);
     case TILE_64x128: return launch_prefill_cfg<64, 128, 2, 2, 4, true, EPI>(p);
     case TILE_128x128_NOPF: return launch_prefill_cfg<128, 128, 2, 2, 4, false, EPI>(p);
-    case TILE_PP_256x256: return launch_pingpong_cfg<256, 256, 4, EPI>(p);
-    case TILE_PP_256x128: return launch_pingpong_cfg<256, 128, 4, EPI>(p);
-    case TILE_PP_128x256: return launch_pingpong_cfg<128, 256, 4, EPI>(p);
     case TILE_256x256_W8_PF: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI>(p);
     case TILE_256x256_W8_PF5: return launch_prefill_cfg<256, 256, 2, 4, 5, true, EPI>(p);
+    case TILE_128x128_W8: return launch_prefill_cfg<128, 128, 2, 4, 4, true, EPI>(p);
+    case TILE_128x128_W8T: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI>(p);
+    case TILE_128x96:
+      // 48-column wave tiles cannot hold whole gate/up pairs: a GLU takes 128 x 128.
+      if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
+      else return launch_prefill_cfg<128, 96, 2, 2, 4, true, EPI>(p);
   }
   return hipErrorInvalidValue;
 }
