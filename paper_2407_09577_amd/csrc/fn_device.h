@@ -86,6 +86,25 @@ __device__ __forceinline__ void load_lds16(i32x4 rsrc, const void* lds_base, uns
                : "memory");
 }
 
+// As load_lds16, with the LDS destination given as a 32-bit LDS byte address.
+__device__ __forceinline__ void load_lds16_at(i32x4 rsrc, unsigned lds_addr, unsigned voffset) {
+  const unsigned m0 = __builtin_amdgcn_readfirstlane(lds_addr);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane(rsrc[0]);
+  r[1] = __builtin_amdgcn_readfirstlane(rsrc[1]);
+  r[2] = __builtin_amdgcn_readfirstlane(rsrc[2]);
+  r[3] = __builtin_amdgcn_readfirstlane(rsrc[3]);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(m0), "v"(voffset), "s"(r)
+               : "memory");
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
 // Cache-policy operand of the buffer loads: the non-temporal hint, for data
 // streamed exactly once (the decode weight stream).
 constexpr int kCachePolicyNT = 2;

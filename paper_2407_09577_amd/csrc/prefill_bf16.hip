@@ -20,56 +20,9 @@
 #include "fn_device.h"
 #include "fn_epilogue.h"
 #include "fn_launch.h"
+#include "fn_tile.h"
 
 namespace fn {
-
-// Workgroup id -> output tile.  Consecutive workgroup ids are dispatched to the
-// 8 XCDs in turn, and each XCD has its own L2.  The tile grid is cut into 8
-// rectangular regions (the factorisation of 8 that keeps a region's activation
-// rows plus weight columns smallest), ids are regrouped so each XCD receives one
-// region, and inside a region tiles run in groups of kGroupM tile rows, so the
-// tiles resident on one XCD share activation rows and weight columns in its L2.
-constexpr int kXcds = 8;
-constexpr int kGroupM = 4;
-
-__device__ __forceinline__ void tile_of_block(int bid, int nblocks, int tiles_m, int tiles_n,
-                                              int& tm, int& tn) {
-  // Region grid rm x rn (rm * rn = 8), derived from the tile counts alone, so
-  // every workgroup computes the same grid.
-  int rm = 1, best = 0x7fffffff;
-#pragma unroll
-  for (int c = 1; c <= kXcds; c *= 2) {
-    const int mm = (tiles_m + c - 1) / c, nn = (tiles_n + kXcds / c - 1) / (kXcds / c);
-    if (c <= tiles_m && kXcds / c <= tiles_n && mm + nn < best) {
-      best = mm + nn;
-      rm = c;
-    }
-  }
-  const int rn = kXcds / rm;
-  if (best == 0x7fffffff || nblocks % kXcds != 0 || tiles_m % rm != 0 || tiles_n % rn != 0) {
-    // Small or uneven grids: contiguous ranges per XCD, grouped by tile rows.
-    const int q = nblocks / kXcds, r = nblocks % kXcds;
-    const int x = bid % kXcds, i = bid / kXcds;
-    const int logical = x * q + min(x, r) + i;
-    const int per_group = kGroupM * tiles_n;
-    const int group = logical / per_group;
-    const int first_m = group * kGroupM;
-    const int gsize = min(tiles_m - first_m, kGroupM);
-    const int in_group = logical - group * per_group;
-    tm = first_m + in_group % gsize;
-    tn = in_group / gsize;
-    return;
-  }
-  const int x = bid % kXcds, i = bid / kXcds;  // XCD x runs its region's tiles in order i
-  const int sm = tiles_m / rm, sn = tiles_n / rn;  // region size in tiles
-  const int gm = min(kGroupM, sm);
-  const int per_group = gm * sn;
-  const int group = i / per_group, in_group = i % per_group;
-  const int first_m = group * gm;
-  const int gsize = min(sm - first_m, gm);
-  tm = (x / rn) * sm + first_m + in_group % gsize;
-  tn = (x % rn) * sn + in_group / gsize;
-}
 
 // Wait until at most `ahead` k blocks of this wave's ring transfers (LOADS each)
 // are still outstanding, i.e. everything issued before them has landed.
@@ -87,7 +40,7 @@ __device__ __forceinline__ void wait_ahead(int ahead) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI>
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false>
 __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep, int tiles_m, int tiles_n) {
@@ -134,7 +87,15 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // Fragment f of a stage: f < A_FRAGS is activation row block f, otherwise weight
   // column block f - A_FRAGS.  Wave w moves fragments w, w + NW, ...
   const int lrow = lane & 15;
-  const int lk = (lane >> 4) * 8;
+  // Activation transfers move 16 rows x 64 bytes per fragment with lane i on
+  // row i / 4, so 4 consecutive lanes read 64 contiguous bytes (one coalesced
+  // access); row r's four 16-byte chunks are stored in the order chunk ^ swz(r),
+  // which keeps the fragment reads (lane L: row L % 16, chunk L / 16) free of
+  // LDS bank conflicts.
+  auto swz = [](int r) { return ((r >> 1) ^ (r >> 3)) & 3; };
+  const int t_row = lane >> 2;
+  const int lk = ((lane & 3) ^ swz(t_row)) * 8;  // k offset of this lane's transfer chunk
+  const unsigned a_rd = (unsigned)((lrow * 4 + ((lane >> 4) ^ swz(lrow))) * 16);
   // Weight column blocks past the packed width (last column tile only) read the
   // next k block's fragments, or zeros past the buffer's end; the columns they
   // feed lie beyond every output column and are never stored.
@@ -143,7 +104,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   for (int i = 0; i < LOADS; ++i) {
     const int f = wave + NW * i;
     if (A_FRAGS % NW == 0 ? i < A_FRAGS / NW : f < A_FRAGS)
-      off0[i] = (unsigned)((f * 16 + lrow) * lda * 2 + lk * 2);
+      off0[i] = (unsigned)((f * 16 + t_row) * lda * 2 + lk * 2);
     else
       off0[i] = (unsigned)((f - A_FRAGS) * kFragBytes + lane * 16);
   }
@@ -184,7 +145,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   auto read_one = [&](int kb, int r, bf16x8 (&af)[FM], bf16x8 (&wf)[FN]) __attribute__((always_inline)) {
     const char* st = smem + (kb % STAGES) * STAGE;
     if (r < FM)
-      af[r] = *reinterpret_cast<const bf16x8*>(st + (wm * FM + r) * kFragBytes + lane * 16);
+      af[r] = *reinterpret_cast<const bf16x8*>(st + (wm * FM + r) * kFragBytes + a_rd);
     else
       wf[r - FM] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + (wn * FN + r - FM) * kFragBytes + lane * 16);
   };
@@ -226,8 +187,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         const int i = t / FM, j = t % FM;
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wfc[i], afc[j], acc[i][j], 0, 0, 0);
       }
+      // Transfer i goes out in group i * LSTEP: spread over the block (SPREAD),
+      // so the workgroup's transfers reach the address unit at the rate it
+      // drains them, or in the first groups.
+      constexpr int LSTEP = SPREAD ? NRD / LOADS : 1;
       if (more) {
-        if (g < LOADS) load_one(kb + STAGES, g);
+        if (g % LSTEP == 0 && g / LSTEP < LOADS) load_one(kb + STAGES, g / LSTEP);
         read_one(kb + 1, g, afn, wfn);
       }
       constexpr int NOWN = (FM - WNC + WN - 1) / WN;
@@ -385,26 +350,26 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     epilogue(std::false_type{});
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI>
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false>
 static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = (p.NP + BN - 1) / BN;
   const int nblocks = tiles_m * tiles_n;
-  hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI>), dim3(nblocks),
+  hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI, SPREAD>), dim3(nblocks),
                      dim3(WM * WN * 64), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y,
                      p.ldy, p.ep, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
 // Shape-specialised tile choice (measured on MI355X).  The 256 x 256 tile with 8
-// waves and register prefetch when it still yields at least one tile per compute
-// unit.  Otherwise 128-row tiles with 8 waves, 128 or 96 columns wide, whichever
+// waves, register prefetch and transfers spread over the k block when it still
+// yields at least one tile per compute unit.  Otherwise 128-row tiles with 8 waves, 128 or 96 columns wide, whichever
 // fills the 256 compute units best (whole rounds of tiles); 96 is not used for a
 // GLU, whose wave tiles must hold whole gate/up block pairs.
 static int auto_tile(int M, int NP, bool glu) {
   constexpr int kCUs = 256;
   const int64_t big = ((int64_t)(M + 255) / 256) * ((NP + 255) / 256);
-  if (big >= kCUs) return TILE_256x256_W8_PF;
+  if (big >= kCUs) return TILE_256x256_W8_PF_SP;
   if (glu) return TILE_128x128_W8T;
   const int64_t t128 = ((int64_t)(M + 127) / 128) * ((NP + 127) / 128);
   const int64_t t96 = ((int64_t)(M + 127) / 128) * ((NP + 95) / 96);
@@ -437,6 +402,14 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
       // 48-column wave tiles cannot hold whole gate/up pairs: a GLU takes 128 x 128.
       if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
       else return launch_prefill_cfg<128, 96, 2, 2, 4, true, EPI>(p);
+    case TILE_PP_256x256: return launch_prefill_pp_bf16(p);
+    case TILE_WD_256x256:
+    case TILE_WD_128x256: return launch_prefill_wd_bf16(p);
+    case TILE_256x256_W8_PF_SP: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
+    case TILE_128x128_W8T_SP: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, true>(p);
+    case TILE_128x96_W8_SP:
+      if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, true>(p);
+      else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI, true>(p);
   }
   return hipErrorInvalidValue;
 }
