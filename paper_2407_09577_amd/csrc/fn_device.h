@@ -150,22 +150,6 @@ __device__ __forceinline__ float sumsq8(const bf16x8& v, float acc) {
 __device__ __forceinline__ float bf16_lo(unsigned w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(unsigned w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Pair q (elements 2q, 2q+1) of an 8-element fragment: acc + v[2q]^2 + v[2q+1]^2,
-// and acc + v[2q] + v[2q+1].  The bf16 values are widened exactly to fp32 (a
-// shift and a mask) and accumulated with plain fp32 multiply-adds: unlike the
-// bf16 dot instructions, these issue alongside the matrix-core ops of the
-// other waves on the SIMD instead of taking matrix-core issue cycles.
-__device__ __forceinline__ float sumsq2(const bf16x8& v, int q, float acc) {
-  const unsigned w = __builtin_bit_cast(u32x4, v)[q];
-  const float lo = bf16_lo(w), hi = bf16_hi(w);
-  return fmaf(hi, hi, fmaf(lo, lo, acc));
-}
-
-__device__ __forceinline__ float sum2(const bf16x8& v, int q, float acc) {
-  const unsigned w = __builtin_bit_cast(u32x4, v)[q];
-  return acc + bf16_lo(w) + bf16_hi(w);
-}
-
 __device__ __forceinline__ float sum8(const bf16x8& v, float acc) {
   const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
   bf16x2 p0 = {v[0], v[1]}, p1 = {v[2], v[3]}, p2 = {v[4], v[5]}, p3 = {v[6], v[7]};

@@ -62,6 +62,52 @@ __device__ __forceinline__ const float* epi_vec(const EpiArgs& ep) {
   else return nullptr;
 }
 
+// The 4 outputs of one lane (logical columns n .. n+3, n % 4 == 0, all inside
+// the output) as bf16: 16-byte vector loads of the per-column vectors.
+template <int EPI, bool VEC>
+__device__ __forceinline__ u32x2 epi4_bf16(int n, f32x4 v, f32x4 u, RowStat st, const EpiArgs& ep) {
+  f32x4 vec = {0.f, 0.f, 0.f, 0.f}, cs = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (VEC) vec = *reinterpret_cast<const f32x4*>(epi_vec<EPI>(ep) + n);
+  if constexpr (EPI == EPI_LN) cs = *reinterpret_cast<const f32x4*>(ep.colsum + n);
+  float o[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) o[r] = epi_value<EPI>(v[r], u[r], st, vec[r], cs[r]);
+  return pack4_bf16(o);
+}
+
+// Output tiles staged through LDS, so that the global stores are whole rows
+// written 16 bytes per lane instead of 8-byte pieces of 16 rows per store
+// instruction.  Row r of a staged tile holds UPR 16-byte units.  With UPR a
+// multiple of 8, unit u sits at position u ^ (r % 8) of the row; otherwise rows
+// are padded by one unit.  Either way the 8-byte writes of 16 lanes on 16 rows
+// spread over the LDS banks, and a row reads back as consecutive units.
+template <int UPR>
+__device__ __forceinline__ constexpr int stage_pos(int r, int u) {
+  if constexpr (UPR % 8 == 0) return r * UPR + (u ^ (r & 7));
+  else return r * (UPR + 1) + u;
+}
+template <int ROWS, int UPR>
+constexpr int stage_bytes() { return ROWS * (UPR % 8 == 0 ? UPR : UPR + 1) * 16; }
+
+template <int UPR>
+__device__ __forceinline__ void stage4(char* tile, int r, int c, u32x2 val) {
+  const int byte = c * 2;  // c % 4 == 0: an 8-byte half of a 16-byte unit
+  *reinterpret_cast<u32x2*>(tile + stage_pos<UPR>(r, byte >> 4) * 16 + (byte & 8)) = val;
+}
+
+// Copy a staged ROWS x (UPR*8) bf16 tile to y[m0.., n0..]: thread tid of NT
+// moves 16-byte units in row-major order.  y + n0 and ldy keep 16-byte alignment.
+template <int ROWS, int UPR, int NT>
+__device__ __forceinline__ void copy_tile_out(const char* tile, __bf16* __restrict__ y, int64_t ldy, int m0, int n0,
+                                              int tid) {
+#pragma unroll
+  for (int q = tid; q < ROWS * UPR; q += NT) {
+    const int r = q / UPR, u = q % UPR;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(tile + stage_pos<UPR>(r, u) * 16);
+    *reinterpret_cast<u32x4*>(y + (int64_t)(m0 + r) * ldy + n0 + u * 8) = v;
+  }
+}
+
 // Store 4 consecutive outputs of row m starting at logical column n (n % 4 == 0)
 // when all four lie inside the output: one 8-byte store, 16-byte vector loads of
 // the per-column vectors.  VEC: the optional per-column vector is present.
@@ -69,13 +115,7 @@ __device__ __forceinline__ const float* epi_vec(const EpiArgs& ep) {
 template <int EPI, bool VEC>
 __device__ __forceinline__ void store4_bf16_full(__bf16* __restrict__ y, int64_t ldy, int m, int n,
                                                  f32x4 v, f32x4 u, RowStat st, const EpiArgs& ep) {
-  f32x4 vec = {0.f, 0.f, 0.f, 0.f}, cs = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (VEC) vec = *reinterpret_cast<const f32x4*>(epi_vec<EPI>(ep) + n);
-  if constexpr (EPI == EPI_LN) cs = *reinterpret_cast<const f32x4*>(ep.colsum + n);
-  float o[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) o[r] = epi_value<EPI>(v[r], u[r], st, vec[r], cs[r]);
-  *reinterpret_cast<u32x2*>(y + (int64_t)m * ldy + n) = pack4_bf16(o);
+  *reinterpret_cast<u32x2*>(y + (int64_t)m * ldy + n) = epi4_bf16<EPI, VEC>(n, v, u, st, ep);
 }
 
 // The same for the ragged edge: row m may lie past M and columns past ncols

@@ -30,9 +30,6 @@ enum Tile : int {
   TILE_256x256_W8_PF_SP = 15,  // TILE_256x256_W8_PF, transfers spread over the k block
   TILE_128x128_W8T_SP = 16,    // TILE_128x128_W8T, transfers spread over the k block
   TILE_128x96_W8_SP = 17,      // TILE_128x96_W8, transfers spread over the k block
-  TILE_PP_256x256 = 18,        // 8 waves in two ping-pong groups, 64-deep steps
-  TILE_WD_256x256 = 19,        // 8 waves of 128 x 64, weights straight to registers
-  TILE_WD_128x256 = 20,        // 8 waves of 64 x 64, weights straight to registers
   TILE_COUNT
 };
 
@@ -58,8 +55,6 @@ struct PrefillArgs {
   hipStream_t stream;
 };
 hipError_t launch_prefill_bf16(const PrefillArgs& p);
-hipError_t launch_prefill_pp_bf16(const PrefillArgs& p);
-hipError_t launch_prefill_wd_bf16(const PrefillArgs& p);
 
 struct DecodeArgs {
   const __bf16* a;

@@ -150,15 +150,11 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       wf[r - FM] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + (wn * FN + r - FM) * kFragBytes + lane * 16);
   };
 
-  // Row statistics of fragment j (squares, and sums for LayerNorm), whole or
-  // one element pair q at a time.
+  // Row statistics of fragment j: squares (and sums, for LayerNorm) of its 8
+  // elements per lane, as packed bf16 dot products accumulated in fp32.
   auto stats_one = [&](int j, const bf16x8 (&af)[FM]) __attribute__((always_inline)) {
     if constexpr (kSS) ss[j] = sumsq8(af[j], ss[j]);
     if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
-  };
-  auto stats_pair = [&](int j, int q, const bf16x8 (&af)[FM]) __attribute__((always_inline)) {
-    if constexpr (kSS) ss[j] = sumsq2(af[j], q, ss[j]);
-    if constexpr (kSA) sa[j] = sum2(af[j], q, sa[j]);
   };
 
   auto sync_block = [&]() __attribute__((always_inline)) {
@@ -166,20 +162,23 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     __builtin_amdgcn_s_barrier();
   };
 
-  // One k block of work for the matrix cores, issued as NRD groups: group g
-  // holds its share of the NMF matrix-core ops, LDS read g of the next block
-  // (PF), transfer g of block kb+STAGES (g < LOADS) and a share of the row
-  // statistics.  The scheduling fences keep this interleaving, so memory
-  // traffic overlaps the matrix cores.
-  // Row statistics are split across the WN waves of a row band at compile time:
-  // the wave with column index WNC squares activation fragments j = WNC + WN t,
-  // over the whole of K, so no wave branches on whose turn it is.  Its NOWN
-  // fragments x 4 element pairs are dealt round-robin over the groups, so
-  // consecutive accumulations into one row total sit groups apart.
+  // One k block of work for the matrix cores.  First this wave's share of the
+  // row statistics, as one clump of dot products: the waves of a row band split
+  // its fragments at compile time (the wave with column index WNC takes
+  // fragments WNC, WNC + WN, ...), over the whole of K.  Measured on MI355X, a
+  // clump at the start of the block costs next to nothing, while the same work
+  // spread between the matrix-core ops costs several percent.  Then NRD groups:
+  // group g holds its share of the NMF matrix-core ops, LDS read g of the next
+  // block (PF) and, spread over the block, transfer i of block kb+STAGES.  The
+  // scheduling fences keep this interleaving, so memory traffic overlaps the
+  // matrix cores.
   auto multiply_interleaved = [&](auto wnc, int kb, const bf16x8 (&afc)[FM], const bf16x8 (&wfc)[FN],
                                   bf16x8 (&afn)[FM], bf16x8 (&wfn)[FN], bool more)
                                   __attribute__((always_inline)) {
     constexpr int WNC = decltype(wnc)::value;
+#pragma unroll
+    for (int j = WNC; j < FM; j += WN) stats_one(j, afc);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int g = 0; g < NRD; ++g) {
 #pragma unroll
@@ -195,10 +194,6 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         if (g % LSTEP == 0 && g / LSTEP < LOADS) load_one(kb + STAGES, g / LSTEP);
         read_one(kb + 1, g, afn, wfn);
       }
-      constexpr int NOWN = (FM - WNC + WN - 1) / WN;
-#pragma unroll
-      for (int idx = g; idx < NOWN * 4; idx += NRD)  // resolved when unrolled
-        stats_pair(WNC + WN * (idx % NOWN), idx / NOWN, afc);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -248,11 +243,11 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 #pragma unroll
         for (int r = 0; r < NRD; ++r) read_one(kb, r, af0, wf0);
 #pragma unroll
+        for (int j = WNC; j < FM; j += WN) stats_one(j, af0);
+#pragma unroll
         for (int t = 0; t < NMF; ++t)
           acc[t / FM][t % FM] =
               __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[t / FM], af0[t % FM], acc[t / FM][t % FM], 0, 0, 0);
-#pragma unroll
-        for (int j = WNC; j < FM; j += WN) stats_one(j, af0);
       }
     }
   };
@@ -308,20 +303,56 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     }
   }
 
-  // Epilogue: one uniform decision per 16 x 16 fragment picks the fast store
-  // (fragment fully inside the output) or the guarded edge store, and the
-  // optional per-column vector is dispatched once for the whole tile.
+  // Epilogue.  A tile that lies wholly inside the output (and a 16-byte
+  // aligned row pitch) is staged through LDS and written as whole rows, 16
+  // bytes per lane.  Otherwise one uniform decision per 16 x 16 fragment picks
+  // the plain store or the guarded edge store.  The optional per-column vector
+  // is dispatched once for the whole tile.
+  constexpr int OUT_COLS = epi_is_glu(EPI) ? BN / 2 : BN;  // output columns of a tile
+  constexpr int UPR = OUT_COLS / 8;                       // 16-byte units per output row
+  constexpr bool kStageable = OUT_COLS % 8 == 0 && stage_bytes<BM, UPR>() <= STAGES * STAGE;
+  const int n0 = epi_is_glu(EPI) ? p0 / 2 : p0;
   const int n_lane = (lane >> 4) * 4;
-  auto epilogue = [&](auto vec_tag) __attribute__((always_inline)) {
+  auto write_inv_rms = [&](int j, const RowStat& st) __attribute__((always_inline)) {
+    if constexpr (EPI == EPI_RMS) {
+      const int m = m0 + wm * TM + j * 16 + lrow;
+      if (ep.inv_rms && wn == 0 && lane < 16 && m < M) ep.inv_rms[m] = st.s;
+    }
+  };
+  auto staged = [&](auto vec_tag) __attribute__((always_inline)) {
+    constexpr bool VEC = decltype(vec_tag)::value;
+    wait_vmcnt<0>();  // the ring's last (zero-filling) transfers have landed
+    __syncthreads();  // every wave is done with the ring and the row totals
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      const RowStat st = row_stat<EPI>(ss[j], sa[j], ep);
+      write_inv_rms(j, st);
+      const int r = wm * TM + j * 16 + lrow;
+      if constexpr (epi_is_glu(EPI)) {
+#pragma unroll
+        for (int i = 0; i < FN; i += 2) {
+          const int c = wn * (TN / 2) + (i / 2) * 16 + n_lane;
+          stage4<UPR>(smem, r, c, epi4_bf16<EPI, VEC>(n0 + c, acc[i][j], acc[i + 1][j], st, ep));
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+          const int c = wn * TN + i * 16 + n_lane;
+          stage4<UPR>(smem, r, c, epi4_bf16<EPI, VEC>(n0 + c, acc[i][j], acc[i][j], st, ep));
+        }
+      }
+    }
+    __syncthreads();
+    copy_tile_out<BM, UPR, NW * 64>(smem, y, ldy, m0, n0, threadIdx.x);
+  };
+  auto direct = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       const int mb = m0 + wm * TM + j * 16;
       const int m = mb + lrow;
       const RowStat st = row_stat<EPI>(ss[j], sa[j], ep);
-      if constexpr (EPI == EPI_RMS) {
-        if (ep.inv_rms && wn == 0 && lane < 16 && m < M) ep.inv_rms[m] = st.s;
-      }
+      write_inv_rms(j, st);
       const bool rows_full = mb + 16 <= M;
       if constexpr (epi_is_glu(EPI)) {
 #pragma unroll
@@ -344,10 +375,20 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       }
     }
   };
-  if (epi_vec<EPI>(ep) != nullptr)
-    epilogue(std::true_type{});
+  // Workgroup-uniform: every wave takes the same branch (the staged path has barriers).
+  const bool whole = kStageable && m0 + BM <= M && n0 + OUT_COLS <= ncols && (ldy & 7) == 0;
+  const bool vec = epi_vec<EPI>(ep) != nullptr;
+  if constexpr (kStageable) {
+    if (whole) {
+      if (vec) staged(std::true_type{});
+      else staged(std::false_type{});
+      return;
+    }
+  }
+  if (vec)
+    direct(std::true_type{});
   else
-    epilogue(std::false_type{});
+    direct(std::false_type{});
 }
 
 template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false>
@@ -402,9 +443,6 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
       // 48-column wave tiles cannot hold whole gate/up pairs: a GLU takes 128 x 128.
       if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
       else return launch_prefill_cfg<128, 96, 2, 2, 4, true, EPI>(p);
-    case TILE_PP_256x256: return launch_prefill_pp_bf16(p);
-    case TILE_WD_256x256:
-    case TILE_WD_128x256: return launch_prefill_wd_bf16(p);
     case TILE_256x256_W8_PF_SP: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
     case TILE_128x128_W8T_SP: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, true>(p);
     case TILE_128x96_W8_SP:

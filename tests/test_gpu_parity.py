@@ -284,7 +284,7 @@ def test_non_contiguous_activation_rows(fn):
 
 
 # ------------------------------------------------------------------ every kernel configuration
-PREFILL_TILES = list(range(1, 21))   # forced through the high byte of the path argument
+PREFILL_TILES = list(range(1, 18))   # forced through the high byte of the path argument
 DECODE_CFGS = list(range(1, 13))
 
 
