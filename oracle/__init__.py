@@ -61,6 +61,11 @@ def _load():
     for name in ("fn_oracle_layernorm_linear", "fn_oracle_layernorm_linear_deferred"):
         getattr(lib, name).argtypes = [P, I, I, P, P, P, I, D, P, P, I, P]
         getattr(lib, name).restype = None
+    for name in ("fn_oracle_rmsnorm_glu_act", "fn_oracle_glu_act_deferred"):
+        getattr(lib, name).argtypes = [P, I, I, P, P, I, D, ctypes.c_int, P, I, P]
+        getattr(lib, name).restype = None
+    lib.fn_oracle_rmsnorm_ffn.argtypes = [P, I, I, P, P, I, P, I, D, ctypes.c_int, P, I, P]
+    lib.fn_oracle_rmsnorm_ffn.restype = None
     lib.fn_oracle_round_bf16.argtypes = [D]
     lib.fn_oracle_round_bf16.restype = D
     lib.fn_oracle_round_f32.argtypes = [D]
@@ -149,6 +154,47 @@ def rmsnorm_swiglu(a, g, Wgu, eps, rows=None) -> np.ndarray:
     out = np.empty((nr, F), dtype=np.float64)
     _load().fn_oracle_rmsnorm_swiglu(_ptr(a), M, K, _ptr(g), _ptr(Wgu), F, _eps(eps), _ptr(r), nr, _ptr(out))
     return out
+
+
+GLU_SWIGLU, GLU_REGLU, GLU_BILINEAR, FFN_RELU = 0, 1, 2, 3
+
+
+def _glu_like(fn, a, g, Wgu, eps, act, rows):
+    a, g, Wgu = _f64(a), _f64(g), _f64(Wgu)
+    M, K = a.shape
+    K2, N2 = Wgu.shape
+    if K2 != K or N2 % 2 or g.shape != (K,) or act not in (GLU_SWIGLU, GLU_REGLU, GLU_BILINEAR):
+        raise ValueError("shape mismatch or unknown act")
+    F = N2 // 2
+    r, nr = _rows(rows, M)
+    out = np.empty((nr, F), dtype=np.float64)
+    fn(_ptr(a), M, K, _ptr(g), _ptr(Wgu), F, _eps(eps), int(act), _ptr(r), nr, _ptr(out))
+    return out
+
+
+def rmsnorm_glu_act(a, g, Wgu, eps, act, rows=None) -> np.ndarray:
+    """out = act(x Wg) * (x Wu), x = RMSNorm(a; g); act = silu, ReLU or identity (Sec. 4.1, App.)."""
+    return _glu_like(_load().fn_oracle_rmsnorm_glu_act, a, g, Wgu, eps, act, rows)
+
+
+def glu_act_deferred(a, g, Wgu, eps, act, rows=None) -> np.ndarray:
+    """The same with W* = diag(g) W and the scale deferred (1/MS for ReGLU / bilinear). Self-check."""
+    return _glu_like(_load().fn_oracle_glu_act_deferred, a, g, Wgu, eps, act, rows)
+
+
+def rmsnorm_ffn(a, g, Wup, Wdown, eps, act, rows=None) -> np.ndarray:
+    """y = h Wdown after x = RMSNorm(a; g): h = ReLU(x Wup) (act 3) or act(x Wg) * (x Wu) (act 0-2)."""
+    a, g, Wup, Wdown = _f64(a), _f64(g), _f64(Wup), _f64(Wdown)
+    M, K = a.shape
+    K2, NU = Wup.shape
+    F, N = Wdown.shape
+    if K2 != K or g.shape != (K,) or act not in (0, 1, 2, 3) or NU != (F if act == FFN_RELU else 2 * F):
+        raise ValueError("shape mismatch or unknown act")
+    r, nr = _rows(rows, M)
+    y = np.empty((nr, N), dtype=np.float64)
+    _load().fn_oracle_rmsnorm_ffn(_ptr(a), M, K, _ptr(g), _ptr(Wup), F, _ptr(Wdown), N, _eps(eps), int(act),
+                                  _ptr(r), nr, _ptr(y))
+    return y
 
 
 def _ln_like(fn, a, g, beta, W, eps, bias, rows):

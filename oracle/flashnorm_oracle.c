@@ -150,6 +150,111 @@ ORACLE_EXPORT void fn_oracle_rmsnorm_swiglu(const double* a, int64_t M, int64_t 
   }
 }
 
+/* Gate nonlinearities of the GLU variants: 0 = SwiGLU (silu), 1 = ReGLU (ReLU),
+ * 2 = bilinear GLU (identity); and 3 = the plain ReLU of a non-gated FFN. */
+static double glu_act(int act, double t) {
+  if (act == 0) return silu(t);
+  if (act == 1 || act == 3) return t > 0.0 ? t : 0.0;
+  return t;
+}
+
+/* RMSNorm followed by a GLU-variant FFN input projection, standard form
+ * (Sec. 4.1, Fig. 3(a); App. "FFN with ReGLU and Bilinear GLU", Fig. 4(a)):
+ *   x = RMSNorm(a; g),  h_g = x Wg,  h_u = x Wu,  out = act(h_g) * h_u,
+ * act = silu (0), ReLU (1) or the identity (2).  Wgu = [Wg | Wu], [K, 2F]. */
+ORACLE_EXPORT void fn_oracle_rmsnorm_glu_act(const double* a, int64_t M, int64_t K,
+                                             const double* g, const double* Wgu, int64_t F,
+                                             double eps, int act, const int64_t* rows,
+                                             int64_t nrows, double* out) {
+  (void)M;
+  const int64_t N2 = 2 * F;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < nrows; ++r) {
+    const double* ar = a + row_of(rows, r) * K;
+    double* x = (double*)malloc(sizeof(double) * (size_t)K);
+    double* h = (double*)calloc((size_t)N2, sizeof(double));
+    double rms = fn_oracle_rms(ar, K, eps);
+    for (int64_t k = 0; k < K; ++k) x[k] = ar[k] / rms * g[k];
+    for (int64_t k = 0; k < K; ++k) {
+      const double* wk = Wgu + k * N2;
+      for (int64_t n = 0; n < N2; ++n) h[n] += x[k] * wk[n];
+    }
+    for (int64_t f = 0; f < F; ++f) out[r * F + f] = glu_act(act, h[f]) * h[F + f];
+    free(x);
+    free(h);
+  }
+}
+
+/* The same with the normalisation deferred past the projections (self-check
+ * only): W* = diag(g) W in fp64 (Prop. 1), and the per-token scale s = 1/RMSe(a)
+ * applied after the matrix multiply (Prop. 2).  For ReGLU and the bilinear GLU
+ * both branch scales merge into one factor s^2 = 1/MSe(a) = 1/(eps + sum a^2/K)
+ * on the product (App. "FFN with ReGLU and Bilinear GLU": ReLU(s t) = s ReLU(t)
+ * for s >= 0); SwiGLU keeps the scale inside the silu (Fig. 3). */
+ORACLE_EXPORT void fn_oracle_glu_act_deferred(const double* a, int64_t M, int64_t K,
+                                              const double* g, const double* Wgu, int64_t F,
+                                              double eps, int act, const int64_t* rows,
+                                              int64_t nrows, double* out) {
+  (void)M;
+  const int64_t N2 = 2 * F;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < nrows; ++r) {
+    const double* ar = a + row_of(rows, r) * K;
+    double* h = (double*)calloc((size_t)N2, sizeof(double));
+    double ss = 0.0;
+    for (int64_t k = 0; k < K; ++k) ss += ar[k] * ar[k];
+    const double ms = eps + ss / (double)K;
+    for (int64_t k = 0; k < K; ++k) {
+      const double* wk = Wgu + k * N2;
+      for (int64_t n = 0; n < N2; ++n) h[n] += ar[k] * (g[k] * wk[n]);
+    }
+    for (int64_t f = 0; f < F; ++f) {
+      if (act == 0) {
+        const double s = 1.0 / sqrt(ms);
+        out[r * F + f] = silu(s * h[f]) * (s * h[F + f]);
+      } else {
+        out[r * F + f] = glu_act(act, h[f]) * h[F + f] / ms;
+      }
+    }
+    free(h);
+  }
+}
+
+/* A whole FFN after an RMSNorm, standard form: x = RMSNorm(a; g), then
+ *   act 3 (App. "FFN with ReLU", Fig. 2(a)):  h = ReLU(x Wup), Wup [K, F];
+ *   act 0/1/2 (Fig. 3(a), Fig. 4(a)):         h = act(x Wg) * (x Wu), Wup = [Wg | Wu], [K, 2F];
+ * and y = h Wdown, Wdown [F, N]. */
+ORACLE_EXPORT void fn_oracle_rmsnorm_ffn(const double* a, int64_t M, int64_t K, const double* g,
+                                         const double* Wup, int64_t F, const double* Wdown,
+                                         int64_t N, double eps, int act, const int64_t* rows,
+                                         int64_t nrows, double* y) {
+  (void)M;
+  const int64_t NU = act == 3 ? F : 2 * F;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < nrows; ++r) {
+    const double* ar = a + row_of(rows, r) * K;
+    double* x = (double*)malloc(sizeof(double) * (size_t)K);
+    double* u = (double*)calloc((size_t)NU, sizeof(double));
+    double* h = (double*)malloc(sizeof(double) * (size_t)F);
+    double rms = fn_oracle_rms(ar, K, eps);
+    for (int64_t k = 0; k < K; ++k) x[k] = ar[k] / rms * g[k];
+    for (int64_t k = 0; k < K; ++k) {
+      const double* wk = Wup + k * NU;
+      for (int64_t n = 0; n < NU; ++n) u[n] += x[k] * wk[n];
+    }
+    for (int64_t f = 0; f < F; ++f) h[f] = act == 3 ? glu_act(3, u[f]) : glu_act(act, u[f]) * u[F + f];
+    double* yr = y + r * N;
+    for (int64_t n = 0; n < N; ++n) yr[n] = 0.0;
+    for (int64_t f = 0; f < F; ++f) {
+      const double* wf = Wdown + f * N;
+      for (int64_t n = 0; n < N; ++n) yr[n] += h[f] * wf[n];
+    }
+    free(x);
+    free(u);
+    free(h);
+  }
+}
+
 /* LayerNorm followed by a linear layer, standard form (Sec. 2 "Normalization in
  * transformers": centering, then RMS scaling with g, then the bias beta; the
  * epsilon sits inside the root as in App. "RMS with epsilon"):

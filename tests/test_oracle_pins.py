@@ -379,3 +379,89 @@ def test_workload_recipe():
     t = workloads.tiny_fp32()
     assert t.a.dtype == torch.float32 and t.W.shape == (576, 576)
     assert abs(t.W.std().item() - 1 / 24) < 2e-3
+
+
+# ------------------------------------------------ GLU variants and deferred FFNs
+def test_glu_variants_exact_worked_example():
+    fx = _read_fixture("glu_variants_worked_example.txt")
+    a = np.array([[float(_frac(v)) for v in fx["a"][0]]])
+    g = np.array([float(_frac(v)) for v in fx["g"][0]])
+    Wg = np.array([[float(_frac(v)) for v in r] for r in fx["Wg"]])
+    Wu = np.array([[float(_frac(v)) for v in r] for r in fx["Wu"]])
+    Wd = np.array([[float(_frac(v)) for v in r] for r in fx["Wd"]])
+    Wgu = np.concatenate([Wg, Wu], axis=1)
+    for eps_s, act_s, *vals in fx["glu"]:
+        eps, act = float(_frac(eps_s)), int(act_s)
+        want = np.array([float(_frac(v)) for v in vals])
+        np.testing.assert_allclose(oracle.rmsnorm_glu_act(a, g, Wgu, eps, act)[0], want, rtol=1e-14, atol=1e-14)
+        np.testing.assert_allclose(oracle.glu_act_deferred(a, g, Wgu, eps, act)[0], want, rtol=1e-14, atol=1e-14)
+    for eps_s, act_s, *vals in fx["ffn"]:
+        eps, act = float(_frac(eps_s)), int(act_s)
+        want = np.array([float(_frac(v)) for v in vals])
+        Wup = Wg if act == oracle.FFN_RELU else Wgu
+        np.testing.assert_allclose(oracle.rmsnorm_ffn(a, g, Wup, Wd, eps, act)[0], want, rtol=1e-14, atol=1e-14)
+
+
+@pytest.mark.parametrize("act", [oracle.GLU_SWIGLU, oracle.GLU_REGLU, oracle.GLU_BILINEAR])
+@pytest.mark.parametrize("M,K,F_,eps,seed", [(4, 32, 9, 1e-6, 0), (2, 576, 40, 1e-5, 1)])
+def test_glu_variants_match_torch(act, M, K, F_, eps, seed):
+    a, g, Wgu = _rand_case(M, K, 2 * F_, seed + 10 * act, neg_g=True)
+    ta, tg, tW = (torch.from_numpy(x) for x in (a, g, Wgu))
+    x = F.rms_norm(ta, (K,), weight=tg, eps=float(np.float32(eps)))
+    hg, hu = x @ tW[:, :F_], x @ tW[:, F_:]
+    gate = {oracle.GLU_SWIGLU: F.silu, oracle.GLU_REGLU: F.relu, oracle.GLU_BILINEAR: lambda t: t}[act](hg)
+    np.testing.assert_allclose(oracle.rmsnorm_glu_act(a, g, Wgu, eps, act), (gate * hu).numpy(),
+                               rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("act", [oracle.FFN_RELU, oracle.GLU_SWIGLU, oracle.GLU_REGLU, oracle.GLU_BILINEAR])
+def test_ffn_matches_torch(act):
+    M, K, F_, N, eps = 3, 48, 20, 12, 1e-5
+    a, g, Wup = _rand_case(M, K, F_ if act == oracle.FFN_RELU else 2 * F_, 5 + act, neg_g=True)
+    Wd = np.random.default_rng(9).standard_normal((F_, N)) / math.sqrt(F_)
+    ta, tg, tu, td = (torch.from_numpy(x) for x in (a, g, Wup, Wd))
+    x = F.rms_norm(ta, (K,), weight=tg, eps=float(np.float32(eps)))
+    u = x @ tu
+    if act == oracle.FFN_RELU:
+        h = F.relu(u)
+    else:
+        gate = {oracle.GLU_SWIGLU: F.silu, oracle.GLU_REGLU: F.relu, oracle.GLU_BILINEAR: lambda t: t}[act]
+        h = gate(u[:, :F_]) * u[:, F_:]
+    np.testing.assert_allclose(oracle.rmsnorm_ffn(a, g, Wup, Wd, eps, act), (h @ td).numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_bilinear_and_reglu_closed_form_sums():
+    # g = 1, Wg = Wu = I (F = K), eps = 0: the bilinear output is a_k^2 / MS(a), so it sums to K
+    # exactly; the ReGLU output keeps only the positive a_k, so it sums to K * sum_+ a^2 / sum a^2.
+    K = 12
+    a = np.random.default_rng(3).standard_normal((4, K))
+    I2 = np.concatenate([np.eye(K), np.eye(K)], axis=1)
+    g = np.ones(K)
+    bil = oracle.rmsnorm_glu_act(a, g, I2, 0.0, oracle.GLU_BILINEAR)
+    np.testing.assert_allclose(bil.sum(axis=1), K, rtol=1e-14)
+    rel = oracle.rmsnorm_glu_act(a, g, I2, 0.0, oracle.GLU_REGLU)
+    want = K * (np.where(a > 0, a, 0.0) ** 2).sum(axis=1) / (a ** 2).sum(axis=1)
+    np.testing.assert_allclose(rel.sum(axis=1), want, rtol=1e-14)
+    assert (rel >= 0).all()
+
+
+@pytest.mark.parametrize("act", [oracle.GLU_SWIGLU, oracle.GLU_REGLU, oracle.GLU_BILINEAR])
+def test_glu_deferred_form_agrees(act):
+    # Prop. 1-2 with the GLU scales: W* = diag(g) W, deferred scale (1/MS for ReGLU and bilinear)
+    a, g, Wgu = _rand_case(6, 40, 18, 21 + act, neg_g=True)
+    for eps in (0.0, 1e-5, 0.3):
+        assert _rel(oracle.glu_act_deferred(a, g, Wgu, eps, act), oracle.rmsnorm_glu_act(a, g, Wgu, eps, act)) < 1e-13
+
+
+def test_relu_and_bilinear_ffn_scale_invariance():
+    # ReLU(s t) = s ReLU(t) for s >= 0 (App. "FFN with ReLU"): with eps = 0 the FFN of c*a equals that
+    # of a for c > 0; the bilinear GLU is invariant for c < 0 as well (the two scales multiply).
+    a, g, Wup = _rand_case(3, 24, 10, 31, neg_g=True)
+    Wd = np.random.default_rng(1).standard_normal((10, 6))
+    _, _, Wgu = _rand_case(3, 24, 20, 32)
+    for c in (2.0 ** -10, 3.0, 2.0 ** 10):
+        assert _rel(oracle.rmsnorm_ffn(c * a, g, Wup, Wd, 0.0, oracle.FFN_RELU),
+                    oracle.rmsnorm_ffn(a, g, Wup, Wd, 0.0, oracle.FFN_RELU)) < 1e-13
+    for c in (-3.0, 0.25):
+        assert _rel(oracle.rmsnorm_ffn(c * a, g, Wgu, Wd, 0.0, oracle.GLU_BILINEAR),
+                    oracle.rmsnorm_ffn(a, g, Wgu, Wd, 0.0, oracle.GLU_BILINEAR)) < 1e-13
