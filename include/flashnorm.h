@@ -161,6 +161,61 @@ int flashnorm_layernorm_linear_ex(const void* a, int64_t M, int64_t K, int64_t l
                                   int64_t N, float eps, void* y, int64_t ldy, int y_dtype,
                                   int path, void* stream);
 
+/* Gate nonlinearity of a GLU-variant FFN input projection (Sec. 4.1 and App. "FFN with
+ * ReGLU and Bilinear GLU").  SWIGLU_DEFER_UP is SwiGLU with the up-branch scale left
+ * for the FFN output (Fig. 3(b)). */
+typedef enum {
+  FN_GLU_SWIGLU = 0,
+  FN_GLU_REGLU = 1,
+  FN_GLU_BILINEAR = 2,
+  FN_GLU_SWIGLU_DEFER_UP = 3
+} fn_glu_act;
+
+/* RMSNorm -> GLU-variant FFN input projection with the normalisation deferred past
+ * the products; s_m = 1/sqrt(eps + ss_m/K) as in flashnorm_linear:
+ *   FN_GLU_SWIGLU:          out = silu(s_m hg) * (s_m hu)            (Fig. 3(a))
+ *   FN_GLU_REGLU:           out = relu(hg) * hu * s_m^2              (Fig. 4(b))
+ *   FN_GLU_BILINEAR:        out = hg * hu * s_m^2                    (Fig. 4(b))
+ *   FN_GLU_SWIGLU_DEFER_UP: out = silu(s_m hg) * hu                  (Fig. 3(b))
+ * with hg = (a W*g)[m,f], hu = (a W*u)[m,f].  For ReGLU and the bilinear GLU both
+ * branch scales merge into one factor s^2 = 1/MSe(a) because ReLU(s t) = s ReLU(t)
+ * for s >= 0 (App. "FFN with ReGLU and Bilinear GLU").
+ *   W_star_gu  packed by fold_weights(..., 2F, FN_LAYOUT_GLU, a_dtype, ...).
+ *   out        [M, F], leading dimension ldo >= F, dtype out_dtype == a_dtype.
+ *   inv_rms    [M] fp32 output of s_m: required for FN_GLU_SWIGLU_DEFER_UP (the
+ *              consumer, e.g. rowscale_linear for the down projection, applies it),
+ *              optional for FN_GLU_SWIGLU, and must be NULL for ReGLU and bilinear
+ *              (FN_ERR_VALUE), whose output carries the whole scale.
+ *   path       FN_PATH_AUTO / PREFILL / DECODE with the automatic configuration
+ *              (bits 8..15 zero, else FN_ERR_UNSUPPORTED). */
+int flashnorm_glu_act(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                      const void* W_star_gu, int64_t F, float eps, int act, void* out,
+                      int64_t ldo, int out_dtype, float* inv_rms, int path, void* stream);
+
+/* RMSNorm -> up projection of a ReLU FFN with the normalisation deferred all the
+ * way to the FFN output (App. "FFN with ReLU", Fig. 2(b): ReLU(s t) = s ReLU(t) for
+ * s >= 0, so the scale passes the ReLU and the down projection):
+ *   y[m,n] = relu((a W*)[m,n])   and   inv_rms[m] = s_m (required).
+ * The FFN output is rowscale_linear(y, W_down, inv_rms).  Arguments as for
+ * flashnorm_linear; path as for flashnorm_glu_act. */
+int flashnorm_linear_relu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                          const void* W_star, int64_t N, float eps, void* y, int64_t ldy,
+                          int y_dtype, float* inv_rms, int path, void* stream);
+
+/* Linear layer applying a per-row scale deferred from an earlier normalisation
+ * (Prop. 2 carried to the FFN output, Fig. 2(b) and Fig. 3(b)):
+ *   y[m,n] = (sum_k x[m,k] W[k,n]) * row_scale[m].
+ *   x          [M, K] (e.g. the output of flashnorm_linear_relu or of
+ *              flashnorm_glu_act with FN_GLU_SWIGLU_DEFER_UP), dtype x_dtype.
+ *   W_packed   packed by fold_weights(..., N, FN_LAYOUT_LINEAR, x_dtype, ...); pass
+ *              g = NULL unless a per-input-channel weight should be folded in.
+ *   row_scale  [M] fp32 (required), e.g. the inv_rms side output of the producer.
+ *   y          [M, N], leading dimension ldy >= N, dtype y_dtype == x_dtype.
+ *   path as for flashnorm_glu_act. */
+int rowscale_linear(const void* x, int64_t M, int64_t K, int64_t ldx, int x_dtype,
+                    const void* W_packed, int64_t N, const float* row_scale, void* y,
+                    int64_t ldy, int y_dtype, int path, void* stream);
+
 /* Unfused baselines in the same library (the sequential RMSNorm -> GEMM of Fig. 1(a)
  * and Sec. 6): a normalisation kernel writes the normalised activations
  * x = RMSNorm(a; g) (or LayerNorm(a; g, beta)) to the caller's workspace x_ws

@@ -226,6 +226,59 @@ int flashnorm_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda,
                                        y_dtype, FN_PATH_AUTO, stream);
 }
 
+// The epilogue family beyond the core kinds runs with the automatic configuration
+// of the chosen path only.
+static int check_auto_config(int path) {
+  return (path >> FN_PATH_TILE_SHIFT) ? FN_ERR_UNSUPPORTED : FN_OK;
+}
+
+int flashnorm_glu_act(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star_gu,
+                      int64_t F, float eps, int act, void* out, int64_t ldo, int out_dtype, float* inv_rms,
+                      int path, void* stream) {
+  int epi;
+  switch (act) {
+    case FN_GLU_SWIGLU: epi = fn::EPI_GLU; break;
+    case FN_GLU_REGLU: epi = fn::EPI_REGLU; break;
+    case FN_GLU_BILINEAR: epi = fn::EPI_BILINEAR; break;
+    case FN_GLU_SWIGLU_DEFER_UP: epi = fn::EPI_GLU_DEFER; break;
+    default: return FN_ERR_VALUE;
+  }
+  OpDesc d{a, M, K, lda, a_dtype, W_star_gu, F, 1, out, ldo, epi, make_ep(eps, K), path, (hipStream_t)stream};
+  d.ep.inv_rms = inv_rms;
+  int s = validate_op(d, out_dtype);
+  if (s) return s;
+  if ((s = check_auto_config(path))) return s;
+  if (act == FN_GLU_SWIGLU_DEFER_UP && M > 0 && !inv_rms) return FN_ERR_NULL;
+  if ((act == FN_GLU_REGLU || act == FN_GLU_BILINEAR) && inv_rms) return FN_ERR_VALUE;
+  return run_op(d);
+}
+
+int flashnorm_linear_relu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star,
+                          int64_t N, float eps, void* y, int64_t ldy, int y_dtype, float* inv_rms, int path,
+                          void* stream) {
+  OpDesc d{a, M, K, lda, a_dtype, W_star, N, 0, y, ldy, fn::EPI_RELU_DEFER, make_ep(eps, K), path,
+           (hipStream_t)stream};
+  d.ep.inv_rms = inv_rms;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  if ((s = check_auto_config(path))) return s;
+  if (M > 0 && !inv_rms) return FN_ERR_NULL;
+  return run_op(d);
+}
+
+int rowscale_linear(const void* x, int64_t M, int64_t K, int64_t ldx, int x_dtype, const void* W_packed,
+                    int64_t N, const float* row_scale, void* y, int64_t ldy, int y_dtype, int path,
+                    void* stream) {
+  OpDesc d{x, M, K, ldx, x_dtype, W_packed, N, 0, y, ldy, fn::EPI_ROWSCALE, make_ep(0.0f, K), path,
+           (hipStream_t)stream};
+  d.ep.row_scale = row_scale;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  if ((s = check_auto_config(path))) return s;
+  if (M > 0 && !row_scale) return FN_ERR_NULL;
+  return run_op(d);
+}
+
 // Unfused baselines: normalise into the workspace, then the plain matrix multiply.
 static int baseline_common(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
                            const float* beta, const void* Wp, int64_t ncols, int glu, float eps, void* x_ws,

@@ -149,8 +149,8 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
       sa_t += red_sa[w][m];
     }
   }
-  const RowStat st = row_stat<EPI>(ss_t, sa_t, ep);
-  if constexpr (EPI == EPI_RMS) {
+  const RowStat st = row_stat_at<EPI>(ss_t, sa_t, ep, m, M);
+  if constexpr (epi_exports_s(EPI)) {
     if (ep.inv_rms && blockIdx.x == 0 && wave == 0 && lane < 16) ep.inv_rms[m] = st.s;
   }
   const int n_lane = (lane >> 4) * 4;
@@ -190,6 +190,11 @@ static hipError_t launch_decode_cfg(const DecodeArgs& p) {
 
 template <int EPI>
 static hipError_t launch_decode_epi(const DecodeArgs& p) {
+  if constexpr (EPI >= EPI_REGLU) {
+    // The epilogue family beyond the core kinds: the automatic configuration only.
+    if (p.cfg == 0 || p.cfg == 1) return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT>(p);
+    return hipErrorInvalidValue;
+  }
   // Configurations (NCB column blocks per workgroup, KSPLIT waves, U k blocks
   // per load set, double-buffered sets, non-temporal weight loads).  Measured on
   // MI355X (Llama-7B SwiGLU decode, 180 MB of weights): one wave per workgroup,
@@ -219,6 +224,11 @@ hipError_t launch_decode_bf16(const DecodeArgs& p) {
     case EPI_LN: return launch_decode_epi<EPI_LN>(p);
     case EPI_NONE: return launch_decode_epi<EPI_NONE>(p);
     case EPI_GLU_NOSCALE: return launch_decode_epi<EPI_GLU_NOSCALE>(p);
+    case EPI_REGLU: return launch_decode_epi<EPI_REGLU>(p);
+    case EPI_BILINEAR: return launch_decode_epi<EPI_BILINEAR>(p);
+    case EPI_GLU_DEFER: return launch_decode_epi<EPI_GLU_DEFER>(p);
+    case EPI_RELU_DEFER: return launch_decode_epi<EPI_RELU_DEFER>(p);
+    case EPI_ROWSCALE: return launch_decode_epi<EPI_ROWSCALE>(p);
   }
   return hipErrorInvalidValue;
 }

@@ -9,6 +9,7 @@
 // computes rows ty + 16 i and packed columns tx + 16 j, so columns j = 0, 1 (and
 // 2, 3) are a GLU gate block and its up block.
 #include "fn_device.h"
+#include "fn_epilogue.h"
 #include "fn_launch.h"
 
 namespace fn {
@@ -80,37 +81,26 @@ __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, i
     const int r = ty + 16 * i;
     const int m = m0 + r;
     if (m >= M) continue;
-    float s = 1.f, mu = 0.f;
-    if constexpr (EPI == EPI_RMS || EPI == EPI_GLU) {
-      s = rsqrtf(fmaf(row_ss[r], ep.inv_k, ep.eps));
-      if (EPI == EPI_RMS && ep.inv_rms && blockIdx.x == 0 && tx == 0) ep.inv_rms[m] = s;
-    } else if constexpr (EPI == EPI_LN) {
-      mu = row_sa[r] * ep.inv_k;
-      const float var = fmaxf(fmaf(row_ss[r], ep.inv_k, -mu * mu), 0.f);
-      s = rsqrtf(var + ep.eps);
+    const RowStat st = row_stat_at<EPI>(row_ss[r], row_sa[r], ep, m, M);
+    if constexpr (epi_exports_s(EPI)) {
+      if (ep.inv_rms && blockIdx.x == 0 && tx == 0) ep.inv_rms[m] = st.s;
     }
     float* yr = y + (int64_t)m * ldy;
     if constexpr (epi_is_glu(EPI)) {
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         const int f = p0 / 2 + 16 * q + tx;
-        const float gate = acc[i][2 * q], up = acc[i][2 * q + 1];
-        if (f < ncols)
-          yr[f] = EPI == EPI_GLU ? silu(gate * s) * (up * s) : silu(gate) * up;
+        if (f < ncols) yr[f] = epi_value<EPI>(acc[i][2 * q], acc[i][2 * q + 1], st, 0.f, 0.f);
       }
     } else {
+      const float* vp = epi_vec<EPI>(ep);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int c = p0 + tx + 16 * j;
         if (c >= ncols) continue;
-        float v = acc[i][j];
-        if constexpr (EPI == EPI_RMS) {
-          v *= s;
-          if (ep.bias) v += ep.bias[c];
-        } else if constexpr (EPI == EPI_LN) {
-          v = fmaf(fmaf(-mu, ep.colsum[c], v), s, ep.cstar ? ep.cstar[c] : 0.f);
-        }
-        yr[c] = v;
+        const float vec = vp ? vp[c] : 0.f;
+        const float cs = EPI == EPI_LN ? ep.colsum[c] : 0.f;
+        yr[c] = epi_value<EPI>(acc[i][j], acc[i][j], st, vec, cs);
       }
     }
   }
@@ -131,6 +121,11 @@ hipError_t launch_f32(const F32Args& p) {
     case EPI_LN: return launch_f32_epi<EPI_LN>(p);
     case EPI_NONE: return launch_f32_epi<EPI_NONE>(p);
     case EPI_GLU_NOSCALE: return launch_f32_epi<EPI_GLU_NOSCALE>(p);
+    case EPI_REGLU: return launch_f32_epi<EPI_REGLU>(p);
+    case EPI_BILINEAR: return launch_f32_epi<EPI_BILINEAR>(p);
+    case EPI_GLU_DEFER: return launch_f32_epi<EPI_GLU_DEFER>(p);
+    case EPI_RELU_DEFER: return launch_f32_epi<EPI_RELU_DEFER>(p);
+    case EPI_ROWSCALE: return launch_f32_epi<EPI_ROWSCALE>(p);
   }
   return hipErrorInvalidValue;
 }

@@ -162,17 +162,31 @@ __device__ __forceinline__ float sum8(const bf16x8& v, float acc) {
 
 __device__ __forceinline__ float silu(float t) { return t / (1.0f + __expf(-t)); }
 
-// Epilogue kinds of the fused kernels.
+// Epilogue kinds of the fused kernels.  s = 1/RMSe(a) = rsqrt(eps + sum a^2/K).
 enum Epi : int {
   EPI_RMS = 0,          // y = acc * s (+ bias)
-  EPI_GLU = 1,          // out = silu(s * gate) * (s * up)
+  EPI_GLU = 1,          // out = silu(s * gate) * (s * up)                  (Fig. 3(a))
   EPI_LN = 2,           // y = (acc - mu * colsum) * rstd + c*
   EPI_NONE = 3,         // y = acc                      (unfused baseline GEMM)
   EPI_GLU_NOSCALE = 4,  // out = silu(gate) * up        (unfused baseline GEMM)
+  EPI_REGLU = 5,        // out = relu(gate) * up * s^2  (both scales merged: 1/MSe)
+  EPI_BILINEAR = 6,     // out = gate * up * s^2
+  EPI_GLU_DEFER = 7,    // out = silu(s * gate) * up, s exported        (Fig. 3(b))
+  EPI_RELU_DEFER = 8,   // y = relu(acc), s exported                    (Fig. 2(b))
+  EPI_ROWSCALE = 9,     // y = acc * row_scale[m]   (applies a deferred scale)
 };
 
-constexpr bool epi_is_glu(int e) { return e == EPI_GLU || e == EPI_GLU_NOSCALE; }
-constexpr bool epi_needs_ss(int e) { return e == EPI_RMS || e == EPI_GLU || e == EPI_LN; }
+constexpr bool epi_is_glu(int e) {
+  return e == EPI_GLU || e == EPI_GLU_NOSCALE || e == EPI_REGLU || e == EPI_BILINEAR || e == EPI_GLU_DEFER;
+}
+constexpr bool epi_needs_ss(int e) {
+  return e == EPI_RMS || e == EPI_GLU || e == EPI_LN || e == EPI_REGLU || e == EPI_BILINEAR ||
+         e == EPI_GLU_DEFER || e == EPI_RELU_DEFER;
+}
+// Kinds whose per-row scale s = 1/RMSe(a) can be written to the inv_rms output.
+constexpr bool epi_exports_s(int e) {
+  return e == EPI_RMS || e == EPI_GLU || e == EPI_GLU_DEFER || e == EPI_RELU_DEFER;
+}
 
 struct EpiArgs {
   float eps;
@@ -180,7 +194,8 @@ struct EpiArgs {
   const float* bias;    // EPI_RMS: optional [N]
   const float* colsum;  // EPI_LN: [N]
   const float* cstar;   // EPI_LN: optional [N]
-  float* inv_rms;       // EPI_RMS: optional [M]
+  float* inv_rms;       // optional [M] output of s (kinds with epi_exports_s)
+  const float* row_scale;  // EPI_ROWSCALE: [M]
 };
 
 }  // namespace fn

@@ -13,16 +13,21 @@
 namespace fn {
 
 struct RowStat {
-  float s;   // 1/RMSe(a) (RMSNorm) or 1/sigma (LayerNorm); 1 for the baselines
+  float s;   // 1/RMSe(a) (RMSNorm kinds), 1/MSe(a) (ReGLU, bilinear), 1/sigma (LayerNorm),
+             // the given row scale (EPI_ROWSCALE); 1 for the baselines
   float mu;  // LayerNorm mean (0 otherwise)
 };
 
 template <int EPI>
 __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& ep) {
   RowStat st{1.0f, 0.0f};
-  if constexpr (EPI == EPI_RMS || EPI == EPI_GLU) {
+  if constexpr (EPI == EPI_RMS || EPI == EPI_GLU || EPI == EPI_GLU_DEFER || EPI == EPI_RELU_DEFER) {
     // RMSe(a) = sqrt(eps + ss/K)  (App. "RMS with epsilon")
     st.s = rsqrtf(fmaf(ss, ep.inv_k, ep.eps));
+  } else if constexpr (EPI == EPI_REGLU || EPI == EPI_BILINEAR) {
+    // both branch scales merged: 1/RMSe^2 = 1/MSe = 1/(eps + ss/K)  (App. "FFN with ReGLU
+    // and Bilinear GLU"; ReLU(s t) = s ReLU(t) for s >= 0)
+    st.s = 1.0f / fmaf(ss, ep.inv_k, ep.eps);
   } else if constexpr (EPI == EPI_LN) {
     float mu = sa * ep.inv_k;
     float var = fmaxf(fmaf(ss, ep.inv_k, -mu * mu), 0.0f);
@@ -32,6 +37,15 @@ __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& e
   (void)ss;
   (void)sa;
   (void)ep;
+  return st;
+}
+
+// Row statistics of output row m (< M for the rows that are stored): the kinds
+// that apply a scale computed elsewhere read it here.
+template <int EPI>
+__device__ __forceinline__ RowStat row_stat_at(float ss, float sa, const EpiArgs& ep, int m, int M) {
+  RowStat st = row_stat<EPI>(ss, sa, ep);
+  if constexpr (EPI == EPI_ROWSCALE) st.s = m < M ? ep.row_scale[m] : 0.0f;
   return st;
 }
 
@@ -51,7 +65,12 @@ __device__ __forceinline__ float epi_value(float v, float u, RowStat st, float v
   else if constexpr (EPI == EPI_GLU) return silu(v * st.s) * (u * st.s);
   else if constexpr (EPI == EPI_LN) return fmaf(fmaf(-st.mu, cs, v), st.s, vec);
   else if constexpr (EPI == EPI_NONE) return v;
-  else return silu(v) * u;  // EPI_GLU_NOSCALE
+  else if constexpr (EPI == EPI_GLU_NOSCALE) return silu(v) * u;
+  else if constexpr (EPI == EPI_REGLU) return (v > 0.0f ? v : 0.0f) * u * st.s;
+  else if constexpr (EPI == EPI_BILINEAR) return v * u * st.s;
+  else if constexpr (EPI == EPI_GLU_DEFER) return silu(v * st.s) * u;
+  else if constexpr (EPI == EPI_RELU_DEFER) return v > 0.0f ? v : 0.0f;
+  else return v * st.s;  // EPI_ROWSCALE
 }
 
 // The optional per-column vector of an epilogue (bias or c*), or nullptr.

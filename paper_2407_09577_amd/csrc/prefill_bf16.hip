@@ -314,7 +314,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   const int n0 = epi_is_glu(EPI) ? p0 / 2 : p0;
   const int n_lane = (lane >> 4) * 4;
   auto write_inv_rms = [&](int j, const RowStat& st) __attribute__((always_inline)) {
-    if constexpr (EPI == EPI_RMS) {
+    if constexpr (epi_exports_s(EPI)) {
       const int m = m0 + wm * TM + j * 16 + lrow;
       if (ep.inv_rms && wn == 0 && lane < 16 && m < M) ep.inv_rms[m] = st.s;
     }
@@ -325,9 +325,9 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     __syncthreads();  // every wave is done with the ring and the row totals
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
-      const RowStat st = row_stat<EPI>(ss[j], sa[j], ep);
-      write_inv_rms(j, st);
       const int r = wm * TM + j * 16 + lrow;
+      const RowStat st = row_stat_at<EPI>(ss[j], sa[j], ep, m0 + r, M);
+      write_inv_rms(j, st);
       if constexpr (epi_is_glu(EPI)) {
 #pragma unroll
         for (int i = 0; i < FN; i += 2) {
@@ -351,7 +351,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     for (int j = 0; j < FM; ++j) {
       const int mb = m0 + wm * TM + j * 16;
       const int m = mb + lrow;
-      const RowStat st = row_stat<EPI>(ss[j], sa[j], ep);
+      const RowStat st = row_stat_at<EPI>(ss[j], sa[j], ep, m, M);
       write_inv_rms(j, st);
       const bool rows_full = mb + 16 <= M;
       if constexpr (epi_is_glu(EPI)) {
@@ -423,6 +423,18 @@ template <int EPI>
 static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   int tile = p.tile;
   if (tile == TILE_AUTO) tile = auto_tile(p.M, p.NP, epi_is_glu(EPI));
+  if constexpr (EPI >= EPI_REGLU) {
+    // The epilogue family beyond the core kinds is built for the automatically
+    // chosen tiles only.
+    switch (tile) {
+      case TILE_256x256_W8_PF_SP: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
+      case TILE_128x128_W8T: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI>(p);
+      case TILE_128x96_W8:
+        if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
+        else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI>(p);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (tile) {
     case TILE_256x256: return launch_prefill_cfg<256, 256, 2, 2, 4, true, EPI>(p);
     case TILE_128x128: return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
@@ -459,6 +471,11 @@ hipError_t launch_prefill_bf16(const PrefillArgs& p) {
     case EPI_LN: return launch_prefill_epi<EPI_LN>(p);
     case EPI_NONE: return launch_prefill_epi<EPI_NONE>(p);
     case EPI_GLU_NOSCALE: return launch_prefill_epi<EPI_GLU_NOSCALE>(p);
+    case EPI_REGLU: return launch_prefill_epi<EPI_REGLU>(p);
+    case EPI_BILINEAR: return launch_prefill_epi<EPI_BILINEAR>(p);
+    case EPI_GLU_DEFER: return launch_prefill_epi<EPI_GLU_DEFER>(p);
+    case EPI_RELU_DEFER: return launch_prefill_epi<EPI_RELU_DEFER>(p);
+    case EPI_ROWSCALE: return launch_prefill_epi<EPI_ROWSCALE>(p);
   }
   return hipErrorInvalidValue;
 }

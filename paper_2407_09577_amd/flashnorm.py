@@ -20,6 +20,7 @@ FN_F32, FN_BF16 = 0, 1
 FN_LAYOUT_LINEAR, FN_LAYOUT_GLU = 0, 1
 FN_PATH_AUTO, FN_PATH_PREFILL, FN_PATH_DECODE = 0, 1, 2
 FN_DECODE_MAX_M = 16
+FN_GLU_SWIGLU, FN_GLU_REGLU, FN_GLU_BILINEAR, FN_GLU_SWIGLU_DEFER_UP = 0, 1, 2, 3
 
 STATUS = {0: "FN_OK", -1: "FN_ERR_NULL", -2: "FN_ERR_SHAPE", -3: "FN_ERR_DTYPE", -4: "FN_ERR_ALIGN",
           -5: "FN_ERR_UNSUPPORTED", -6: "FN_ERR_VALUE", -7: "FN_ERR_HIP", -8: "FN_ERR_ALIAS",
@@ -55,6 +56,9 @@ def _load():
         "baseline_rmsnorm_linear": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P], I),
         "baseline_rmsnorm_glu": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P], I),
         "baseline_layernorm_linear": ([P, I64, I64, I64, I, P, P, P, I64, F, P, P, I64, I, P], I),
+        "flashnorm_glu_act": ([P, I64, I64, I64, I, P, I64, F, I, P, I64, I, P, I, P], I),
+        "flashnorm_linear_relu": ([P, I64, I64, I64, I, P, I64, F, P, I64, I, P, I, P], I),
+        "rowscale_linear": ([P, I64, I64, I64, I, P, I64, P, P, I64, I, I, P], I),
         "flashnorm_status_string": ([I], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -160,6 +164,39 @@ def flashnorm_glu(a: torch.Tensor, W_star_gu: torch.Tensor, F: int, eps: float, 
     _check(_load().flashnorm_glu_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star_gu), F, eps, _ptr(o), _ld(o),
                                     _dt(o), path, _stream(stream)), "flashnorm_glu")
     return o
+
+
+def flashnorm_glu_act(a: torch.Tensor, W_star_gu: torch.Tensor, F: int, eps: float, act: int, out=None,
+                      inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    """GLU-variant FFN input projection (act = FN_GLU_*); inv_rms receives s = 1/RMSe(a) where allowed."""
+    M, K = a.shape
+    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    _check(_load().flashnorm_glu_act(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star_gu), F, eps, act, _ptr(o),
+                                     _ld(o), _dt(o), _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
+           "flashnorm_glu_act")
+    return o
+
+
+def flashnorm_linear_relu(a: torch.Tensor, W_star: torch.Tensor, N: int, eps: float, inv_rms: torch.Tensor,
+                          out=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    """ReLU FFN up projection with the scale deferred: y = relu(a W*), inv_rms = 1/RMSe(a)."""
+    M, K = a.shape
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    _check(_load().flashnorm_linear_relu(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star), N, eps, _ptr(y), _ld(y),
+                                         _dt(y), _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
+           "flashnorm_linear_relu")
+    return y
+
+
+def rowscale_linear(x: torch.Tensor, W_packed: torch.Tensor, N: int, row_scale: torch.Tensor, out=None,
+                    path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    """y = (x W) * row_scale[m]: applies a normalisation scale deferred to this layer's output."""
+    M, K = x.shape
+    y = out if out is not None else torch.empty(M, N, dtype=x.dtype, device=x.device)
+    _check(_load().rowscale_linear(_ptr(x), M, K, _ld(x), _dt(x), _ptr(W_packed), N,
+                                   _ptr(_vec(row_scale, M, "row_scale")), _ptr(y), _ld(y), _dt(y), path,
+                                   _stream(stream)), "rowscale_linear")
+    return y
 
 
 def flashnorm_layernorm_linear(a: torch.Tensor, W_star: torch.Tensor, colsum: torch.Tensor, c_star, N: int,

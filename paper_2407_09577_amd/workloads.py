@@ -59,6 +59,14 @@ class Workload:
         return self.a.dtype
 
 
+def weight(K: int, N: int, *, dtype=torch.bfloat16, seed: int = 0) -> torch.Tensor:
+    """A further seeded weight [K, N] ~ N(0, 1/K) (e.g. an FFN down projection), drawn in fp32
+    and cast once to dtype."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed)
+    return (torch.randn(K, N, generator=gen, dtype=torch.float32) * K ** -0.5).to(dtype)
+
+
 def make(kind: str, M: int, K: int, N: int, *, dtype=torch.bfloat16, eps: float = 1e-6,
          seed: int = 0, a_mean: float = 0.0, outlier_frac: float = 0.0,
          outlier_scale: float = 20.0, name: str = "") -> Workload:

@@ -152,3 +152,22 @@ def test_vector_alignment_validation(fnlib):
     assert lib.flashnorm_linear_ex(A, 4, 64, 64, 1, W, 32, 1e-6, X + 4, Y, 32, 1, None, 0, None) == -4
     assert lib.flashnorm_layernorm_linear_ex(A, 4, 64, 64, 1, W, X + 8, None, 32, 1e-5, Y, 32, 1, 0, None) == -4
     assert lib.flashnorm_layernorm_linear_ex(A, 4, 64, 64, 1, W, X, X + 4, 32, 1e-5, Y, 32, 1, 0, None) == -4
+
+
+def test_epilogue_family_validation(fnlib):
+    lib = fnlib.lib()
+    ga = lambda **kw: lib.flashnorm_glu_act(A, kw.get("M", 4), 64, 64, 1, W, 16, 1e-6, kw.get("act", 0), Y, 16, 1,
+                                            kw.get("inv", None), kw.get("path", 0), None)
+    assert ga(act=7) == -6                          # unknown gate nonlinearity
+    assert ga(act=3) == -1                          # deferred up scale: inv_rms must be given
+    assert ga(act=1, inv=X) == -6                   # ReGLU / bilinear carry the whole scale
+    assert ga(act=2, inv=X) == -6
+    assert ga(act=0, path=1 | (3 << 8)) == -5       # forced tile: automatic configuration only
+    assert ga(act=3, M=0) == 0                      # M == 0: no-op
+    lr = lambda **kw: lib.flashnorm_linear_relu(A, 4, 64, 64, 1, W, 32, 1e-6, Y, 32, 1, kw.get("inv", X),
+                                                kw.get("path", 0), None)
+    assert lr(inv=0) == -1
+    assert lr(path=2 | (1 << 8)) == -5
+    rs = lambda **kw: lib.rowscale_linear(A, 4, 64, 64, 1, W, 32, kw.get("s", X), Y, 32, kw.get("ydt", 1), 0, None)
+    assert rs(s=0) == -1
+    assert rs(ydt=0) == -3

@@ -360,3 +360,59 @@ def test_graph_replay_matches_eager(fn):
         torch.cuda.synchronize()
         for got, want in zip((yl, yg, yn), ref):
             assert torch.equal(got.view(torch.int16), want.view(torch.int16)), f"replay {it}"
+
+
+# ------------------------------------------- epilogue family and deferred FFNs
+GLU_ACTS = {"swiglu": (0, 0), "reglu": (1, 1), "bilinear": (2, 2)}   # C-ABI act, oracle act
+
+
+@pytest.mark.parametrize("name", list(GLU_ACTS))
+@pytest.mark.parametrize("dtype,M,K,F,path", [(torch.bfloat16, 300, 328, 80, 1), (torch.bfloat16, 1, 1032, 72, 2),
+                                              (torch.bfloat16, 7, 1032, 72, 2), (torch.bfloat16, 16, 576, 48, 2),
+                                              (torch.float32, 37, 96, 40, 0)])
+def test_glu_variants(fn, name, dtype, M, K, F, path):
+    act, oact = GLU_ACTS[name]
+    w = workloads.make("glu", M, K, F, dtype=dtype, eps=1e-5, seed=61 + act + M, outlier_frac=0.05)
+    ws_dt = fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), layout=fn.FN_LAYOUT_GLU, ws_dtype=ws_dt)
+    inv = torch.empty(M, dtype=torch.float32, device=DEV) if act == 0 else None
+    out = fn.flashnorm_glu_act(w.a.to(DEV), Ws, F, w.eps, act, inv_rms=inv, path=path)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm_glu_act(w.a, w.g, w.W, w.eps, oact)
+    assert row_err(to_np(out), ref) <= TOL[dtype]
+    if inv is not None:
+        want = np.array([1.0 / oracle.rms(r, w.eps) for r in w.a.double().numpy()])
+        np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
+
+
+@pytest.mark.parametrize("kind", ["relu", "swiglu_defer", "reglu"])
+@pytest.mark.parametrize("dtype,M,K,F,N,path", [(torch.bfloat16, 300, 328, 200, 144, 1),
+                                                (torch.bfloat16, 9, 1024, 160, 96, 2),
+                                                (torch.float32, 33, 64, 48, 40, 0)])
+def test_deferred_ffn(fn, kind, dtype, M, K, F, N, path):
+    # The normalisation scale travels to the FFN output: App. "FFN with ReLU" (Fig. 2(b)),
+    # Fig. 3(b) (SwiGLU, up scale deferred) and App. "FFN with ReGLU" (both scales merged
+    # into the input projection, 1/MS).  Compared with the whole FFN in standard form.
+    glu = kind != "relu"
+    w = workloads.make("glu" if glu else "linear", M, K, F, dtype=dtype, eps=1e-5, seed=71 + M + len(kind))
+    Wd = workloads.weight(F, N, dtype=dtype, seed=72 + M)
+    ws_dt = fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32
+    a = w.a.to(DEV)
+    Wup, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), layout=fn.FN_LAYOUT_GLU if glu else fn.FN_LAYOUT_LINEAR,
+                                ws_dtype=ws_dt)
+    Wdp, _, _ = fn.fold_weights(Wd.to(DEV), None, ws_dtype=ws_dt)
+    s = torch.empty(M, dtype=torch.float32, device=DEV)
+    if kind == "relu":
+        h = fn.flashnorm_linear_relu(a, Wup, F, w.eps, s, path=path)
+        oact = oracle.FFN_RELU
+    elif kind == "swiglu_defer":
+        h = fn.flashnorm_glu_act(a, Wup, F, w.eps, fn.FN_GLU_SWIGLU_DEFER_UP, inv_rms=s, path=path)
+        oact = oracle.GLU_SWIGLU
+    else:
+        h = fn.flashnorm_glu_act(a, Wup, F, w.eps, fn.FN_GLU_REGLU, path=path)
+        s.fill_(1.0)
+        oact = oracle.GLU_REGLU
+    y = fn.rowscale_linear(h, Wdp, N, s, path=path)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm_ffn(w.a, w.g, w.W, Wd, w.eps, oact)
+    assert row_err(to_np(y), ref) <= TOL[dtype]
