@@ -216,6 +216,28 @@ int rowscale_linear(const void* x, int64_t M, int64_t K, int64_t ldx, int x_dtyp
                     const void* W_packed, int64_t N, const float* row_scale, void* y,
                     int64_t ldy, int y_dtype, int path, void* stream);
 
+/* Deferred normalisation with the UNFOLDED weight (Remark "Unfolded case": the
+ * deferral of Prop. 2 needs only that 1/RMS is a per-token scalar, so it serves a
+ * checkpoint as it is, with g applied at run time instead of folded into W):
+ *   flashnorm_linear_unfolded:  y = (sum_k bf(a[m,k] g_k) W[k,n]) * s_m (+ bias[n])
+ *   flashnorm_glu_unfolded:     out = silu(s_m hg) * (s_m hu), hg/hu from bf(a g) [Wg | Wu]
+ * where s_m = 1/sqrt(eps + ss_m/K) with ss_m the squares of the RAW activations, and
+ * bf() is the activation dtype: each product a_k g_k is rounded once to it before
+ * the matrix multiply (the folded path instead rounds g_k W[k,n] once).
+ *   g         [K] fp32 (required), 16-byte aligned.
+ *   W_packed  the unfolded weight packed by fold_weights(..., g = NULL, ...), with
+ *             FN_LAYOUT_LINEAR or FN_LAYOUT_GLU respectively.
+ * Other arguments as for flashnorm_linear / flashnorm_glu; path as for
+ * flashnorm_glu_act.  The bf16 tile path stages g in LDS and takes K <= 8128
+ * (FN_ERR_UNSUPPORTED beyond; the decode and fp32 paths have no such limit). */
+int flashnorm_linear_unfolded(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                              const float* g, const void* W_packed, int64_t N, float eps,
+                              const float* bias, void* y, int64_t ldy, int y_dtype, float* inv_rms,
+                              int path, void* stream);
+int flashnorm_glu_unfolded(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                           const float* g, const void* W_packed_gu, int64_t F, float eps, void* out,
+                           int64_t ldo, int out_dtype, int path, void* stream);
+
 /* Unfused baselines in the same library (the sequential RMSNorm -> GEMM of Fig. 1(a)
  * and Sec. 6): a normalisation kernel writes the normalised activations
  * x = RMSNorm(a; g) (or LayerNorm(a; g, beta)) to the caller's workspace x_ws

@@ -62,6 +62,7 @@ struct OpDesc {
   EpiArgs ep;
   int path;
   hipStream_t stream;
+  bool gs = false;  // run-time g in ep.g_rt, unfolded packed W
 };
 
 // Validation shared by the three fused ops (and the baselines' matrix multiply).
@@ -102,7 +103,7 @@ int run_op(const OpDesc& d) {
   const int NP = (int)fn::packed_cols(N, d.glu), KP = (int)fn::packed_rows(d.K);
   if (d.dtype == FN_F32) {
     fn::F32Args p{(const float*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const float*)d.ws, NP, KP,
-                  (int)d.ncols, (float*)d.y, (int)d.ldy, d.epi, d.ep, d.stream};
+                  (int)d.ncols, (float*)d.y, (int)d.ldy, d.epi, d.ep, d.stream, d.gs};
     return status_of(fn::launch_f32(p));
   }
   const int base_path = d.path & 0xff;
@@ -110,12 +111,12 @@ int run_op(const OpDesc& d) {
   if (decode) {
     fn::DecodeArgs p{(const __bf16*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const __bf16*)d.ws, NP, KP,
                      (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, d.path >> FN_PATH_TILE_SHIFT, d.ep,
-                     d.stream};
+                     d.stream, d.gs};
     return status_of(fn::launch_decode_bf16(p));
   }
   fn::PrefillArgs p{(const __bf16*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const __bf16*)d.ws, NP, KP,
                     (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, d.path >> FN_PATH_TILE_SHIFT, d.ep,
-                    d.stream};
+                    d.stream, d.gs};
   return status_of(fn::launch_prefill_bf16(p));
 }
 
@@ -276,6 +277,47 @@ int rowscale_linear(const void* x, int64_t M, int64_t K, int64_t ldx, int x_dtyp
   if (s) return s;
   if ((s = check_auto_config(path))) return s;
   if (M > 0 && !row_scale) return FN_ERR_NULL;
+  return run_op(d);
+}
+
+// Run-time g (unfolded W): g must be given, 16-byte aligned; the bf16 tile path
+// stages g in LDS and takes K <= fn::kGsMaxK.
+static int check_runtime_g(const OpDesc& d, const float* g) {
+  if (d.M > 0 && !g) return FN_ERR_NULL;
+  if (!aligned16(g)) return FN_ERR_ALIGN;
+  if (d.M > 0 && overlaps(d.y, extent_bytes(d.M, d.ncols, d.ldy, d.dtype), g, d.K * (int64_t)sizeof(float)))
+    return FN_ERR_ALIAS;
+  const int base_path = d.path & 0xff;
+  const bool decode = base_path == FN_PATH_DECODE || (base_path == FN_PATH_AUTO && d.M <= FN_DECODE_MAX_M);
+  if (d.dtype == FN_BF16 && !decode && d.K > fn::kGsMaxK) return FN_ERR_UNSUPPORTED;
+  return check_auto_config(d.path);
+}
+
+int flashnorm_linear_unfolded(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
+                              const void* W_packed, int64_t N, float eps, const float* bias, void* y, int64_t ldy,
+                              int y_dtype, float* inv_rms, int path, void* stream) {
+  OpDesc d{a, M, K, lda, a_dtype, W_packed, N, 0, y, ldy, fn::EPI_RMS, make_ep(eps, K), path, (hipStream_t)stream};
+  d.ep.bias = bias;
+  d.ep.inv_rms = inv_rms;
+  d.ep.g_rt = g;
+  d.gs = true;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  if (!aligned16(bias)) return FN_ERR_ALIGN;
+  if ((s = check_runtime_g(d, g))) return s;
+  return run_op(d);
+}
+
+int flashnorm_glu_unfolded(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
+                           const void* W_packed_gu, int64_t F, float eps, void* out, int64_t ldo, int out_dtype,
+                           int path, void* stream) {
+  OpDesc d{a, M, K, lda, a_dtype, W_packed_gu, F, 1, out, ldo, fn::EPI_GLU, make_ep(eps, K), path,
+           (hipStream_t)stream};
+  d.ep.g_rt = g;
+  d.gs = true;
+  int s = validate_op(d, out_dtype);
+  if (s) return s;
+  if ((s = check_runtime_g(d, g))) return s;
   return run_op(d);
 }
 

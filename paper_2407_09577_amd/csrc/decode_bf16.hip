@@ -22,7 +22,7 @@
 
 namespace fn {
 
-template <int NCB, int KSPLIT, int U, bool DB, int CPOL, int EPI>
+template <int NCB, int KSPLIT, int U, bool DB, int CPOL, int EPI, bool GS = false>
 __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep) {
@@ -61,24 +61,46 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
   // One set = U k blocks of this wave (kb, kb + KSPLIT, ...): U activation
   // fragments and U x NCB weight fragments, one 16-byte load per lane each.
   // Blocks past K read as zeros.
-  auto load_set = [&](int kb0, u32x4 (&af)[U], u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
+  // GS: run-time g (unfolded W): the 8 values of g at this lane's k chunk come
+  // with each activation fragment (zeros past K).
+  const __amdgpu_buffer_rsrc_t rs_g = make_rsrc(ep.g_rt, GS ? (uint32_t)K * 4u : 0u);
+  f32x4 gv0[GS ? U : 1][2], gv1[GS ? U : 1][2];
+  auto load_set = [&](int kb0, u32x4 (&af)[U], u32x4 (&wf)[U][NCB], f32x4 (&gv)[GS ? U : 1][2])
+                      __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kb = kb0 + KSPLIT * u;
       const int k = kb * kKB + lk;
       const bool kb_ok = kb < KB;
       af[u] = load_buf16(rs_a, (kb_ok && row_ok && k < K) ? a_row_off + (unsigned)k * 2 : kOobOffset);
+      if constexpr (GS) {
+        const unsigned go = (kb_ok && k < K) ? (unsigned)k * 4 : kOobOffset;
+        gv[u][0] = __builtin_bit_cast(f32x4, load_buf16(rs_g, go));
+        gv[u][1] = __builtin_bit_cast(f32x4, load_buf16(rs_g, go == kOobOffset ? go : go + 16));
+      }
 #pragma unroll
       for (int c = 0; c < NCB; ++c)
         wf[u][c] = load_buf16<CPOL>(rs_w, kb_ok ? (unsigned)((kb * npb + c) * kFragBytes + lane * 16) : kOobOffset);
     }
   };
-  auto compute_set = [&](const u32x4 (&af)[U], const u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
+  auto compute_set = [&](const u32x4 (&af)[U], const u32x4 (&wf)[U][NCB], const f32x4 (&gv)[GS ? U : 1][2])
+                         __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const bf16x8 av = __builtin_bit_cast(bf16x8, af[u]);
+      bf16x8 av = __builtin_bit_cast(bf16x8, af[u]);
       if constexpr (kSS) ss = sumsq8(av, ss);
       if constexpr (kSA) sa = sum8(av, sa);
+      if constexpr (GS) {  // a_k g_k, rounded once to bf16
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[e] = (float)av[e] * gv[u][0][e];
+          o[4 + e] = (float)av[4 + e] * gv[u][1][e];
+        }
+        const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
+        const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
+        av = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+      }
 #pragma unroll
       for (int c = 0; c < NCB; ++c)
         acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[u][c]), av,
@@ -92,22 +114,22 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     // current set is consumed, so every wave keeps a full set in flight.  Sets
     // past K are issued as zero-returning loads, which keeps the loop uniform.
     u32x4 af0[U], wf0[U][NCB], af1[U], wf1[U][NCB];
-    load_set(wave, af0, wf0);
+    load_set(wave, af0, wf0, gv0);
     for (int kb0 = wave; kb0 < KB; kb0 += 2 * STEP) {
-      load_set(kb0 + STEP, af1, wf1);
+      load_set(kb0 + STEP, af1, wf1, gv1);
       __builtin_amdgcn_sched_barrier(0);
-      compute_set(af0, wf0);
+      compute_set(af0, wf0, gv0);
       __builtin_amdgcn_sched_barrier(0);
-      load_set(kb0 + 2 * STEP, af0, wf0);
+      load_set(kb0 + 2 * STEP, af0, wf0, gv0);
       __builtin_amdgcn_sched_barrier(0);
-      compute_set(af1, wf1);
+      compute_set(af1, wf1, gv1);
       __builtin_amdgcn_sched_barrier(0);
     }
   } else {
     for (int kb0 = wave; kb0 < KB; kb0 += STEP) {
       u32x4 af[U], wf[U][NCB];
-      load_set(kb0, af, wf);
-      compute_set(af, wf);
+      load_set(kb0, af, wf, gv0);
+      compute_set(af, wf, gv0);
     }
   }
 
@@ -180,16 +202,21 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     epilogue(std::false_type{});
 }
 
-template <int NCB, int KSPLIT, int U, int EPI, bool DB = false, int CPOL = 0>
+template <int NCB, int KSPLIT, int U, int EPI, bool DB = false, int CPOL = 0, bool GS = false>
 static hipError_t launch_decode_cfg(const DecodeArgs& p) {
   const int nblocks = (p.NP / 16 + NCB - 1) / NCB;
-  hipLaunchKernelGGL((decode_bf16_kernel<NCB, KSPLIT, U, DB, CPOL, EPI>), dim3(nblocks), dim3(KSPLIT * 64), 0,
+  hipLaunchKernelGGL((decode_bf16_kernel<NCB, KSPLIT, U, DB, CPOL, EPI, GS>), dim3(nblocks), dim3(KSPLIT * 64), 0,
                      p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y, p.ldy, p.ep);
   return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_decode_epi(const DecodeArgs& p) {
+  if (p.gs) {  // run-time g: RMS kinds, the automatic configuration
+    if constexpr (EPI == EPI_RMS || EPI == EPI_GLU)
+      if (p.cfg == 0 || p.cfg == 1) return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT, true>(p);
+    return hipErrorInvalidValue;
+  }
   if constexpr (EPI >= EPI_REGLU) {
     // The epilogue family beyond the core kinds: the automatic configuration only.
     if (p.cfg == 0 || p.cfg == 1) return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT>(p);

@@ -14,7 +14,7 @@
 
 namespace fn {
 
-template <int EPI>
+template <int EPI, bool GS = false>
 __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, int M, int K, int lda,
                                                   const float* __restrict__ ws, int NP, int KP,
                                                   int ncols, float* __restrict__ y, int ldy,
@@ -44,6 +44,15 @@ __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, i
     ss = fmaf(av.z, av.z, ss);
     ss = fmaf(av.w, av.w, ss);
     sa += (av.x + av.y) + (av.z + av.w);
+    if constexpr (GS) {  // run-time g (unfolded W): a_k g_k in fp32
+      if (lr_ok && k0 + lkq < K) {
+        const float4 gv = *reinterpret_cast<const float4*>(ep.g_rt + k0 + lkq);
+        av.x *= gv.x;
+        av.y *= gv.y;
+        av.z *= gv.z;
+        av.w *= gv.w;
+      }
+    }
     float4 wv = make_float4(0.f, 0.f, 0.f, 0.f);
     if (wc_ok) wv = *reinterpret_cast<const float4*>(ws + (int64_t)(k0 + wk) * NP + p0 + wc);
     __syncthreads();
@@ -106,15 +115,20 @@ __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, i
   }
 }
 
-template <int EPI>
+template <int EPI, bool GS = false>
 static hipError_t launch_f32_epi(const F32Args& p) {
   dim3 grid((p.NP + 63) / 64, (p.M + 63) / 64);
-  hipLaunchKernelGGL(f32_kernel<EPI>, grid, dim3(256), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP,
+  hipLaunchKernelGGL((f32_kernel<EPI, GS>), grid, dim3(256), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP,
                      p.KP, p.ncols, p.y, p.ldy, p.ep);
   return hipGetLastError();
 }
 
 hipError_t launch_f32(const F32Args& p) {
+  if (p.gs) {  // run-time g: RMS kinds
+    if (p.epi == EPI_RMS) return launch_f32_epi<EPI_RMS, true>(p);
+    if (p.epi == EPI_GLU) return launch_f32_epi<EPI_GLU, true>(p);
+    return hipErrorInvalidValue;
+  }
   switch (p.epi) {
     case EPI_RMS: return launch_f32_epi<EPI_RMS>(p);
     case EPI_GLU: return launch_f32_epi<EPI_GLU>(p);

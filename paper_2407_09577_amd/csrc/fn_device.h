@@ -196,6 +196,7 @@ struct EpiArgs {
   const float* cstar;   // EPI_LN: optional [N]
   float* inv_rms;       // optional [M] output of s (kinds with epi_exports_s)
   const float* row_scale;  // EPI_ROWSCALE: [M]
+  const float* g_rt;       // run-time normalisation weight [K] (unfolded W), or nullptr
 };
 
 }  // namespace fn

@@ -41,6 +41,10 @@ inline int64_t packed_cols(int64_t N, int glu) {
 }
 inline int64_t packed_rows(int64_t K) { return round_up(K, kKPad); }
 
+// Largest K of the bf16 run-time-g prefill path: g is staged once in LDS
+// (kGsMaxK + 64 floats beside a 128 KiB ring fill the 160 KiB).
+constexpr int kGsMaxK = 8128;
+
 struct PrefillArgs {
   const __bf16* a;
   int M, K, lda;
@@ -53,6 +57,7 @@ struct PrefillArgs {
   int tile;
   EpiArgs ep;
   hipStream_t stream;
+  bool gs;  // run-time g (ep.g_rt) applied to the activations; unfolded W
 };
 hipError_t launch_prefill_bf16(const PrefillArgs& p);
 
@@ -68,6 +73,7 @@ struct DecodeArgs {
   int cfg;  // decode configuration (0 = automatic), see launch_decode_bf16
   EpiArgs ep;
   hipStream_t stream;
+  bool gs;  // run-time g (ep.g_rt) applied to the activations; unfolded W
 };
 hipError_t launch_decode_bf16(const DecodeArgs& p);
 constexpr int kDecodeCfgCount = 13;
@@ -83,6 +89,7 @@ struct F32Args {
   int epi;
   EpiArgs ep;
   hipStream_t stream;
+  bool gs;  // run-time g (ep.g_rt) applied to the activations; unfolded W
 };
 hipError_t launch_f32(const F32Args& p);
 

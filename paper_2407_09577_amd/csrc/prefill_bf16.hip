@@ -40,7 +40,7 @@ __device__ __forceinline__ void wait_ahead(int ahead) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false>
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false>
 __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep, int tiles_m, int tiles_n) {
@@ -61,9 +61,18 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   static_assert(NRD <= NMF && LOADS <= NRD, "schedule needs at least one op per group");
   constexpr bool kSS = epi_needs_ss(EPI);
   constexpr bool kSA = EPI == EPI_LN;
+  // GS: the normalisation weight g is applied at run time to the activation
+  // tiles (unfolded W; Remark "Unfolded case"), once per workgroup: every
+  // fragment of block kb+2 is scaled in LDS during block kb by the wave that owns
+  // its row block, which also takes the row's squares from the raw values.
+  static_assert(!GS || (PF && A_FRAGS % NW == 0 && (EPI == EPI_RMS || EPI == EPI_GLU) && STAGES >= 4),
+                "run-time g: prefetching ring, even split of row blocks, RMS kinds");
+  constexpr int SPW = GS ? A_FRAGS / NW : 0;  // row blocks each wave scales
 
   // STAGES ring of k blocks, plus one slot that absorbs padding loads.
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE + (kUneven ? kFragBytes : 0)];
+  // Run-time g (GS), staged once: g[k] for k < K, zeros up to kGsMaxK + 64.
+  __shared__ __attribute__((aligned(16))) float g_lds[GS ? kGsMaxK + 64 : 4];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -157,6 +166,37 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
   };
 
+  // GS: scale the activation fragments of block b in place, g applied per k
+  // (each product rounded once to bf16), and take the row squares from the raw
+  // values.  The lane reads the 16 bytes it transferred: row t_row of the row
+  // block, k chunk lk of the block (the transfer layout of the ring).
+  float ss_own[SPW > 0 ? SPW : 1];
+#pragma unroll
+  for (int t = 0; t < (SPW > 0 ? SPW : 1); ++t) ss_own[t] = 0.f;
+  auto scale_block = [&](int b) __attribute__((always_inline)) {
+    if constexpr (GS) {
+      char* st = smem + (b % STAGES) * STAGE;
+      const float* gk = g_lds + b * kKB + lk;
+      const f32x4 g0 = *reinterpret_cast<const f32x4*>(gk);
+      const f32x4 g1 = *reinterpret_cast<const f32x4*>(gk + 4);
+#pragma unroll
+      for (int t = 0; t < SPW; ++t) {
+        u32x4* p = reinterpret_cast<u32x4*>(st + (wave + NW * t) * kFragBytes + lane * 16);
+        const bf16x8 v = __builtin_bit_cast(bf16x8, *p);
+        ss_own[t] = sumsq8(v, ss_own[t]);
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[e] = (float)v[e] * g0[e];
+          o[4 + e] = (float)v[4 + e] * g1[e];
+        }
+        const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
+        const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
+        *p = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      }
+    }
+  };
+
   auto sync_block = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS reads have landed
     __builtin_amdgcn_s_barrier();
@@ -176,8 +216,10 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
                                   bf16x8 (&afn)[FM], bf16x8 (&wfn)[FN], bool more)
                                   __attribute__((always_inline)) {
     constexpr int WNC = decltype(wnc)::value;
+    if constexpr (!GS) {
 #pragma unroll
-    for (int j = WNC; j < FM; j += WN) stats_one(j, afc);
+      for (int j = WNC; j < FM; j += WN) stats_one(j, afc);
+    }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int g = 0; g < NRD; ++g) {
@@ -214,22 +256,40 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   for (int s = 0; s < (PF ? STAGES : STAGES - 1); ++s)
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) load_one(s, i);
+  // GS: the run-time g goes to LDS once (zeros past K), after the first
+  // transfers are on their way.
+  if constexpr (GS) {
+    for (int i = threadIdx.x; i < kGsMaxK + 64; i += NW * 64) g_lds[i] = i < K ? ep.g_rt[i] : 0.f;
+  }
+  // GS needs block kb+2 landed (and scaled during block kb) before block kb+1
+  // reads it; otherwise block kb+1 must have landed before step kb.
+  constexpr int kAheadWait = GS ? (STAGES - 3) * LOADS : (STAGES - 2) * LOADS;
   auto mainloop = [&](auto wnc) __attribute__((always_inline)) {
     constexpr int WNC = decltype(wnc)::value;
     if constexpr (PF) {
-      wait_vmcnt<(STAGES - 1) * LOADS>();
-      sync_block();
+      if constexpr (GS) {
+        wait_vmcnt<(STAGES - 2) * LOADS>();  // blocks 0 and 1
+        sync_block();
+        scale_block(0);
+        scale_block(1);
+        sync_block();
+      } else {
+        wait_vmcnt<(STAGES - 1) * LOADS>();
+        sync_block();
+      }
 #pragma unroll
       for (int r = 0; r < NRD; ++r) read_one(0, r, af0, wf0);
       for (int kb = 0; kb < nkb - 2; kb += 2) {
-        wait_vmcnt<(STAGES - 2) * LOADS>();
+        wait_vmcnt<kAheadWait>();
         sync_block();
+        scale_block(kb + 2);
         multiply_interleaved(wnc, kb, af0, wf0, af1, wf1, true);
-        wait_vmcnt<(STAGES - 2) * LOADS>();
+        wait_vmcnt<kAheadWait>();
         sync_block();
+        scale_block(kb + 3);
         multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true);
       }
-      wait_vmcnt<(STAGES - 2) * LOADS>();
+      wait_vmcnt<kAheadWait>();
       sync_block();
       multiply_interleaved(wnc, nkb - 2, af0, wf0, af1, wf1, true);
       __builtin_amdgcn_s_waitcnt(0xc07f);
@@ -252,9 +312,9 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     }
   };
   // One copy of the main loop per column-wave index (wave-uniform dispatch); a
-  // single copy when there are no row statistics to split.
+  // single copy when there are no row statistics to split (or GS takes them).
   static_assert(WN <= 4, "mainloop dispatch covers up to 4 column waves");
-  if constexpr (!kSS && !kSA) {
+  if constexpr ((!kSS && !kSA) || GS) {
     mainloop(std::integral_constant<int, 0>{});
   } else switch (wn) {
     case 0: mainloop(std::integral_constant<int, 0>{}); break;
@@ -263,6 +323,25 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     default: if constexpr (WN > 3) mainloop(std::integral_constant<int, 3>{}); break;
   }
 
+  // GS: the squares were taken by the wave that scaled each row block: lanes
+  // 4r .. 4r+3 hold disjoint k of row r.  Totals reach the waves through LDS.
+  if constexpr (GS) {
+    float (*row_tot)[BM] = reinterpret_cast<float (*)[BM]>(smem);
+#pragma unroll
+    for (int t = 0; t < SPW; ++t) {
+      ss_own[t] += __shfl_xor(ss_own[t], 1);
+      ss_own[t] += __shfl_xor(ss_own[t], 2);
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+    if ((lane & 3) == 0) {
+#pragma unroll
+      for (int t = 0; t < SPW; ++t) row_tot[0][(wave + NW * t) * 16 + t_row] = ss_own[t];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < FM; ++j) ss[j] = row_tot[0][wm * TM + j * 16 + lrow];
+  } else
   // Row statistics: lanes l, l^16, l^32, l^48 hold disjoint k of the same row.
   // Each fragment's totals live in the one wave of the row band that squared it;
   // they reach the other WN-1 waves through LDS.
@@ -391,12 +470,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     direct(std::false_type{});
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false>
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false>
 static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = (p.NP + BN - 1) / BN;
   const int nblocks = tiles_m * tiles_n;
-  hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI, SPREAD>), dim3(nblocks),
+  hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI, SPREAD, GS>), dim3(nblocks),
                      dim3(WM * WN * 64), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y,
                      p.ldy, p.ep, tiles_m, tiles_n);
   return hipGetLastError();
@@ -423,6 +502,20 @@ template <int EPI>
 static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   int tile = p.tile;
   if (tile == TILE_AUTO) tile = auto_tile(p.M, p.NP, epi_is_glu(EPI));
+  if constexpr (EPI == EPI_RMS || EPI == EPI_GLU) {
+    if (p.gs) {  // run-time g: the automatically chosen tiles only
+      switch (tile) {
+        case TILE_256x256_W8_PF_SP: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true, true>(p);
+        case TILE_128x128_W8T: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, false, true>(p);
+        case TILE_128x96_W8:
+          if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, false, true>(p);
+          else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI, false, true>(p);
+      }
+      return hipErrorInvalidValue;
+    }
+  } else {
+    if (p.gs) return hipErrorInvalidValue;
+  }
   if constexpr (EPI >= EPI_REGLU) {
     // The epilogue family beyond the core kinds is built for the automatically
     // chosen tiles only.

@@ -59,6 +59,8 @@ def _load():
         "flashnorm_glu_act": ([P, I64, I64, I64, I, P, I64, F, I, P, I64, I, P, I, P], I),
         "flashnorm_linear_relu": ([P, I64, I64, I64, I, P, I64, F, P, I64, I, P, I, P], I),
         "rowscale_linear": ([P, I64, I64, I64, I, P, I64, P, P, I64, I, I, P], I),
+        "flashnorm_linear_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P, I, P], I),
+        "flashnorm_glu_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, I64, I, I, P], I),
         "flashnorm_status_string": ([I], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -197,6 +199,29 @@ def rowscale_linear(x: torch.Tensor, W_packed: torch.Tensor, N: int, row_scale: 
                                    _ptr(_vec(row_scale, M, "row_scale")), _ptr(y), _ld(y), _dt(y), path,
                                    _stream(stream)), "rowscale_linear")
     return y
+
+
+def flashnorm_linear_unfolded(a: torch.Tensor, g: torch.Tensor, W_packed: torch.Tensor, N: int, eps: float,
+                              bias=None, out=None, inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    """Deferred RMSNorm -> linear with g applied at run time to an unfolded packed W."""
+    M, K = a.shape
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    _check(_load().flashnorm_linear_unfolded(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed),
+                                             N, eps, _ptr(_vec(bias, N, "bias")), _ptr(y), _ld(y), _dt(y),
+                                             _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
+           "flashnorm_linear_unfolded")
+    return y
+
+
+def flashnorm_glu_unfolded(a: torch.Tensor, g: torch.Tensor, W_packed_gu: torch.Tensor, F: int, eps: float,
+                           out=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    """Deferred RMSNorm -> SwiGLU with g applied at run time to an unfolded packed [Wg | Wu]."""
+    M, K = a.shape
+    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    _check(_load().flashnorm_glu_unfolded(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed_gu),
+                                          F, eps, _ptr(o), _ld(o), _dt(o), path, _stream(stream)),
+           "flashnorm_glu_unfolded")
+    return o
 
 
 def flashnorm_layernorm_linear(a: torch.Tensor, W_star: torch.Tensor, colsum: torch.Tensor, c_star, N: int,

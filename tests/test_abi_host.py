@@ -171,3 +171,20 @@ def test_epilogue_family_validation(fnlib):
     rs = lambda **kw: lib.rowscale_linear(A, 4, 64, 64, 1, W, 32, kw.get("s", X), Y, 32, kw.get("ydt", 1), 0, None)
     assert rs(s=0) == -1
     assert rs(ydt=0) == -3
+
+
+def test_unfolded_validation(fnlib):
+    lib = fnlib.lib()
+    lu = lambda **kw: lib.flashnorm_linear_unfolded(A, kw.get("M", 64), kw.get("K", 64), kw.get("K", 64), 1,
+                                                    kw.get("g", X), W, 32, 1e-6, None, Y, 32, 1, None,
+                                                    kw.get("path", 0), None)
+    assert lu(g=0) == -1                            # run-time g must be given
+    assert lu(g=X + 4) == -4
+    assert lu(g=Y) == -8                            # g overlaps the output
+    assert lu(path=1 | (2 << 8)) == -5              # forced tile: automatic configuration only
+    assert lu(K=8136) == -5                         # bf16 tile path stages g in LDS: K <= 8128
+    assert lu(M=0, g=0) == 0                        # M == 0: no-op
+    gu = lambda **kw: lib.flashnorm_glu_unfolded(A, kw.get("M", 64), 8200, 8200, 1, kw.get("g", X), W, 16, 1e-6,
+                                                 Y, 16, 1, kw.get("path", 0), None)
+    assert gu(g=0) == -1
+    assert gu(path=1) == -5

@@ -416,3 +416,66 @@ def test_deferred_ffn(fn, kind, dtype, M, K, F, N, path):
     torch.cuda.synchronize()
     ref = oracle.rmsnorm_ffn(w.a, w.g, w.W, Wd, w.eps, oact)
     assert row_err(to_np(y), ref) <= TOL[dtype]
+
+
+# ------------------------------------------- run-time g (unfolded weight)
+def _unfolded_linear(fn, w, path=0, bias=None):
+    a, W = w.a.to(DEV), w.W.to(DEV)
+    ws_dt = fn.FN_BF16 if w.dtype == torch.bfloat16 else fn.FN_F32
+    Wp, _, _ = fn.fold_weights(W, None, ws_dtype=ws_dt)
+    y = padded_out(w.M, w.N, w.dtype, align=8 if w.dtype == torch.bfloat16 else 4)
+    inv = torch.empty(w.M, dtype=torch.float32, device=DEV)
+    b = bias.to(DEV) if bias is not None else None
+    fn.flashnorm_linear_unfolded(a, w.g.to(DEV), Wp, w.N, w.eps, bias=b, out=y, inv_rms=inv, path=path)
+    torch.cuda.synchronize()
+    return y, inv
+
+
+@pytest.mark.parametrize("dtype,M,K,N,path", [(torch.bfloat16, 300, 328, 296, 1), (torch.bfloat16, 1, 1032, 72, 2),
+                                              (torch.bfloat16, 7, 1032, 200, 2), (torch.bfloat16, 16, 576, 48, 0),
+                                              (torch.bfloat16, 4, 8256, 40, 2), (torch.bfloat16, 70, 8128, 100, 1),
+                                              (torch.float32, 37, 96, 40, 0), (torch.float32, 5, 200, 72, 0)])
+def test_linear_unfolded(fn, dtype, M, K, N, path):
+    # Remark "Unfolded case": the same deferral with g applied at run time to an
+    # unfolded W; compared with the standard form RMSNorm(a) W (+ bias).
+    w = workloads.make("linear", M, K, N, dtype=dtype, eps=1e-5, seed=81 + M + K, outlier_frac=0.05)
+    bias = torch.randn(N, generator=torch.Generator().manual_seed(4))
+    y, inv = _unfolded_linear(fn, w, path=path, bias=bias)
+    assert row_err(to_np(y), oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps, bias=bias)) <= TOL[dtype]
+    want = np.array([1.0 / oracle.rms(r, w.eps) for r in w.a.double().numpy()])
+    np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
+
+
+def test_llama7b_qkv_unfolded_sampled(fn):
+    # The full QKV projection, in the tile the benchmark times for it.
+    w = workloads.llama7b_qkv_prefill()
+    y, _ = _unfolded_linear(fn, w)
+    rows = sample_rows(w.M, n=24)
+    err = row_err(to_np(y)[rows], oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps, rows=rows))
+    assert err <= TOL[torch.bfloat16], err
+
+
+@pytest.mark.parametrize("dtype,M,K,F,path", [(torch.bfloat16, 300, 328, 80, 1), (torch.bfloat16, 7, 1032, 72, 2),
+                                              (torch.bfloat16, 1, 4096, 48, 0), (torch.bfloat16, 520, 512, 136, 0),
+                                              (torch.float32, 37, 96, 40, 0)])
+def test_glu_unfolded(fn, dtype, M, K, F, path):
+    w = workloads.make("glu", M, K, F, dtype=dtype, eps=1e-6, seed=91 + M, outlier_frac=0.05)
+    ws_dt = fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32
+    Wp, _, _ = fn.fold_weights(w.W.to(DEV), None, layout=fn.FN_LAYOUT_GLU, ws_dtype=ws_dt)
+    out = fn.flashnorm_glu_unfolded(w.a.to(DEV), w.g.to(DEV), Wp, F, w.eps, path=path)
+    torch.cuda.synchronize()
+    assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("M,path", [(260, 1), (5, 2)])
+def test_unfolded_matches_folded_where_g_is_one(fn, M, path):
+    # With g = 1 both forms multiply the same bf16 values and take the squares in
+    # the same order: identical bits.
+    w = workloads.make("linear", M, 264, 136, eps=1e-6, seed=17)
+    a, W = w.a.to(DEV), w.W.to(DEV)
+    ones = torch.ones(w.K, dtype=torch.float32, device=DEV)
+    Wp, _, _ = fn.fold_weights(W, None)
+    yf = fn.flashnorm_linear(a, Wp, w.N, w.eps, path=path)
+    yu = fn.flashnorm_linear_unfolded(a, ones, Wp, w.N, w.eps, path=path)
+    torch.cuda.synchronize()
+    assert torch.equal(yf.view(torch.int16), yu.view(torch.int16))
