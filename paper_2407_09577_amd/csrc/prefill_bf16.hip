@@ -68,6 +68,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   static_assert(!GS || (PF && A_FRAGS % NW == 0 && (EPI == EPI_RMS || EPI == EPI_GLU) && STAGES >= 4),
                 "run-time g: prefetching ring, even split of row blocks, RMS kinds");
   constexpr int SPW = GS ? A_FRAGS / NW : 0;  // row blocks each wave scales
+  static_assert(SPW < NRD, "run-time g: one matrix-core group per scaled fragment after the first");
 
   // STAGES ring of k blocks, plus one slot that absorbs padding loads.
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE + (kUneven ? kFragBytes : 0)];
@@ -168,33 +169,48 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 
   // GS: scale the activation fragments of block b in place, g applied per k
   // (each product rounded once to bf16), and take the row squares from the raw
-  // values.  The lane reads the 16 bytes it transferred: row t_row of the row
-  // block, k chunk lk of the block (the transfer layout of the ring).
+  // values.  The lane handles the 16 bytes it transferred: row t_row of the row
+  // block, k chunk lk of the block (the transfer layout of the ring).  The LDS
+  // reads go out right after the barrier (scale_fetch) and the arithmetic and
+  // write-back run between the matrix-core groups of the block (scale_store),
+  // so the read latency and the VALU work overlap the matrix cores.
   float ss_own[SPW > 0 ? SPW : 1];
+  u32x4 sc_raw[SPW > 0 ? SPW : 1];
+  f32x4 sc_g0, sc_g1;
+  int sc_slot = 0;
 #pragma unroll
   for (int t = 0; t < (SPW > 0 ? SPW : 1); ++t) ss_own[t] = 0.f;
-  auto scale_block = [&](int b) __attribute__((always_inline)) {
+  auto scale_fetch = [&](int b) __attribute__((always_inline)) {
     if constexpr (GS) {
-      char* st = smem + (b % STAGES) * STAGE;
+      sc_slot = (b % STAGES) * STAGE;
       const float* gk = g_lds + b * kKB + lk;
-      const f32x4 g0 = *reinterpret_cast<const f32x4*>(gk);
-      const f32x4 g1 = *reinterpret_cast<const f32x4*>(gk + 4);
+      sc_g0 = *reinterpret_cast<const f32x4*>(gk);
+      sc_g1 = *reinterpret_cast<const f32x4*>(gk + 4);
 #pragma unroll
-      for (int t = 0; t < SPW; ++t) {
-        u32x4* p = reinterpret_cast<u32x4*>(st + (wave + NW * t) * kFragBytes + lane * 16);
-        const bf16x8 v = __builtin_bit_cast(bf16x8, *p);
-        ss_own[t] = sumsq8(v, ss_own[t]);
-        float o[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          o[e] = (float)v[e] * g0[e];
-          o[4 + e] = (float)v[4 + e] * g1[e];
-        }
-        const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
-        const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
-        *p = u32x4{lo[0], lo[1], hi[0], hi[1]};
-      }
+      for (int t = 0; t < SPW; ++t)
+        sc_raw[t] = *reinterpret_cast<const u32x4*>(smem + sc_slot + (wave + NW * t) * kFragBytes + lane * 16);
     }
+  };
+  auto scale_store = [&](int t) __attribute__((always_inline)) {
+    if constexpr (GS) {
+      const bf16x8 v = __builtin_bit_cast(bf16x8, sc_raw[t]);
+      ss_own[t] = sumsq8(v, ss_own[t]);
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[e] = (float)v[e] * sc_g0[e];
+        o[4 + e] = (float)v[4 + e] * sc_g1[e];
+      }
+      const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
+      const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
+      *reinterpret_cast<u32x4*>(smem + sc_slot + (wave + NW * t) * kFragBytes + lane * 16) =
+          u32x4{lo[0], lo[1], hi[0], hi[1]};
+    }
+  };
+  auto scale_block = [&](int b) __attribute__((always_inline)) {
+    scale_fetch(b);
+#pragma unroll
+    for (int t = 0; t < SPW; ++t) scale_store(t);
   };
 
   auto sync_block = [&]() __attribute__((always_inline)) {
@@ -213,7 +229,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // scheduling fences keep this interleaving, so memory traffic overlaps the
   // matrix cores.
   auto multiply_interleaved = [&](auto wnc, int kb, const bf16x8 (&afc)[FM], const bf16x8 (&wfc)[FN],
-                                  bf16x8 (&afn)[FM], bf16x8 (&wfn)[FN], bool more)
+                                  bf16x8 (&afn)[FM], bf16x8 (&wfn)[FN], bool more, bool scale = false)
                                   __attribute__((always_inline)) {
     constexpr int WNC = decltype(wnc)::value;
     if constexpr (!GS) {
@@ -227,6 +243,10 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       for (int t = g * NMF / NRD; t < (g + 1) * NMF / NRD; ++t) {
         const int i = t / FM, j = t % FM;
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wfc[i], afc[j], acc[i][j], 0, 0, 0);
+      }
+      // GS: fragment t of the block being scaled is finished in group t + 1.
+      if constexpr (GS) {
+        if (scale && g >= 1 && g - 1 < SPW) scale_store(g - 1);
       }
       // Transfer i goes out in group i * LSTEP: spread over the block (SPREAD),
       // so the workgroup's transfers reach the address unit at the rate it
@@ -282,12 +302,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       for (int kb = 0; kb < nkb - 2; kb += 2) {
         wait_vmcnt<kAheadWait>();
         sync_block();
-        scale_block(kb + 2);
-        multiply_interleaved(wnc, kb, af0, wf0, af1, wf1, true);
+        scale_fetch(kb + 2);
+        multiply_interleaved(wnc, kb, af0, wf0, af1, wf1, true, true);
         wait_vmcnt<kAheadWait>();
         sync_block();
-        scale_block(kb + 3);
-        multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true);
+        scale_fetch(kb + 3);
+        multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true, true);
       }
       wait_vmcnt<kAheadWait>();
       sync_block();
