@@ -4,8 +4,8 @@ A summary records, for one kernel and workload: the commands that produced it,
 the kernel's average duration from ``--kernel-trace --stats``, the FETCH_SIZE and
 WRITE_SIZE counters per dispatch (KiB) scaled by the factors a plain device copy
 of known size yields on the same machine, the matrix-core busy fraction, and a
-SHA-256 of the library's kernel sources.  bench.py reports the measured HBM
-traffic only while that hash still matches the sources.
+SHA-256 of the kernel's source file and the shared headers.  bench.py reports the
+measured HBM traffic only while that hash still matches the sources.
 
   python -m paper_2407_09577_amd.profiling --workload smollm2_prefill --kernel prefill_bf16_kernel \
       --trace DIR --fetch DIR --write DIR --mfma DIR --cal-fetch DIR --cal-write DIR --copy-bytes N \
@@ -25,12 +25,19 @@ ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def kernel_sources_sha256() -> str:
+def kernel_sources_sha256(kernel: str) -> str:
+    """SHA-256 over the source file that defines ``kernel`` (``fn::<name>_kernel`` lives in
+    ``csrc/<name>.hip``) and every shared header, i.e. everything its code is built from."""
+    m = re.search(r"(\w+)_kernel", kernel)
+    if not m:
+        raise ValueError(f"not a kernel name: {kernel}")
+    src = os.path.join(HERE, "csrc", m.group(1).split("::")[-1] + ".hip")
+    if not os.path.exists(src):
+        raise ValueError(f"no source {src} for {kernel}")
     h = hashlib.sha256()
-    for path in sorted(glob.glob(os.path.join(HERE, "csrc", "*"))):
-        if path.endswith((".hip", ".h")):
-            h.update(os.path.basename(path).encode())
-            h.update(open(path, "rb").read())
+    for path in [src] + sorted(glob.glob(os.path.join(HERE, "csrc", "*.h"))):
+        h.update(os.path.basename(path).encode())
+        h.update(open(path, "rb").read())
     return h.hexdigest()
 
 
@@ -83,7 +90,7 @@ def summarize(a) -> str:
         f"hbm_write_bytes_per_launch: {write_kib * 1024 * f_write:.0f}",
         f"traffic_bytes_per_launch: {traffic:.0f}",
         f"mfma_busy_fraction: {util:.4f}  (SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE/{a.xcds} x {a.simds} SIMDs))",
-        f"kernel_sources_sha256: {kernel_sources_sha256()}",
+        f"kernel_sources_sha256: {kernel_sources_sha256(a.kernel)}",
     ]
     return "\n".join(lines) + "\n"
 
@@ -97,7 +104,9 @@ def read_summary(workload: str):
             m = re.match(r"^([a-z_0-9]+):\s*(\S+)", line)
             if m:
                 kv[m.group(1)] = m.group(2)
-        if "traffic_bytes_per_launch" in kv and kv.get("kernel_sources_sha256") == kernel_sources_sha256():
+        m = re.search(r"^kernel: .*?fn::(\w+_kernel)", open(p).read(), flags=re.M)
+        if ("traffic_bytes_per_launch" in kv and m
+                and kv.get("kernel_sources_sha256") == kernel_sources_sha256(m.group(1))):
             kv["path"] = os.path.relpath(p, ROOT)
             return kv
     return None
