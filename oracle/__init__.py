@@ -197,6 +197,73 @@ def rmsnorm_ffn(a, g, Wup, Wdown, eps, act, rows=None) -> np.ndarray:
     return y
 
 
+def rope(x, h, pos, cos_tab, sin_tab) -> np.ndarray:
+    """Rotary position embedding of every h-wide head of each row of x (Sec. 4.2 with the
+    rotation of the RoPE paper): row i is a token at position pos[i]; within each head the
+    consecutive pairs (x_2j, x_2j+1) turn by the angle whose cosine and sine are
+    cos_tab[pos[i], j] and sin_tab[pos[i], j]:
+        y_2j = x_2j cos - x_2j+1 sin,   y_2j+1 = x_2j sin + x_2j+1 cos.
+    A row whose position lies outside the table is NaN."""
+    x, c_tab, s_tab = _f64(x), _f64(cos_tab), _f64(sin_tab)
+    M, N = x.shape
+    if h % 2 or N % h or c_tab.shape != s_tab.shape or c_tab.shape[1] != h // 2:
+        raise ValueError("shape mismatch")
+    pos = np.asarray(pos).ravel()
+    out = np.empty_like(x)
+    for i in range(M):
+        p = int(pos[i])
+        if not 0 <= p < c_tab.shape[0]:
+            out[i] = np.nan
+            continue
+        pairs = x[i].reshape(N // h, h // 2, 2)  # [head, j, (even, odd)]
+        c, s = c_tab[p], s_tab[p]
+        out[i, 0::2] = (pairs[:, :, 0] * c - pairs[:, :, 1] * s).ravel()
+        out[i, 1::2] = (pairs[:, :, 0] * s + pairs[:, :, 1] * c).ravel()
+    return out
+
+
+def rmsnorm_qkv_rope(a, g, W, eps, Hq, Hkv, h, pos, cos_tab, sin_tab, q_scale, bias=None,
+                     rows=None) -> np.ndarray:
+    """Standard form of Fig. 5(a): x = RMSNorm(a; g), t = x W (+ c), W = [Wq | Wk | Wv] with Hq
+    query heads and Hkv key/value heads of width h; Q and K heads rotated by RoPE at each
+    row's position, Q also multiplied by q_scale (the 1/sqrt(h) of the attention scores).
+    V is t itself."""
+    qk = (Hq + Hkv) * h
+    if _f64(W).shape[1] != (Hq + 2 * Hkv) * h:
+        raise ValueError("W must have (Hq + 2 Hkv) h columns")
+    t = rmsnorm_linear(a, g, W, eps, bias=bias, rows=rows)
+    p = np.asarray(pos).ravel()
+    if rows is not None:
+        p = p[np.asarray(rows, dtype=np.int64)]
+    out = t.copy()
+    out[:, :qk] = rope(t[:, :qk], h, p, cos_tab, sin_tab)
+    out[:, :Hq * h] *= float(np.float32(q_scale))
+    return out
+
+
+def qkv_rope_deferred(a, g, W, eps, Hq, Hkv, h, pos, cos_tab, sin_tab, q_scale, rows=None) -> np.ndarray:
+    """Deferred form of Fig. 5(b): z = a W* with W* = diag(g) W, then RoPE with per-token tables
+    cos/RMSe(a) and sin/RMSe(a) (times q_scale for Q); V is z / RMSe(a). Self-check."""
+    a, g, W = _f64(a), _f64(g), _f64(W)
+    r, nr = _rows(rows, a.shape[0])
+    if r is None:
+        r = np.arange(nr)
+    a = a[r]
+    p = np.asarray(pos).ravel()[r]
+    qk = (Hq + Hkv) * h
+    z = a @ (g[:, None] * W)
+    s = np.array([1.0 / rms(row, _eps(eps)) for row in a])
+    c_tab, s_tab = _f64(cos_tab), _f64(sin_tab)
+    valid = (p >= 0) & (p < c_tab.shape[0])
+    pc = np.where(valid, p, 0)
+    c_rows = np.where(valid[:, None], c_tab[pc] * s[:, None], np.nan)  # per-token tables
+    s_rows = np.where(valid[:, None], s_tab[pc] * s[:, None], np.nan)
+    out = z * s[:, None]
+    out[:, :qk] = rope(z[:, :qk], h, np.arange(nr), c_rows, s_rows)
+    out[:, :Hq * h] *= float(np.float32(q_scale))
+    return out
+
+
 def _ln_like(fn, a, g, beta, W, eps, bias, rows):
     a, g, beta, W, bias = _f64(a), _f64(g), _f64(beta), _f64(W), _f64(bias)
     M, K = a.shape

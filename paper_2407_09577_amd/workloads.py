@@ -67,6 +67,21 @@ def weight(K: int, N: int, *, dtype=torch.bfloat16, seed: int = 0) -> torch.Tens
     return (torch.randn(K, N, generator=gen, dtype=torch.float32) * K ** -0.5).to(dtype)
 
 
+def rope_tables(P: int, h: int, base: float = 10000.0):
+    """Precomputed RoPE inputs shared by every head: cos and sin of p * base^(-2j/h) for
+    positions p < P and pairs j < h/2, evaluated in fp64 and cast once to fp32 ([P, h/2] each).
+    These are the caller's tables, inputs of the fused op like the weights."""
+    p = torch.arange(P, dtype=torch.float64)[:, None]
+    j = torch.arange(h // 2, dtype=torch.float64)[None, :]
+    ang = p * base ** (-2.0 * j / h)
+    return torch.cos(ang).to(torch.float32), torch.sin(ang).to(torch.float32)
+
+
+def positions(M: int, seq_len: int) -> torch.Tensor:
+    """Token positions of M rows packed as sequences of seq_len tokens: m % seq_len (int32)."""
+    return (torch.arange(M, dtype=torch.int64) % seq_len).to(torch.int32)
+
+
 def make(kind: str, M: int, K: int, N: int, *, dtype=torch.bfloat16, eps: float = 1e-6,
          seed: int = 0, a_mean: float = 0.0, outlier_frac: float = 0.0,
          outlier_scale: float = 20.0, name: str = "") -> Workload:

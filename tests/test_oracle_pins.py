@@ -465,3 +465,95 @@ def test_relu_and_bilinear_ffn_scale_invariance():
     for c in (-3.0, 0.25):
         assert _rel(oracle.rmsnorm_ffn(c * a, g, Wgu, Wd, 0.0, oracle.GLU_BILINEAR),
                     oracle.rmsnorm_ffn(a, g, Wgu, Wd, 0.0, oracle.GLU_BILINEAR)) < 1e-13
+
+
+# ---------------------------------------------------------------- RoPE after the QKV projection (Fig. 5)
+def test_qkv_rope_exact_worked_example():
+    fx = _read_fixture("qkv_rope_worked_example.txt")
+    h, Hq, Hkv = int(fx["h"][0][0]), int(fx["Hq"][0][0]), int(fx["Hkv"][0][0])
+    qs = float(_frac(fx["q_scale"][0][0]))
+    a = np.array([[float(_frac(v)) for v in fx["a"][0]]])
+    g = np.array([float(_frac(v)) for v in fx["g"][0]])
+    W = np.array([[float(_frac(v)) for v in r] for r in fx["W"]])
+    cos = np.array([[float(_frac(v)) for v in r] for r in fx["cos"]])
+    sin = np.array([[float(_frac(v)) for v in r] for r in fx["sin"]])
+    c = np.array([float(_frac(v)) for v in fx["c"][0]])
+    for eps_s, pos_s, bias_s, *vals in fx["case"]:
+        eps, pos, with_bias = float(_frac(eps_s)), np.array([int(pos_s)]), bias_s == "1"
+        want = np.array([float(_frac(v)) for v in vals])
+        got = oracle.rmsnorm_qkv_rope(a, g, W, eps, Hq, Hkv, h, pos, cos, sin, qs, bias=c if with_bias else None)
+        np.testing.assert_allclose(got[0], want, rtol=1e-14, atol=1e-14)
+        if not with_bias:
+            got = oracle.qkv_rope_deferred(a, g, W, eps, Hq, Hkv, h, pos, cos, sin, qs)
+            np.testing.assert_allclose(got[0], want, rtol=1e-14, atol=1e-14)
+
+
+def _complex_rope(x, h, pos, cos, sin):
+    # The same rotation written as complex multiplication: z_j = x_2j + i x_2j+1 of each head
+    # times exp(i theta) = cos + i sin of the token's position.
+    M, N = x.shape
+    z = x.reshape(M, N // h, h // 2, 2)
+    z = z[..., 0] + 1j * z[..., 1]
+    rot = (cos[pos] + 1j * sin[pos])[:, None, :]
+    w = z * rot
+    return np.stack([w.real, w.imag], axis=-1).reshape(M, N)
+
+
+@pytest.mark.parametrize("h,heads,P,seed", [(8, 3, 17, 0), (64, 2, 300, 1), (128, 5, 40, 2)])
+def test_rope_matches_complex_rotation(h, heads, P, seed):
+    rng = np.random.default_rng(seed)
+    cos, sin = (t.double().numpy() for t in workloads.rope_tables(P, h))
+    x = rng.standard_normal((6, heads * h))
+    pos = rng.integers(0, P, 6)
+    np.testing.assert_allclose(oracle.rope(x, h, pos, cos, sin), _complex_rope(x, h, pos, cos, sin),
+                               rtol=1e-13, atol=1e-13)
+
+
+def test_rope_relative_position_and_norm():
+    # RoPE's defining property: the score between a query at m and a key at n depends only
+    # on m - n; each pair keeps its length; position 0 is the identity.
+    h, P = 16, 64
+    cos, sin = (t.double().numpy() for t in workloads.rope_tables(P, h))
+    rng = np.random.default_rng(5)
+    q, k = rng.standard_normal((1, h)), rng.standard_normal((1, h))
+    rq = lambda m: oracle.rope(q, h, [m], cos, sin)[0]
+    rk = lambda n: oracle.rope(k, h, [n], cos, sin)[0]
+    for m, n, d in [(9, 3, 20), (0, 5, 7), (30, 30, 11)]:
+        assert abs(rq(m) @ rk(n) - rq(m + d) @ rk(n + d)) < 1e-5 * np.linalg.norm(q) * np.linalg.norm(k)
+    y = oracle.rope(q, h, [13], cos, sin)[0]
+    np.testing.assert_allclose(np.hypot(y[0::2], y[1::2]), np.hypot(q[0, 0::2], q[0, 1::2]), rtol=1e-6)
+    np.testing.assert_array_equal(oracle.rope(q, h, [0], cos, sin), q)
+
+
+@pytest.mark.parametrize("M,K,Hq,Hkv,h,eps,seed", [(5, 32, 4, 2, 8, 1e-6, 0), (3, 96, 2, 2, 16, 0.5, 1),
+                                                   (4, 64, 3, 1, 4, 0.0, 2)])
+def test_qkv_rope_deferred_equals_standard_and_torch(M, K, Hq, Hkv, h, eps, seed):
+    # Fig. 5(b) = Fig. 5(a) (Prop. 2 with RoPE linear per token), and the standard form
+    # rebuilt from torch's rms_norm, a matmul and complex rotation.
+    N = (Hq + 2 * Hkv) * h
+    a, g, W = _rand_case(M, K, N, seed, neg_g=True)
+    P = 50
+    cos, sin = (t.double().numpy() for t in workloads.rope_tables(P, h))
+    pos = np.random.default_rng(seed).integers(0, P, M)
+    qs = 1.0 / math.sqrt(h)
+    std = oracle.rmsnorm_qkv_rope(a, g, W, eps, Hq, Hkv, h, pos, cos, sin, qs)
+    np.testing.assert_allclose(oracle.qkv_rope_deferred(a, g, W, eps, Hq, Hkv, h, pos, cos, sin, qs), std,
+                               rtol=1e-12, atol=1e-13)
+    x = F.rms_norm(torch.from_numpy(a), (K,), weight=torch.from_numpy(g), eps=float(np.float32(eps)))
+    t = (x @ torch.from_numpy(W)).numpy()
+    qk = (Hq + Hkv) * h
+    ref = t.copy()
+    ref[:, :qk] = _complex_rope(t[:, :qk], h, pos, cos, sin)
+    ref[:, :Hq * h] *= float(np.float32(qs))
+    np.testing.assert_allclose(std, ref, rtol=1e-12, atol=1e-13)
+    sub = oracle.rmsnorm_qkv_rope(a, g, W, eps, Hq, Hkv, h, pos, cos, sin, qs, rows=[M - 1, 0])
+    np.testing.assert_allclose(sub, std[[M - 1, 0]], rtol=0, atol=0)
+
+
+def test_qkv_rope_position_outside_table_is_nan_in_q_and_k_only():
+    a, g, W = _rand_case(3, 16, (2 + 2) * 4, 9)
+    cos, sin = (t.double().numpy() for t in workloads.rope_tables(8, 4))
+    y = oracle.rmsnorm_qkv_rope(a, g, W, 1e-6, 2, 1, 4, np.array([1, 8, -1]), cos, sin, 0.5)
+    assert np.isfinite(y[0]).all()
+    for r in (1, 2):
+        assert np.isnan(y[r, :12]).all() and np.isfinite(y[r, 12:]).all()
