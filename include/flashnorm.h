@@ -216,6 +216,32 @@ int rowscale_linear(const void* x, int64_t M, int64_t K, int64_t ldx, int x_dtyp
                     const void* W_packed, int64_t N, const float* row_scale, void* y,
                     int64_t ldy, int y_dtype, int path, void* stream);
 
+/* RMSNorm -> fused QKV projection -> RoPE (Sec. 4.2, Fig. 5).  W_star_qkv is
+ * [Wq | Wk | Wv] folded with g (FN_LAYOUT_LINEAR, N = (Hq + 2 Hkv) h columns: Hq
+ * query heads, then Hkv key heads, then Hkv value heads, each h wide).  Row m is a
+ * token at position positions[m].  With t = (a W*) s_m (+ bias, added before the
+ * rotation), s_m = 1/RMSe(a_m):
+ *   Q and K heads:  y_2j = t_2j cos - t_2j+1 sin,  y_2j+1 = t_2j sin + t_2j+1 cos,
+ *                   cos = cos_tab[positions[m]][j], sin = sin_tab[positions[m]][j],
+ *                   j the pair index within the head (consecutive pairs, as in the
+ *                   RoPE paper); Q also times q_scale (e.g. 1/sqrt(h), the
+ *                   attention-score scale folded into the same multiply);
+ *   V heads:        y = t.
+ * Without a bias the kernels fold s_m (and q_scale) into the token's table values,
+ * cos*s and sin*s, as in Fig. 5(b).
+ *   positions  [M] int32, 16-byte aligned.  A position outside [0, P) makes that
+ *              row's Q and K outputs NaN (V is still written).
+ *   cos_tab, sin_tab  [P][h/2] fp32 row-major, 16-byte aligned, shared by all heads.
+ *   h          a multiple of 4 (FN_ERR_SHAPE otherwise); Hq >= 1, Hkv >= 0.
+ *   bias       optional [N] fp32, 16-byte aligned.  inv_rms optional [M] output of s.
+ *   path       as for flashnorm_glu_act (automatic configuration only).
+ * The output may not overlap the tables or positions (FN_ERR_ALIAS). */
+int flashnorm_qkv_rope(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                       const void* W_star_qkv, int64_t Hq, int64_t Hkv, int64_t h, float eps,
+                       const float* bias, const int32_t* positions, const float* cos_tab,
+                       const float* sin_tab, int64_t P, float q_scale, void* y, int64_t ldy,
+                       int y_dtype, float* inv_rms, int path, void* stream);
+
 /* Deferred normalisation with the UNFOLDED weight (Remark "Unfolded case": the
  * deferral of Prop. 2 needs only that 1/RMS is a per-token scalar, so it serves a
  * checkpoint as it is, with g applied at run time instead of folded into W):

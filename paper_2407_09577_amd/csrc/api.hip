@@ -280,6 +280,41 @@ int rowscale_linear(const void* x, int64_t M, int64_t K, int64_t ldx, int x_dtyp
   return run_op(d);
 }
 
+// Fused QKV projection with RoPE on Q and K (Sec. 4.2, Fig. 5(b)).
+int flashnorm_qkv_rope(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star_qkv,
+                       int64_t Hq, int64_t Hkv, int64_t h, float eps, const float* bias, const int32_t* positions,
+                       const float* cos_tab, const float* sin_tab, int64_t P, float q_scale, void* y, int64_t ldy,
+                       int y_dtype, float* inv_rms, int path, void* stream) {
+  if (Hq < 1 || Hkv < 0 || h < 4 || h % 4 || P < 1) return FN_ERR_SHAPE;
+  if (Hq > kMaxRows || Hkv > kMaxRows || h > kMaxRows) return FN_ERR_SHAPE;
+  if (P > INT32_MAX / h) return FN_ERR_SIZE;
+  if (!isfinite(q_scale)) return FN_ERR_VALUE;
+  const int64_t N = (Hq + 2 * Hkv) * h;
+  OpDesc d{a, M, K, lda, a_dtype, W_star_qkv, N, 0, y, ldy, fn::EPI_ROPE, make_ep(eps, K), path,
+           (hipStream_t)stream};
+  d.ep.bias = bias;
+  d.ep.inv_rms = inv_rms;
+  d.ep.rope_pos = positions;
+  d.ep.rope_cos = cos_tab;
+  d.ep.rope_sin = sin_tab;
+  d.ep.rope_h = (int)h;
+  d.ep.rope_P = (int)P;
+  d.ep.rope_q_end = (int)(Hq * h);
+  d.ep.rope_k_end = (int)((Hq + Hkv) * h);
+  d.ep.rope_q_scale = q_scale;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  if ((s = check_auto_config(path))) return s;
+  if (M == 0) return FN_OK;
+  if (!positions || !cos_tab || !sin_tab) return FN_ERR_NULL;
+  if (!aligned16(bias) || !aligned16(cos_tab) || !aligned16(sin_tab) || !aligned16(positions)) return FN_ERR_ALIGN;
+  const int64_t ybytes = extent_bytes(M, N, ldy, a_dtype), tbytes = P * (h / 2) * (int64_t)sizeof(float);
+  if (overlaps(y, ybytes, cos_tab, tbytes) || overlaps(y, ybytes, sin_tab, tbytes) ||
+      overlaps(y, ybytes, positions, M * (int64_t)sizeof(int32_t)))
+    return FN_ERR_ALIAS;
+  return run_op(d);
+}
+
 // Run-time g (unfolded W): g must be given, 16-byte aligned; the bf16 tile path
 // stages g in LDS and takes K <= fn::kGsMaxK.
 static int check_runtime_g(const OpDesc& d, const float* g) {

@@ -259,6 +259,7 @@ hipError_t launch_decode_bf16(const DecodeArgs& p) {
     case EPI_GLU_DEFER: return launch_decode_epi<EPI_GLU_DEFER>(p);
     case EPI_RELU_DEFER: return launch_decode_epi<EPI_RELU_DEFER>(p);
     case EPI_ROWSCALE: return launch_decode_epi<EPI_ROWSCALE>(p);
+    case EPI_ROPE: return launch_decode_epi<EPI_ROPE>(p);
   }
   return hipErrorInvalidValue;
 }

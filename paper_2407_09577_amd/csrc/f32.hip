@@ -85,31 +85,57 @@ __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, i
   }
   __syncthreads();
 
+  if constexpr (EPI == EPI_ROPE) {
+    // Pair partners (column c ^ 1) sit in the neighbouring lane (tx ^ 1, same rows);
+    // every lane takes part in the exchange before any guard.
+    float part[4][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = ty + 16 * i;
-    const int m = m0 + r;
-    if (m >= M) continue;
-    const RowStat st = row_stat_at<EPI>(row_ss[r], row_sa[r], ep, m, M);
-    if constexpr (epi_exports_s(EPI)) {
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) part[i][j] = __shfl_xor(acc[i][j], 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = ty + 16 * i;
+      const int m = m0 + r;
+      if (m >= M) continue;
+      const RowStat st = row_stat_at<EPI>(row_ss[r], row_sa[r], ep, m, M);
       if (ep.inv_rms && blockIdx.x == 0 && tx == 0) ep.inv_rms[m] = st.s;
-    }
-    float* yr = y + (int64_t)m * ldy;
-    if constexpr (epi_is_glu(EPI)) {
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const int f = p0 / 2 + 16 * q + tx;
-        if (f < ncols) yr[f] = epi_value<EPI>(acc[i][2 * q], acc[i][2 * q + 1], st, 0.f, 0.f);
-      }
-    } else {
-      const float* vp = epi_vec<EPI>(ep);
+      float* yr = y + (int64_t)m * ldy;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int c = p0 + tx + 16 * j;
         if (c >= ncols) continue;
-        const float vec = vp ? vp[c] : 0.f;
-        const float cs = EPI == EPI_LN ? ep.colsum[c] : 0.f;
-        yr[c] = epi_value<EPI>(acc[i][j], acc[i][j], st, vec, cs);
+        const float bv = ep.bias ? ep.bias[c] : 0.f, bw = ep.bias ? ep.bias[c ^ 1] : 0.f;
+        yr[c] = rope1(c, acc[i][j], part[i][j], bv, bw, st, ep);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = ty + 16 * i;
+      const int m = m0 + r;
+      if (m >= M) continue;
+      const RowStat st = row_stat_at<EPI>(row_ss[r], row_sa[r], ep, m, M);
+      if constexpr (epi_exports_s(EPI)) {
+        if (ep.inv_rms && blockIdx.x == 0 && tx == 0) ep.inv_rms[m] = st.s;
+      }
+      float* yr = y + (int64_t)m * ldy;
+      if constexpr (epi_is_glu(EPI)) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int f = p0 / 2 + 16 * q + tx;
+          if (f < ncols) yr[f] = epi_value<EPI>(acc[i][2 * q], acc[i][2 * q + 1], st, 0.f, 0.f);
+        }
+      } else {
+        const float* vp = epi_vec<EPI>(ep);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = p0 + tx + 16 * j;
+          if (c >= ncols) continue;
+          const float vec = vp ? vp[c] : 0.f;
+          const float cs = EPI == EPI_LN ? ep.colsum[c] : 0.f;
+          yr[c] = epi_value<EPI>(acc[i][j], acc[i][j], st, vec, cs);
+        }
       }
     }
   }
@@ -140,6 +166,7 @@ hipError_t launch_f32(const F32Args& p) {
     case EPI_GLU_DEFER: return launch_f32_epi<EPI_GLU_DEFER>(p);
     case EPI_RELU_DEFER: return launch_f32_epi<EPI_RELU_DEFER>(p);
     case EPI_ROWSCALE: return launch_f32_epi<EPI_ROWSCALE>(p);
+    case EPI_ROPE: return launch_f32_epi<EPI_ROPE>(p);
   }
   return hipErrorInvalidValue;
 }

@@ -26,6 +26,7 @@ namespace fn {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
 
@@ -174,6 +175,7 @@ enum Epi : int {
   EPI_GLU_DEFER = 7,    // out = silu(s * gate) * up, s exported        (Fig. 3(b))
   EPI_RELU_DEFER = 8,   // y = relu(acc), s exported                    (Fig. 2(b))
   EPI_ROWSCALE = 9,     // y = acc * row_scale[m]   (applies a deferred scale)
+  EPI_ROPE = 10,        // fused QKV: RoPE on Q and K with s folded into the tables (Fig. 5(b))
 };
 
 constexpr bool epi_is_glu(int e) {
@@ -181,11 +183,11 @@ constexpr bool epi_is_glu(int e) {
 }
 constexpr bool epi_needs_ss(int e) {
   return e == EPI_RMS || e == EPI_GLU || e == EPI_LN || e == EPI_REGLU || e == EPI_BILINEAR ||
-         e == EPI_GLU_DEFER || e == EPI_RELU_DEFER;
+         e == EPI_GLU_DEFER || e == EPI_RELU_DEFER || e == EPI_ROPE;
 }
 // Kinds whose per-row scale s = 1/RMSe(a) can be written to the inv_rms output.
 constexpr bool epi_exports_s(int e) {
-  return e == EPI_RMS || e == EPI_GLU || e == EPI_GLU_DEFER || e == EPI_RELU_DEFER;
+  return e == EPI_RMS || e == EPI_GLU || e == EPI_GLU_DEFER || e == EPI_RELU_DEFER || e == EPI_ROPE;
 }
 
 struct EpiArgs {
@@ -197,6 +199,14 @@ struct EpiArgs {
   float* inv_rms;       // optional [M] output of s (kinds with epi_exports_s)
   const float* row_scale;  // EPI_ROWSCALE: [M]
   const float* g_rt;       // run-time normalisation weight [K] (unfolded W), or nullptr
+  // EPI_ROPE: output columns [0, q_end) are Q heads, [q_end, k_end) K heads, the rest V;
+  // heads are rope_h wide; row m is a token at position rope_pos[m], whose angles are
+  // rope_cos / rope_sin [rope_P][rope_h / 2]; Q is also multiplied by rope_q_scale.
+  const int* rope_pos;
+  const float* rope_cos;
+  const float* rope_sin;
+  int rope_h, rope_P, rope_q_end, rope_k_end;
+  float rope_q_scale;
 };
 
 }  // namespace fn

@@ -16,12 +16,14 @@ struct RowStat {
   float s;   // 1/RMSe(a) (RMSNorm kinds), 1/MSe(a) (ReGLU, bilinear), 1/sigma (LayerNorm),
              // the given row scale (EPI_ROWSCALE); 1 for the baselines
   float mu;  // LayerNorm mean (0 otherwise)
+  int pos;   // EPI_ROPE: the token's position (0 otherwise)
 };
 
 template <int EPI>
 __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& ep) {
-  RowStat st{1.0f, 0.0f};
-  if constexpr (EPI == EPI_RMS || EPI == EPI_GLU || EPI == EPI_GLU_DEFER || EPI == EPI_RELU_DEFER) {
+  RowStat st{1.0f, 0.0f, 0};
+  if constexpr (EPI == EPI_RMS || EPI == EPI_GLU || EPI == EPI_GLU_DEFER || EPI == EPI_RELU_DEFER ||
+                EPI == EPI_ROPE) {
     // RMSe(a) = sqrt(eps + ss/K)  (App. "RMS with epsilon")
     st.s = rsqrtf(fmaf(ss, ep.inv_k, ep.eps));
   } else if constexpr (EPI == EPI_REGLU || EPI == EPI_BILINEAR) {
@@ -46,12 +48,12 @@ template <int EPI>
 __device__ __forceinline__ RowStat row_stat_at(float ss, float sa, const EpiArgs& ep, int m, int M) {
   RowStat st = row_stat<EPI>(ss, sa, ep);
   if constexpr (EPI == EPI_ROWSCALE) st.s = m < M ? ep.row_scale[m] : 0.0f;
+  if constexpr (EPI == EPI_ROPE) st.pos = m < M ? ep.rope_pos[m] : 0;
   return st;
 }
 
 // Four fp32 values -> four bf16 (hardware round to nearest even), as 8 bytes.
 __device__ __forceinline__ u32x2 pack4_bf16(const float (&o)[4]) {
-  typedef __attribute__((ext_vector_type(2))) float f32x2;
   const bf16x2 lo = __builtin_convertvector((f32x2{o[0], o[1]}), bf16x2);
   const bf16x2 hi = __builtin_convertvector((f32x2{o[2], o[3]}), bf16x2);
   return u32x2{__builtin_bit_cast(unsigned, lo), __builtin_bit_cast(unsigned, hi)};
@@ -61,6 +63,7 @@ __device__ __forceinline__ u32x2 pack4_bf16(const float (&o)[4]) {
 // bias, added after the scaling; LN: c*), 0 when absent; cs: colsum (LN).
 template <int EPI>
 __device__ __forceinline__ float epi_value(float v, float u, RowStat st, float vec, float cs) {
+  static_assert(EPI != EPI_ROPE, "RoPE outputs come in pairs: rope4 / rope1");
   if constexpr (EPI == EPI_RMS) return fmaf(v, st.s, vec);
   else if constexpr (EPI == EPI_GLU) return silu(v * st.s) * (u * st.s);
   else if constexpr (EPI == EPI_LN) return fmaf(fmaf(-st.mu, cs, v), st.s, vec);
@@ -76,21 +79,86 @@ __device__ __forceinline__ float epi_value(float v, float u, RowStat st, float v
 // The optional per-column vector of an epilogue (bias or c*), or nullptr.
 template <int EPI>
 __device__ __forceinline__ const float* epi_vec(const EpiArgs& ep) {
-  if constexpr (EPI == EPI_RMS) return ep.bias;
+  if constexpr (EPI == EPI_RMS || EPI == EPI_ROPE) return ep.bias;
   else if constexpr (EPI == EPI_LN) return ep.cstar;
   else return nullptr;
 }
 
+// RoPE after the fused QKV projection (Sec. 4.2, Fig. 5): the four columns n .. n+3
+// of one row (n % 4 == 0; heads are a multiple of 4 wide, so these are two whole
+// pairs of one head).  Q and K pairs turn by the token's angles; without a bias the
+// token's scale s (times the score scale for Q) is folded into the table values,
+// cos*s and sin*s, as in Fig. 5(b), so the per-head scaling disappears.  A bias is
+// added before the rotation (t = acc*s + c).  V columns take the scale only.  A
+// position outside the table makes the Q and K values NaN.
+template <bool VEC>
+__device__ __forceinline__ void rope4(int n, f32x4 v, f32x4 vec, RowStat st, const EpiArgs& ep, float (&o)[4]) {
+  if (n >= ep.rope_k_end) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o[r] = fmaf(v[r], st.s, vec[r]);
+    return;
+  }
+  const float qs = n < ep.rope_q_end ? ep.rope_q_scale : 1.0f;
+  const int j = (n % ep.rope_h) >> 1;  // pair index of column n (even)
+  float c0 = __builtin_nanf(""), s0 = c0, c1 = c0, s1 = c0;
+  if ((unsigned)st.pos < (unsigned)ep.rope_P) {
+    const int64_t off = (int64_t)st.pos * (ep.rope_h >> 1) + j;
+    const f32x2 c = *reinterpret_cast<const f32x2*>(ep.rope_cos + off);
+    const f32x2 sn = *reinterpret_cast<const f32x2*>(ep.rope_sin + off);
+    c0 = c[0], c1 = c[1], s0 = sn[0], s1 = sn[1];
+  }
+  if constexpr (VEC) {
+    float t[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) t[r] = fmaf(v[r], st.s, vec[r]);
+    o[0] = (t[0] * c0 - t[1] * s0) * qs;
+    o[1] = (t[0] * s0 + t[1] * c0) * qs;
+    o[2] = (t[2] * c1 - t[3] * s1) * qs;
+    o[3] = (t[2] * s1 + t[3] * c1) * qs;
+  } else {
+    const float f = st.s * qs;
+    c0 *= f, s0 *= f, c1 *= f, s1 *= f;
+    o[0] = v[0] * c0 - v[1] * s0;
+    o[1] = v[0] * s0 + v[1] * c0;
+    o[2] = v[2] * c1 - v[3] * s1;
+    o[3] = v[2] * s1 + v[3] * c1;
+  }
+}
+
+// One output of EPI_ROPE at column c from its own accumulator v and that of its
+// pair partner w (column c ^ 1), with the per-column bias of each (0 without).
+__device__ __forceinline__ float rope1(int c, float v, float w, float bv, float bw, RowStat st, const EpiArgs& ep) {
+  const float tv = fmaf(v, st.s, bv);
+  if (c >= ep.rope_k_end) return tv;
+  if ((unsigned)st.pos >= (unsigned)ep.rope_P) return __builtin_nanf("");
+  const float tw = fmaf(w, st.s, bw);
+  const float qs = c < ep.rope_q_end ? ep.rope_q_scale : 1.0f;
+  const int64_t off = (int64_t)st.pos * (ep.rope_h >> 1) + ((c % ep.rope_h) >> 1);
+  const float cs = ep.rope_cos[off], sn = ep.rope_sin[off];
+  return ((c & 1) ? tw * sn + tv * cs : tv * cs - tw * sn) * qs;
+}
+
 // The 4 outputs of one lane (logical columns n .. n+3, n % 4 == 0, all inside
-// the output) as bf16: 16-byte vector loads of the per-column vectors.
+// the output) in fp32: 16-byte vector loads of the per-column vectors.
 template <int EPI, bool VEC>
-__device__ __forceinline__ u32x2 epi4_bf16(int n, f32x4 v, f32x4 u, RowStat st, const EpiArgs& ep) {
+__device__ __forceinline__ void epi4_values(int n, f32x4 v, f32x4 u, RowStat st, const EpiArgs& ep,
+                                            float (&o)[4]) {
   f32x4 vec = {0.f, 0.f, 0.f, 0.f}, cs = {0.f, 0.f, 0.f, 0.f};
   if constexpr (VEC) vec = *reinterpret_cast<const f32x4*>(epi_vec<EPI>(ep) + n);
   if constexpr (EPI == EPI_LN) cs = *reinterpret_cast<const f32x4*>(ep.colsum + n);
-  float o[4];
+  if constexpr (EPI == EPI_ROPE) {
+    rope4<VEC>(n, v, vec, st, ep, o);
+  } else {
 #pragma unroll
-  for (int r = 0; r < 4; ++r) o[r] = epi_value<EPI>(v[r], u[r], st, vec[r], cs[r]);
+    for (int r = 0; r < 4; ++r) o[r] = epi_value<EPI>(v[r], u[r], st, vec[r], cs[r]);
+  }
+}
+
+// The same as bf16, 8 bytes.
+template <int EPI, bool VEC>
+__device__ __forceinline__ u32x2 epi4_bf16(int n, f32x4 v, f32x4 u, RowStat st, const EpiArgs& ep) {
+  float o[4];
+  epi4_values<EPI, VEC>(n, v, u, st, ep, o);
   return pack4_bf16(o);
 }
 
@@ -144,15 +212,25 @@ __device__ __forceinline__ void store4_bf16_edge(__bf16* __restrict__ y, int64_t
                                                  int m, int n, f32x4 v, f32x4 u, RowStat st,
                                                  const EpiArgs& ep) {
   if (m >= M) return;
-  const float* vp = epi_vec<EPI>(ep);
   unsigned short* dst = reinterpret_cast<unsigned short*>(y + (int64_t)m * ldy + n);
+  if constexpr (EPI == EPI_ROPE) {
+    // the output width is a multiple of the head width: the 4 columns lie wholly
+    // inside or wholly outside
+    if (n >= ncols) return;
+    float o[4];
+    epi4_values<EPI, VEC>(n, v, u, st, ep, o);
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int c = n + r;
-    if (c < ncols) {
-      const float vec = VEC ? vp[c] : 0.f;
-      const float cs = EPI == EPI_LN ? ep.colsum[c] : 0.f;
-      dst[r] = __builtin_bit_cast(unsigned short, (__bf16)epi_value<EPI>(v[r], u[r], st, vec, cs));
+    for (int r = 0; r < 4; ++r) dst[r] = __builtin_bit_cast(unsigned short, (__bf16)o[r]);
+  } else {
+    const float* vp = epi_vec<EPI>(ep);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int c = n + r;
+      if (c < ncols) {
+        const float vec = VEC ? vp[c] : 0.f;
+        const float cs = EPI == EPI_LN ? ep.colsum[c] : 0.f;
+        dst[r] = __builtin_bit_cast(unsigned short, (__bf16)epi_value<EPI>(v[r], u[r], st, vec, cs));
+      }
     }
   }
 }

@@ -589,6 +589,7 @@ hipError_t launch_prefill_bf16(const PrefillArgs& p) {
     case EPI_GLU_DEFER: return launch_prefill_epi<EPI_GLU_DEFER>(p);
     case EPI_RELU_DEFER: return launch_prefill_epi<EPI_RELU_DEFER>(p);
     case EPI_ROWSCALE: return launch_prefill_epi<EPI_ROWSCALE>(p);
+    case EPI_ROPE: return launch_prefill_epi<EPI_ROPE>(p);
   }
   return hipErrorInvalidValue;
 }

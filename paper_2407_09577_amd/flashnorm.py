@@ -59,6 +59,8 @@ def _load():
         "flashnorm_glu_act": ([P, I64, I64, I64, I, P, I64, F, I, P, I64, I, P, I, P], I),
         "flashnorm_linear_relu": ([P, I64, I64, I64, I, P, I64, F, P, I64, I, P, I, P], I),
         "rowscale_linear": ([P, I64, I64, I64, I, P, I64, P, P, I64, I, I, P], I),
+        "flashnorm_qkv_rope": ([P, I64, I64, I64, I, P, I64, I64, I64, F, P, P, P, P, I64, F, P, I64, I, P, I, P],
+                               I),
         "flashnorm_linear_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P, I, P], I),
         "flashnorm_glu_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, I64, I, I, P], I),
         "flashnorm_status_string": ([I], ctypes.c_char_p),
@@ -198,6 +200,28 @@ def rowscale_linear(x: torch.Tensor, W_packed: torch.Tensor, N: int, row_scale: 
     _check(_load().rowscale_linear(_ptr(x), M, K, _ld(x), _dt(x), _ptr(W_packed), N,
                                    _ptr(_vec(row_scale, M, "row_scale")), _ptr(y), _ld(y), _dt(y), path,
                                    _stream(stream)), "rowscale_linear")
+    return y
+
+
+def flashnorm_qkv_rope(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv: int, h: int, eps: float,
+                       positions: torch.Tensor, cos_tab: torch.Tensor, sin_tab: torch.Tensor, q_scale: float,
+                       bias=None, out=None, inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    """Deferred RMSNorm -> fused [Wq|Wk|Wv] projection -> RoPE on Q and K (Fig. 5(b))."""
+    M, K = a.shape
+    N = (Hq + 2 * Hkv) * h
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    if positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
+        raise ValueError("positions must be a contiguous int32 tensor of M entries")
+    for name, t in (("cos_tab", cos_tab), ("sin_tab", sin_tab)):
+        if t.dtype != torch.float32 or not t.is_contiguous() or t.dim() != 2 or t.shape[1] != h // 2:
+            raise ValueError(f"{name} must be a contiguous fp32 [P, h/2] tensor")
+    if cos_tab.shape != sin_tab.shape:
+        raise ValueError("cos_tab and sin_tab differ in shape")
+    _check(_load().flashnorm_qkv_rope(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_packed), Hq, Hkv, h, eps,
+                                      _ptr(_vec(bias, N, "bias")), _ptr(positions), _ptr(cos_tab), _ptr(sin_tab),
+                                      cos_tab.shape[0], q_scale, _ptr(y), _ld(y), _dt(y),
+                                      _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
+           "flashnorm_qkv_rope")
     return y
 
 

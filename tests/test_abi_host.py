@@ -188,3 +188,22 @@ def test_unfolded_validation(fnlib):
                                                  Y, 16, 1, kw.get("path", 0), None)
     assert gu(g=0) == -1
     assert gu(path=1) == -5
+
+
+def test_qkv_rope_validation(fnlib):
+    lib = fnlib.lib()
+    T, S, Pz = 0x500000, 0x600000, 0x700000    # cos, sin tables and positions (never dereferenced)
+
+    def qr(**kw):
+        return lib.flashnorm_qkv_rope(A, kw.get("M", 4), 64, 64, kw.get("dt", 1), W, kw.get("Hq", 2), kw.get("Hkv", 1),
+                                      kw.get("h", 8), 1e-6, kw.get("bias", None), kw.get("pos", Pz), kw.get("cos", T),
+                                      kw.get("sin", S), kw.get("P", 16), kw.get("qs", 0.5), kw.get("y", Y), 32,
+                                      kw.get("dt", 1), None, kw.get("path", 0), None)
+    assert qr(h=6) == -2                            # head width a multiple of 4
+    assert qr(h=0) == -2 and qr(Hq=0) == -2 and qr(Hkv=-1) == -2 and qr(P=0) == -2
+    assert qr(qs=float("inf")) == -6
+    assert qr(pos=0) == -1 and qr(cos=0) == -1 and qr(sin=0) == -1
+    assert qr(cos=T + 8) == -4 and qr(pos=Pz + 4) == -4 and qr(bias=X + 4) == -4
+    assert qr(y=T) == -8                            # output overlaps a table
+    assert qr(path=1 | (2 << 8)) == -5              # automatic configuration only
+    assert qr(M=0, pos=0) == 0                      # M == 0: no-op

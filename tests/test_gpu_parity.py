@@ -12,6 +12,8 @@ Full-size workloads run in the launch configuration the benchmark times; where
 the fp64 oracle cannot compute every row in seconds, a fixed sample of rows
 (first, last, tile boundaries and random rows) is compared one by one.
 """
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -479,3 +481,73 @@ def test_unfolded_matches_folded_where_g_is_one(fn, M, path):
     yu = fn.flashnorm_linear_unfolded(a, ones, Wp, w.N, w.eps, path=path)
     torch.cuda.synchronize()
     assert torch.equal(yf.view(torch.int16), yu.view(torch.int16))
+
+
+# ------------------------------------------- fused QKV projection with RoPE (Fig. 5)
+def _qkv_rope_case(fn, M, K, Hq, Hkv, h, dtype, P, seq, seed, bias=False, path=0, pos=None, q_scale=None):
+    N = (Hq + 2 * Hkv) * h
+    w = workloads.make("linear", M, K, N, dtype=dtype, eps=1e-5, seed=seed, outlier_frac=0.05)
+    cos, sin = workloads.rope_tables(P, h)
+    pos = workloads.positions(M, seq) if pos is None else pos
+    qs = 1.0 / math.sqrt(h) if q_scale is None else q_scale
+    b = torch.randn(N, generator=torch.Generator().manual_seed(seed + 1)) if bias else None
+    ws_dt = fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), ws_dtype=ws_dt)
+    inv = torch.empty(M, dtype=torch.float32, device=DEV)
+    y = fn.flashnorm_qkv_rope(w.a.to(DEV), Ws, Hq, Hkv, h, w.eps, pos.to(DEV), cos.to(DEV), sin.to(DEV), qs,
+                              bias=b.to(DEV) if b is not None else None, inv_rms=inv, path=path)
+    torch.cuda.synchronize()
+    return w, y, inv, (pos, cos, sin, qs, b)
+
+
+@pytest.mark.parametrize("dtype,M,K,Hq,Hkv,h,path", [(torch.bfloat16, 300, 328, 3, 1, 64, 1),
+                                                     (torch.bfloat16, 260, 256, 2, 0, 128, 0),
+                                                     (torch.bfloat16, 1, 1032, 4, 2, 128, 2),
+                                                     (torch.bfloat16, 7, 520, 2, 2, 4, 2),
+                                                     (torch.bfloat16, 16, 4096, 8, 8, 128, 0),
+                                                     (torch.float32, 37, 96, 2, 1, 8, 0),
+                                                     (torch.float32, 5, 64, 1, 1, 4, 0)])
+@pytest.mark.parametrize("bias", [False, True])
+def test_qkv_rope(fn, dtype, M, K, Hq, Hkv, h, path, bias):
+    w, y, inv, (pos, cos, sin, qs, b) = _qkv_rope_case(fn, M, K, Hq, Hkv, h, dtype, P=97, seq=61,
+                                                        seed=101 + M + h, bias=bias, path=path)
+    ref = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, Hq, Hkv, h, pos.numpy(), cos, sin, qs, bias=b)
+    assert row_err(to_np(y), ref) <= TOL[dtype]
+    want = np.array([1.0 / oracle.rms(r, w.eps) for r in w.a.double().numpy()])
+    np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
+
+
+def test_llama7b_qkv_rope_sampled(fn):
+    # Llama-7B attention input: 32 query and 32 key/value heads of 128, two sequences of
+    # 2048 tokens, in the tile the QKV workload runs in.
+    w = workloads.llama7b_qkv_prefill()
+    h, H = 128, 32
+    cos, sin = workloads.rope_tables(4096, h)
+    pos = workloads.positions(w.M, 2048)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    y = fn.flashnorm_qkv_rope(w.a.to(DEV), Ws, H, H, h, w.eps, pos.to(DEV), cos.to(DEV), sin.to(DEV),
+                              1.0 / math.sqrt(h))
+    torch.cuda.synchronize()
+    rows = sample_rows(w.M, n=16)
+    ref = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, H, H, h, pos.numpy(), cos, sin, 1.0 / math.sqrt(h),
+                                  rows=rows)
+    err = row_err(to_np(y)[rows], ref)
+    assert err <= TOL[torch.bfloat16], err
+
+
+@pytest.mark.parametrize("dtype,M,path", [(torch.bfloat16, 40, 1), (torch.bfloat16, 3, 2), (torch.float32, 6, 0)])
+def test_qkv_rope_position_outside_table(fn, dtype, M, path):
+    pos = workloads.positions(M, 5)
+    pos[1], pos[-1] = 8, -3                     # outside a table of 8 positions
+    Hq, Hkv, h = 2, 1, 8
+    w, y, _, (pos, cos, sin, qs, _) = _qkv_rope_case(fn, M, 64, Hq, Hkv, h, dtype, P=8, seq=5, seed=7, path=path,
+                                                     pos=pos)
+    got = to_np(y)
+    qk = (Hq + Hkv) * h
+    bad = [1, M - 1]
+    assert np.isnan(got[bad, :qk]).all()
+    assert np.isfinite(got[:, qk:]).all() and np.isfinite(np.delete(got, bad, axis=0)).all()
+    ref = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, Hq, Hkv, h, pos.numpy(), cos, sin, qs)
+    good = np.delete(np.arange(M), bad)
+    assert row_err(got[good], ref[good]) <= TOL[dtype]
+    assert row_err(got[bad][:, qk:], ref[bad][:, qk:]) <= TOL[dtype]
