@@ -281,6 +281,15 @@ int baseline_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, 
                               const float* g, const float* beta, const void* W_packed, int64_t N,
                               float eps, void* x_ws, void* y, int64_t ldy, int path, void* stream);
 
+/* Unfused baseline of flashnorm_qkv_rope's rotation (Fig. 5(a)): RoPE applied in
+ * place to the first (Hq + Hkv) h columns of y (the Q and K heads of a QKV
+ * projection output, leading dimension ldy), Q also times q_scale; arguments as
+ * for flashnorm_qkv_rope.  Run after baseline_rmsnorm_linear for the three-kernel
+ * chain norm -> projection -> rotation. */
+int baseline_rope(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t Hq, int64_t Hkv, int64_t h,
+                  const int32_t* positions, const float* cos_tab, const float* sin_tab, int64_t P,
+                  float q_scale, void* stream);
+
 /* Human-readable name of a status code (static string; never NULL). */
 const char* flashnorm_status_string(int status);
 

@@ -290,6 +290,7 @@ int flashnorm_qkv_rope(const void* a, int64_t M, int64_t K, int64_t lda, int a_d
   if (P > INT32_MAX / h) return FN_ERR_SIZE;
   if (!isfinite(q_scale)) return FN_ERR_VALUE;
   const int64_t N = (Hq + 2 * Hkv) * h;
+  if (N >= (int64_t(1) << 24)) return FN_ERR_SHAPE;  // the head arithmetic runs in fp32
   OpDesc d{a, M, K, lda, a_dtype, W_star_qkv, N, 0, y, ldy, fn::EPI_ROPE, make_ep(eps, K), path,
            (hipStream_t)stream};
   d.ep.bias = bias;
@@ -298,6 +299,7 @@ int flashnorm_qkv_rope(const void* a, int64_t M, int64_t K, int64_t lda, int a_d
   d.ep.rope_cos = cos_tab;
   d.ep.rope_sin = sin_tab;
   d.ep.rope_h = (int)h;
+  d.ep.rope_inv_h = 1.0f / (float)h;
   d.ep.rope_P = (int)P;
   d.ep.rope_q_end = (int)(Hq * h);
   d.ep.rope_k_end = (int)((Hq + Hkv) * h);
@@ -396,6 +398,30 @@ int baseline_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, 
                               void* y, int64_t ldy, int path, void* stream) {
   if (!beta) return FN_ERR_NULL;
   return baseline_common(a, M, K, lda, a_dtype, g, beta, W_packed, N, 0, eps, x_ws, y, ldy, path, stream);
+}
+
+int baseline_rope(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t Hq, int64_t Hkv, int64_t h,
+                  const int32_t* positions, const float* cos_tab, const float* sin_tab, int64_t P, float q_scale,
+                  void* stream) {
+  if (!dtype_ok(y_dtype)) return FN_ERR_DTYPE;
+  if (Hq < 1 || Hkv < 0 || h < 4 || h % 4 || P < 1) return FN_ERR_SHAPE;
+  if (Hq > kMaxRows || Hkv > kMaxRows || h > kMaxRows || (Hq + Hkv) * h > kMaxLd) return FN_ERR_SHAPE;
+  if (P > INT32_MAX / h) return FN_ERR_SIZE;
+  if (!isfinite(q_scale)) return FN_ERR_VALUE;
+  const int64_t qk = (Hq + Hkv) * h;
+  int s = check_matrix(y, M, qk, ldy, y_dtype, true);
+  if (s) return s;
+  if (M == 0) return FN_OK;
+  if (!positions || !cos_tab || !sin_tab) return FN_ERR_NULL;
+  if (!aligned16(cos_tab) || !aligned16(sin_tab) || !aligned16(positions)) return FN_ERR_ALIGN;
+  const int64_t ybytes = extent_bytes(M, qk, ldy, y_dtype), tbytes = P * (h / 2) * (int64_t)sizeof(float);
+  if (overlaps(y, ybytes, cos_tab, tbytes) || overlaps(y, ybytes, sin_tab, tbytes) ||
+      overlaps(y, ybytes, positions, M * (int64_t)sizeof(int32_t)))
+    return FN_ERR_ALIAS;
+  return fn::launch_rope_rows(y, (int)M, (int)ldy, y_dtype, (int)qk, (int)(Hq * h), (int)h, positions, cos_tab,
+                              sin_tab, (int)P, q_scale, (hipStream_t)stream) == hipSuccess
+             ? FN_OK
+             : FN_ERR_HIP;
 }
 
 const char* flashnorm_status_string(int status) {

@@ -112,4 +112,60 @@ hipError_t launch_norm_rows(const void* a, int M, int K, int lda, int dtype, con
               : launch_norm_t<false>(a, M, K, lda, dtype, g, beta, eps, x, ldx, stream);
 }
 
+// Stand-alone RoPE over the Q and K heads of y, in place: the separate rotation
+// of the unfused chain (Fig. 5(a)).  One thread per 4 columns (two pairs of one
+// head) of one row; Q columns also take q_scale.  Memory-bound.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_rows_kernel(T* __restrict__ y, int M, int ldy, int qk, int q_end,
+                                                        int h, const int* __restrict__ pos,
+                                                        const float* __restrict__ cos_tab,
+                                                        const float* __restrict__ sin_tab, int P, float q_scale) {
+  const int groups = qk / 4;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)M * groups) return;
+  const int m = (int)(idx / groups), n = (int)(idx % groups) * 4;
+  T* p = y + (int64_t)m * ldy + n;
+  float t[4];
+  if constexpr (sizeof(T) == 2) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(p);
+    t[0] = bf16_lo(w[0]), t[1] = bf16_hi(w[0]), t[2] = bf16_lo(w[1]), t[3] = bf16_hi(w[1]);
+  } else {
+    const f32x4 w = *reinterpret_cast<const f32x4*>(p);
+    t[0] = w[0], t[1] = w[1], t[2] = w[2], t[3] = w[3];
+  }
+  const int ps = pos[m];
+  const float qs = n < q_end ? q_scale : 1.0f;
+  float o[4];
+  if ((unsigned)ps < (unsigned)P) {
+    const int64_t off = (int64_t)ps * (h / 2) + (n % h) / 2;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const float c = cos_tab[off + q], sn = sin_tab[off + q];
+      o[2 * q] = (t[2 * q] * c - t[2 * q + 1] * sn) * qs;
+      o[2 * q + 1] = (t[2 * q] * sn + t[2 * q + 1] * c) * qs;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o[r] = __builtin_nanf("");
+  }
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<u32x2*>(p) = u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+  } else {
+    *reinterpret_cast<f32x4*>(p) = f32x4{o[0], o[1], o[2], o[3]};
+  }
+}
+
+hipError_t launch_rope_rows(void* y, int M, int ldy, int dtype, int qk, int q_end, int h, const int* pos,
+                            const float* cos_tab, const float* sin_tab, int P, float q_scale, hipStream_t stream) {
+  const int64_t threads = (int64_t)M * (qk / 4);
+  const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+  if (dtype == kDtypeBf16)
+    hipLaunchKernelGGL(rope_rows_kernel<__bf16>, grid, block, 0, stream, (__bf16*)y, M, ldy, qk, q_end, h, pos,
+                       cos_tab, sin_tab, P, q_scale);
+  else
+    hipLaunchKernelGGL(rope_rows_kernel<float>, grid, block, 0, stream, (float*)y, M, ldy, qk, q_end, h, pos,
+                       cos_tab, sin_tab, P, q_scale);
+  return hipGetLastError();
+}
+
 }  // namespace fn

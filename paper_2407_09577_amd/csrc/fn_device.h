@@ -206,6 +206,7 @@ struct EpiArgs {
   const float* rope_cos;
   const float* rope_sin;
   int rope_h, rope_P, rope_q_end, rope_k_end;
+  float rope_inv_h;  // 1/h in fp32
   float rope_q_scale;
 };
 

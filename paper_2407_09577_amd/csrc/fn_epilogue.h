@@ -91,38 +91,66 @@ __device__ __forceinline__ const float* epi_vec(const EpiArgs& ep) {
 // cos*s and sin*s, as in Fig. 5(b), so the per-head scaling disappears.  A bias is
 // added before the rotation (t = acc*s + c).  V columns take the scale only.  A
 // position outside the table makes the Q and K values NaN.
+// n % h without an integer division: the quotient from fp32 (exact for a power of
+// two; otherwise off by at most one for the column counts allowed, n < 2^24), then
+// one correction each way.
+__device__ __forceinline__ int rope_col_in_head(int n, const EpiArgs& ep) {
+  const int q = (int)((float)n * ep.rope_inv_h);
+  int r = n - q * ep.rope_h;
+  r += r < 0 ? ep.rope_h : 0;
+  r -= r >= ep.rope_h ? ep.rope_h : 0;
+  return r;
+}
+
+// The token's angles for the two pairs of columns n .. n+3.  The loads are
+// unconditional (a clamped position; V columns load and ignore their values) and
+// the choices are selects, so the loads of many column groups and rows can be in
+// flight together instead of each waiting inside a branch.
+struct RopeTab {
+  float c0, c1, s0, s1;
+};
+__device__ __forceinline__ RopeTab rope_tab(int n, RowStat st, const EpiArgs& ep) {
+  const bool valid = (unsigned)st.pos < (unsigned)ep.rope_P;
+  const int j = rope_col_in_head(n, ep) >> 1;  // pair of column n (a valid index for V too)
+  const int64_t off = (int64_t)(valid ? st.pos : 0) * (ep.rope_h >> 1) + j;
+  const f32x2 c = *reinterpret_cast<const f32x2*>(ep.rope_cos + off);
+  const f32x2 sn = *reinterpret_cast<const f32x2*>(ep.rope_sin + off);
+  const float nan = __builtin_nanf("");
+  return RopeTab{valid ? c[0] : nan, valid ? c[1] : nan, valid ? sn[0] : nan, valid ? sn[1] : nan};
+}
+
 template <bool VEC>
-__device__ __forceinline__ void rope4(int n, f32x4 v, f32x4 vec, RowStat st, const EpiArgs& ep, float (&o)[4]) {
-  if (n >= ep.rope_k_end) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = fmaf(v[r], st.s, vec[r]);
-    return;
-  }
+__device__ __forceinline__ void rope_apply(int n, f32x4 v, f32x4 vec, RowStat st, RopeTab tb, const EpiArgs& ep,
+                                           float (&o)[4]) {
+  const bool is_v = n >= ep.rope_k_end;
   const float qs = n < ep.rope_q_end ? ep.rope_q_scale : 1.0f;
-  const int j = (n % ep.rope_h) >> 1;  // pair index of column n (even)
-  float c0 = __builtin_nanf(""), s0 = c0, c1 = c0, s1 = c0;
-  if ((unsigned)st.pos < (unsigned)ep.rope_P) {
-    const int64_t off = (int64_t)st.pos * (ep.rope_h >> 1) + j;
-    const f32x2 c = *reinterpret_cast<const f32x2*>(ep.rope_cos + off);
-    const f32x2 sn = *reinterpret_cast<const f32x2*>(ep.rope_sin + off);
-    c0 = c[0], c1 = c[1], s0 = sn[0], s1 = sn[1];
-  }
+  float r[4];
   if constexpr (VEC) {
     float t[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) t[r] = fmaf(v[r], st.s, vec[r]);
-    o[0] = (t[0] * c0 - t[1] * s0) * qs;
-    o[1] = (t[0] * s0 + t[1] * c0) * qs;
-    o[2] = (t[2] * c1 - t[3] * s1) * qs;
-    o[3] = (t[2] * s1 + t[3] * c1) * qs;
+    for (int q = 0; q < 4; ++q) t[q] = fmaf(v[q], st.s, vec[q]);
+    r[0] = (t[0] * tb.c0 - t[1] * tb.s0) * qs;
+    r[1] = (t[0] * tb.s0 + t[1] * tb.c0) * qs;
+    r[2] = (t[2] * tb.c1 - t[3] * tb.s1) * qs;
+    r[3] = (t[2] * tb.s1 + t[3] * tb.c1) * qs;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = is_v ? t[q] : r[q];
   } else {
+    // Fig. 5(b): the token's scale (and the score scale) folded into the angles
     const float f = st.s * qs;
-    c0 *= f, s0 *= f, c1 *= f, s1 *= f;
-    o[0] = v[0] * c0 - v[1] * s0;
-    o[1] = v[0] * s0 + v[1] * c0;
-    o[2] = v[2] * c1 - v[3] * s1;
-    o[3] = v[2] * s1 + v[3] * c1;
+    const float c0 = tb.c0 * f, s0 = tb.s0 * f, c1 = tb.c1 * f, s1 = tb.s1 * f;
+    r[0] = v[0] * c0 - v[1] * s0;
+    r[1] = v[0] * s0 + v[1] * c0;
+    r[2] = v[2] * c1 - v[3] * s1;
+    r[3] = v[2] * s1 + v[3] * c1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = is_v ? v[q] * st.s : r[q];
   }
+}
+
+template <bool VEC>
+__device__ __forceinline__ void rope4(int n, f32x4 v, f32x4 vec, RowStat st, const EpiArgs& ep, float (&o)[4]) {
+  rope_apply<VEC>(n, v, vec, st, rope_tab(n, st, ep), ep, o);
 }
 
 // One output of EPI_ROPE at column c from its own accumulator v and that of its
@@ -133,7 +161,7 @@ __device__ __forceinline__ float rope1(int c, float v, float w, float bv, float 
   if ((unsigned)st.pos >= (unsigned)ep.rope_P) return __builtin_nanf("");
   const float tw = fmaf(w, st.s, bw);
   const float qs = c < ep.rope_q_end ? ep.rope_q_scale : 1.0f;
-  const int64_t off = (int64_t)st.pos * (ep.rope_h >> 1) + ((c % ep.rope_h) >> 1);
+  const int64_t off = (int64_t)st.pos * (ep.rope_h >> 1) + (rope_col_in_head(c, ep) >> 1);
   const float cs = ep.rope_cos[off], sn = ep.rope_sin[off];
   return ((c & 1) ? tw * sn + tv * cs : tv * cs - tw * sn) * qs;
 }
@@ -159,6 +187,15 @@ template <int EPI, bool VEC>
 __device__ __forceinline__ u32x2 epi4_bf16(int n, f32x4 v, f32x4 u, RowStat st, const EpiArgs& ep) {
   float o[4];
   epi4_values<EPI, VEC>(n, v, u, st, ep, o);
+  return pack4_bf16(o);
+}
+
+// EPI_ROPE with the angles (rope_tab) and the bias of the four columns (zeros
+// without) already loaded.
+template <bool VEC>
+__device__ __forceinline__ u32x2 rope4_bf16(int n, f32x4 v, f32x4 vec, RowStat st, RopeTab tb, const EpiArgs& ep) {
+  float o[4];
+  rope_apply<VEC>(n, v, vec, st, tb, ep, o);
   return pack4_bf16(o);
 }
 

@@ -418,14 +418,61 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       if (ep.inv_rms && wn == 0 && lane < 16 && m < M) ep.inv_rms[m] = st.s;
     }
   };
+  // Kinds that read per-row data (a row scale, a token position) take the
+  // statistics of all the lane's rows first, so that every such load is in flight
+  // at once; the others compute them row by row (fewer live registers).
+  constexpr bool kRowData = EPI == EPI_ROWSCALE || EPI == EPI_ROPE;
+  auto row_stats = [&](RowStat (&sts)[FM]) __attribute__((always_inline)) {
+    if constexpr (kRowData) {
+#pragma unroll
+      for (int j = 0; j < FM; ++j) sts[j] = row_stat_at<EPI>(ss[j], sa[j], ep, m0 + wm * TM + j * 16 + lrow, M);
+    }
+  };
+  auto row_stat_j = [&](const RowStat (&sts)[FM], int j) __attribute__((always_inline)) {
+    if constexpr (kRowData) return sts[j];
+    else return row_stat_at<EPI>(ss[j], sa[j], ep, m0 + wm * TM + j * 16 + lrow, M);
+  };
   auto staged = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
+    RowStat sts[FM];
+    row_stats(sts);
     wait_vmcnt<0>();  // the ring's last (zero-filling) transfers have landed
     __syncthreads();  // every wave is done with the ring and the row totals
+    if constexpr (EPI == EPI_ROPE) {
+      // The angles of RB rows at a time are loaded before any of them is used, so
+      // their latencies overlap (the lane's rows hold different tokens).
+      constexpr int RB = FM >= 2 ? 2 : FM;
+      static_assert(FM % RB == 0, "row batches");
+      f32x4 bv[FN];
+#pragma unroll
+      for (int i = 0; i < FN; ++i) {
+        bv[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (VEC) bv[i] = *reinterpret_cast<const f32x4*>(ep.bias + n0 + wn * TN + i * 16 + n_lane);
+      }
+#pragma unroll
+      for (int jb = 0; jb < FM; jb += RB) {
+        RopeTab tb[RB][FN];
+#pragma unroll
+        for (int jj = 0; jj < RB; ++jj)
+#pragma unroll
+          for (int i = 0; i < FN; ++i) tb[jj][i] = rope_tab(n0 + wn * TN + i * 16 + n_lane, sts[jb + jj], ep);
+#pragma unroll
+        for (int jj = 0; jj < RB; ++jj) {
+          const int j = jb + jj;
+          const int r = wm * TM + j * 16 + lrow;
+          write_inv_rms(j, sts[j]);
+#pragma unroll
+          for (int i = 0; i < FN; ++i) {
+            const int c = wn * TN + i * 16 + n_lane;
+            stage4<UPR>(smem, r, c, rope4_bf16<VEC>(n0 + c, acc[i][j], bv[i], sts[j], tb[jj][i], ep));
+          }
+        }
+      }
+    } else
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       const int r = wm * TM + j * 16 + lrow;
-      const RowStat st = row_stat_at<EPI>(ss[j], sa[j], ep, m0 + r, M);
+      const RowStat st = row_stat_j(sts, j);
       write_inv_rms(j, st);
       if constexpr (epi_is_glu(EPI)) {
 #pragma unroll
@@ -446,11 +493,13 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   };
   auto direct = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
+    RowStat sts[FM];
+    row_stats(sts);
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       const int mb = m0 + wm * TM + j * 16;
       const int m = mb + lrow;
-      const RowStat st = row_stat_at<EPI>(ss[j], sa[j], ep, m, M);
+      const RowStat st = row_stat_j(sts, j);
       write_inv_rms(j, st);
       const bool rows_full = mb + 16 <= M;
       if constexpr (epi_is_glu(EPI)) {

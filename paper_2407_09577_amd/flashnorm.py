@@ -61,6 +61,7 @@ def _load():
         "rowscale_linear": ([P, I64, I64, I64, I, P, I64, P, P, I64, I, I, P], I),
         "flashnorm_qkv_rope": ([P, I64, I64, I64, I, P, I64, I64, I64, F, P, P, P, P, I64, F, P, I64, I, P, I, P],
                                I),
+        "baseline_rope": ([P, I64, I64, I, I64, I64, I64, P, P, P, I64, F, P], I),
         "flashnorm_linear_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P, I, P], I),
         "flashnorm_glu_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, I64, I, I, P], I),
         "flashnorm_status_string": ([I], ctypes.c_char_p),
@@ -222,6 +223,17 @@ def flashnorm_qkv_rope(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv: in
                                       cos_tab.shape[0], q_scale, _ptr(y), _ld(y), _dt(y),
                                       _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
            "flashnorm_qkv_rope")
+    return y
+
+
+def baseline_rope(y: torch.Tensor, Hq: int, Hkv: int, h: int, positions: torch.Tensor, cos_tab: torch.Tensor,
+                  sin_tab: torch.Tensor, q_scale: float, stream=None) -> torch.Tensor:
+    """Unfused RoPE on the Q and K heads of y, in place (the rotation kernel of Fig. 5(a))."""
+    M = y.shape[0]
+    if positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
+        raise ValueError("positions must be a contiguous int32 tensor of M entries")
+    _check(_load().baseline_rope(_ptr(y), M, _ld(y), _dt(y), Hq, Hkv, h, _ptr(positions), _ptr(cos_tab),
+                                 _ptr(sin_tab), cos_tab.shape[0], q_scale, _stream(stream)), "baseline_rope")
     return y
 
 

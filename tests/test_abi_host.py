@@ -207,3 +207,19 @@ def test_qkv_rope_validation(fnlib):
     assert qr(y=T) == -8                            # output overlaps a table
     assert qr(path=1 | (2 << 8)) == -5              # automatic configuration only
     assert qr(M=0, pos=0) == 0                      # M == 0: no-op
+
+
+def test_baseline_rope_validation(fnlib):
+    lib = fnlib.lib()
+    T, S, Pz = 0x500000, 0x600000, 0x700000
+
+    def br(**kw):
+        return lib.baseline_rope(kw.get("y", Y), kw.get("M", 4), kw.get("ld", 32), kw.get("dt", 1), 2, 1,
+                                 kw.get("h", 8), kw.get("pos", Pz), T, S, 16, 0.5, None)
+    assert br(h=2) == -2
+    assert br(ld=16) == -2                          # ldy below the Q and K columns
+    assert br(dt=5) == -3
+    assert br(pos=0) == -1
+    assert br(pos=Pz + 4) == -4
+    assert br(y=T) == -8
+    assert br(M=0, pos=0) == 0

@@ -551,3 +551,25 @@ def test_qkv_rope_position_outside_table(fn, dtype, M, path):
     good = np.delete(np.arange(M), bad)
     assert row_err(got[good], ref[good]) <= TOL[dtype]
     assert row_err(got[bad][:, qk:], ref[bad][:, qk:]) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,M", [(torch.bfloat16, 300), (torch.bfloat16, 4), (torch.float32, 37)])
+def test_baseline_qkv_rope_chain(fn, dtype, M):
+    # The unfused chain of Fig. 5(a): normalisation kernel -> projection -> rotation kernel.
+    Hq, Hkv, h = 3, 1, 64
+    N = (Hq + 2 * Hkv) * h
+    w = workloads.make("linear", M, 328, N, dtype=dtype, eps=1e-5, seed=55 + M)
+    cos, sin = workloads.rope_tables(97, h)
+    pos = workloads.positions(M, 61)
+    pos[M // 2] = 97                                  # outside the table: NaN in Q and K
+    ws_dt = fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32
+    Wp, _, _ = fn.fold_weights(w.W.to(DEV), None, ws_dtype=ws_dt)
+    y = fn.baseline_rmsnorm_linear(w.a.to(DEV), w.g.to(DEV), Wp, N, w.eps)
+    fn.baseline_rope(y, Hq, Hkv, h, pos.to(DEV), cos.to(DEV), sin.to(DEV), 0.125)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, Hq, Hkv, h, pos.numpy(), cos, sin, 0.125)
+    got = to_np(y)
+    bad = M // 2
+    assert np.isnan(got[bad, :(Hq + Hkv) * h]).all()
+    good = np.delete(np.arange(M), bad)
+    assert row_err(got[good], ref[good]) <= TOL[dtype]
