@@ -13,7 +13,7 @@ Prints ONE JSON line (rank 0) with the throughput, the roofline of the fused
 kernel (algorithmic FLOPs or bytes per launch / measured launch time) and the
 fp64 CPU oracle timed on a bounded sample of the same workload.
 
-  python bench.py [--steps 100] [--warmup 20] [--workload smollm2_prefill]
+  python bench.py [--steps 100] [--warmup 20] [--workload smollm2_prefill] [--variant folded]
 """
 from __future__ import annotations
 
@@ -44,6 +44,12 @@ def parse_args():
                    choices=["tiny_fp32", "smollm2_prefill", "llama7b_qkv_prefill", "llama7b_swiglu_decode",
                             "layernorm_linear"])
     p.add_argument("--decode-m", type=int, default=16, choices=[1, 4, 16])
+    p.add_argument("--variant", default="folded", choices=["folded", "unfolded", "qkv_rope"],
+                   help="folded: W* = diag(g) W folded offline (the default path); unfolded: g applied at "
+                        "run time to an unfolded W (linear and GLU workloads); qkv_rope: the projection as "
+                        "fused Q|K|V heads with RoPE on Q and K (linear workloads)")
+    p.add_argument("--rope-h", type=int, default=0,
+                   help="qkv_rope head width (default 128 for Llama-7B, else 64); Hq = Hkv = N / (3 h)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-unfused", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle timing sample")
@@ -57,7 +63,7 @@ def parse_args():
 class Setup:
     """GPU-resident rotating operand sets and the closures that run one step."""
 
-    def __init__(self, name, decode_m):
+    def __init__(self, name, decode_m, variant="folded", rope_h=0):
         import torch
         from paper_2407_09577_amd import flashnorm as fn
         from paper_2407_09577_amd import workloads
@@ -95,11 +101,35 @@ class Setup:
         self.M, self.K, self.ncols, self.es = M, K, ncols, es
         self.N = w.N
         self.settle_s = 0.25
+        self.variant = variant
+        if variant == "unfolded" and w.kind == "layernorm":
+            raise SystemExit("--variant unfolded covers the RMSNorm workloads")
+        if variant == "qkv_rope":
+            if w.kind != "linear":
+                raise SystemExit("--variant qkv_rope covers the linear workloads")
+            h = rope_h or (128 if name == "llama7b_qkv_prefill" else 64)
+            if w.N % (3 * h):
+                raise SystemExit(f"N = {w.N} is not 3 x heads x {h}")
+            self.rope = (w.N // (3 * h), w.N // (3 * h), h)  # Hq, Hkv, h
+            cos, sin = workloads.rope_tables(4096, h)
+            self.rope_cos, self.rope_sin = cos.to(dev), sin.to(dev)
+            self.rope_pos_cpu = workloads.positions(M, 2048)  # sequences of 2048 tokens
+            self.rope_pos = self.rope_pos_cpu.to(dev)
+            self.rope_qs = h ** -0.5
 
     def run(self, i):
         fn, w = self.fn, self.w
-        a, Ws, _, y, _ = self.sets[i % self.nsets]
-        if self.kind == "glu":
+        a, Ws, Wp, y, _ = self.sets[i % self.nsets]
+        if self.variant == "unfolded":
+            if self.kind == "glu":
+                fn.flashnorm_glu_unfolded(a, self.g, Wp, self.ncols, w.eps, out=y)
+            else:
+                fn.flashnorm_linear_unfolded(a, self.g, Wp, self.ncols, w.eps, out=y)
+        elif self.variant == "qkv_rope":
+            Hq, Hkv, h = self.rope
+            fn.flashnorm_qkv_rope(a, Ws, Hq, Hkv, h, w.eps, self.rope_pos, self.rope_cos, self.rope_sin,
+                                  self.rope_qs, out=y)
+        elif self.kind == "glu":
             fn.flashnorm_glu(a, Ws, self.ncols, w.eps, out=y)
         elif self.kind == "layernorm":
             fn.flashnorm_layernorm_linear(a, Ws, self.cs, self.cb, self.ncols, w.eps, out=y)
@@ -115,6 +145,9 @@ class Setup:
             fn.baseline_layernorm_linear(a, self.g, self.beta, Wp, self.ncols, w.eps, x_ws=x, out=y)
         else:
             fn.baseline_rmsnorm_linear(a, self.g, Wp, self.ncols, w.eps, x_ws=x, out=y)
+        if self.variant == "qkv_rope":
+            Hq, Hkv, h = self.rope
+            fn.baseline_rope(y, Hq, Hkv, h, self.rope_pos, self.rope_cos, self.rope_sin, self.rope_qs)
 
     def flops(self):
         return 2.0 * self.M * self.K * self.N
@@ -163,7 +196,7 @@ class Setup:
         return start.elapsed_time(end) / steps  # ms per step
 
 
-def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total):
+def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total, s=None):
     """Time the fp64 oracle (as it stands) on a bounded sample of rows of the same workload."""
     import numpy as np
     import oracle
@@ -171,9 +204,15 @@ def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total):
     a = w.a.double().numpy()
     g, W = w.g.double().numpy(), w.W.double().numpy()
     beta = w.beta.double().numpy() if w.beta is not None else None
+    rope = s is not None and s.variant == "qkv_rope"
+    if rope:
+        Hq, Hkv, h = s.rope
+        rope_args = (Hq, Hkv, h, s.rope_pos_cpu.numpy(), s.rope_cos.cpu(), s.rope_sin.cpu(), s.rope_qs)
 
     def call(rows):
-        if w.kind == "glu":
+        if rope:
+            oracle.rmsnorm_qkv_rope(a, g, W, w.eps, *rope_args, rows=rows)
+        elif w.kind == "glu":
             oracle.rmsnorm_swiglu(a, g, W, w.eps, rows=rows)
         elif w.kind == "layernorm":
             oracle.layernorm_linear(a, g, beta, W, w.eps, rows=rows)
@@ -232,7 +271,7 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    s = Setup(args.workload, args.decode_m)
+    s = Setup(args.workload, args.decode_m, args.variant, args.rope_h)
     w = s.w
     decode = args.workload == "llama7b_swiglu_decode"
     fp32 = w.a.dtype == torch.float32
@@ -258,21 +297,32 @@ def main():
     # HBM traffic per launch from the committed rocprofv3 counter summary of this
     # workload, only if it was taken with the current kernel sources.
     from paper_2407_09577_amd import profiling
-    prof = profiling.read_summary(args.workload if not decode else f"{args.workload}_m{args.decode_m}")
+    prof_key = args.workload if not decode else f"{args.workload}_m{args.decode_m}"
+    if args.variant != "folded":
+        prof_key += f"_{args.variant}"
+    prof = profiling.read_summary(prof_key)
     if prof is not None:
         roof["traffic"] = float(prof["traffic_bytes_per_launch"])
 
     cpu = None
     if not args.no_cpu_baseline:
         per_row = 2.0 * w.K * w.N
-        cpu = cpu_baseline(w, unit, args.cpu_seconds, per_row, s.alg_bytes())
+        cpu = cpu_baseline(w, unit, args.cpu_seconds, per_row, s.alg_bytes(), s)
 
     config = {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "out_features": s.ncols, "eps": w.eps,
               "op": {"glu": "flashnorm_glu", "layernorm": "flashnorm_layernorm_linear"}.get(w.kind, "flashnorm_linear"),
+              "variant": args.variant,
               "step": "one fused call on HBM-resident inputs; weight fold done once before timing",
               "launch": "HIP graph replay of the timed steps" if graph else "eager launches from Python",
               "rotating_sets": s.nsets, "alg_flops_per_step": s.flops(), "alg_bytes_per_step": s.alg_bytes(),
               "parallelism": "single GPU"}
+    if args.variant == "unfolded":
+        config["op"] = config["op"].replace("flashnorm_linear", "flashnorm_linear_unfolded").replace(
+            "flashnorm_glu", "flashnorm_glu_unfolded")
+    elif args.variant == "qkv_rope":
+        Hq, Hkv, h = s.rope
+        config.update(op="flashnorm_qkv_rope", heads={"Hq": Hq, "Hkv": Hkv, "h": h},
+                      positions="sequences of 2048 tokens")
     if prof is not None:
         config["traffic_profile"] = prof["path"]
     if ms_unf is not None:
