@@ -573,3 +573,70 @@ def test_baseline_qkv_rope_chain(fn, dtype, M):
     assert np.isnan(got[bad, :(Hq + Hkv) * h]).all()
     good = np.delete(np.arange(M), bad)
     assert row_err(got[good], ref[good]) <= TOL[dtype]
+
+
+def test_graph_replay_matches_eager_extended_ops(fn):
+    # The run-time g, RoPE and GLU-family entry points under HIP-graph capture: every
+    # replay, with eager work in between, reproduces the eager result bit for bit; two
+    # eager calls agree bit for bit (no atomics, no split across workgroups).
+    lin = workloads.make("linear", 300, 256, (2 + 2 * 1) * 64, eps=1e-5, seed=61)
+    dec = workloads.make("glu", 5, 1024, 96, eps=1e-6, seed=62)
+    Wf, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
+    Wu, _, _ = fn.fold_weights(lin.W.to(DEV), None)
+    Wgu, _, _ = fn.fold_weights(dec.W.to(DEV), None, layout=fn.FN_LAYOUT_GLU)
+    Wgf, _, _ = fn.fold_weights(dec.W.to(DEV), dec.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    cos, sin = (t.to(DEV) for t in workloads.rope_tables(64, 64))
+    pos = workloads.positions(300, 50).to(DEV)
+    al, ad, gl, gd = lin.a.to(DEV), dec.a.to(DEV), lin.g.to(DEV), dec.g.to(DEV)
+    outs = [torch.empty(300, lin.N, dtype=torch.bfloat16, device=DEV) for _ in range(2)]
+    outs += [torch.empty(5, 96, dtype=torch.bfloat16, device=DEV) for _ in range(2)]
+    s = torch.empty(5, dtype=torch.float32, device=DEV)
+
+    def step():
+        fn.flashnorm_qkv_rope(al, Wf, 2, 1, 64, lin.eps, pos, cos, sin, 0.125, out=outs[0])
+        fn.flashnorm_linear_unfolded(al, gl, Wu, lin.N, lin.eps, out=outs[1])
+        fn.flashnorm_glu_unfolded(ad, gd, Wgu, 96, dec.eps, out=outs[2])
+        fn.flashnorm_glu_act(ad, Wgf, 96, dec.eps, fn.FN_GLU_SWIGLU_DEFER_UP, inv_rms=s, out=outs[3])
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in outs]
+    step()
+    torch.cuda.synchronize()
+    for got, want in zip(outs, ref):
+        assert torch.equal(got.view(torch.int16), want.view(torch.int16)), "eager repeat"
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for it in range(3):
+        for t in outs:
+            t.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want in zip(outs, ref):
+            assert torch.equal(got.view(torch.int16), want.view(torch.int16)), f"replay {it}"
+
+
+@pytest.mark.parametrize("path", [1, 2])
+def test_extended_ops_with_row_pitch(fn, path):
+    # Activations with a row pitch larger than K (a view into a wider buffer) and a
+    # padded output pitch, for the run-time g and RoPE entry points.
+    M, K, Hq, Hkv, h = 9, 264, 1, 1, 32
+    N = (Hq + 2 * Hkv) * h
+    w = workloads.make("linear", M, K, N, eps=1e-5, seed=63)
+    big = torch.zeros(M, K + 40, dtype=torch.bfloat16, device=DEV)
+    big[:, 8:8 + K] = w.a.to(DEV)
+    a = big[:, 8:8 + K]
+    cos, sin = workloads.rope_tables(16, h)
+    pos = workloads.positions(M, 16)
+    Wf, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    Wu, _, _ = fn.fold_weights(w.W.to(DEV), None)
+    y1 = torch.empty(M, N + 8, dtype=torch.bfloat16, device=DEV)[:, :N]
+    y2 = torch.empty(M, N + 16, dtype=torch.bfloat16, device=DEV)[:, :N]
+    fn.flashnorm_qkv_rope(a, Wf, Hq, Hkv, h, w.eps, pos.to(DEV), cos.to(DEV), sin.to(DEV), 0.5, out=y1, path=path)
+    fn.flashnorm_linear_unfolded(a, w.g.to(DEV), Wu, N, w.eps, out=y2, path=path)
+    torch.cuda.synchronize()
+    ref1 = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, Hq, Hkv, h, pos.numpy(), cos, sin, 0.5)
+    assert row_err(to_np(y1), ref1) <= TOL[torch.bfloat16]
+    assert row_err(to_np(y2), oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
