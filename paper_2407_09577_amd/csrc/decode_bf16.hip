@@ -224,7 +224,7 @@ static hipError_t launch_decode_epi(const DecodeArgs& p) {
     // The epilogue family beyond the core kinds: the automatic configuration only.
     if (p.cfg == 0 || p.cfg == 1) return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT>(p);
     return hipErrorInvalidValue;
-  }
+  } else {
   // Configurations (NCB column blocks per workgroup, KSPLIT waves, U k blocks
   // per load set, double-buffered sets, non-temporal weight loads).  Measured on
   // MI355X (Llama-7B SwiGLU decode, 180 MB of weights): one wave per workgroup,
@@ -245,6 +245,7 @@ static hipError_t launch_decode_epi(const DecodeArgs& p) {
     case 12: return launch_decode_cfg<2, 1, 1, EPI, true, kCachePolicyNT>(p);
   }
   return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_decode_bf16(const DecodeArgs& p) {

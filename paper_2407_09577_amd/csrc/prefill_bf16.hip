@@ -74,6 +74,9 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE + (kUneven ? kFragBytes : 0)];
   // Run-time g (GS), staged once: g[k] for k < K, zeros up to kGsMaxK + 64.
   __shared__ __attribute__((aligned(16))) float g_lds[GS ? kGsMaxK + 64 : 4];
+  // RoPE: each row's scale and token position, for the rotating copy-out.
+  __shared__ float rope_s[EPI == EPI_ROPE ? BM : 1];
+  __shared__ int rope_p[EPI == EPI_ROPE ? BM : 1];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -410,6 +413,14 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   constexpr int OUT_COLS = epi_is_glu(EPI) ? BN / 2 : BN;  // output columns of a tile
   constexpr int UPR = OUT_COLS / 8;                       // 16-byte units per output row
   constexpr bool kStageable = OUT_COLS % 8 == 0 && stage_bytes<BM, UPR>() <= STAGES * STAGE;
+  // RoPE whole tiles: the fp32 accumulators are staged (in passes of RP rows when the
+  // tile does not fit the ring at once) and rotated on the way out (rope_copy_out).
+  constexpr int F32U = OUT_COLS / 4;                       // 16-byte fp32 units per row
+  constexpr bool kF32Xor = F32U % 16 == 0;                 // else rows padded by one unit
+  constexpr int F32_ROW = (kF32Xor ? F32U : F32U + 1) * 16;  // bytes per staged row
+  constexpr int RP = (BM * F32_ROW <= STAGES * STAGE) ? BM : BM / 2;
+  constexpr bool kRopeF32 = EPI == EPI_ROPE && OUT_COLS % 8 == 0 && RP % TM == 0 && BM % RP == 0 &&
+                            RP * F32_ROW <= STAGES * STAGE;
   const int n0 = epi_is_glu(EPI) ? p0 / 2 : p0;
   const int n_lane = (lane >> 4) * 4;
   auto write_inv_rms = [&](int j, const RowStat& st) __attribute__((always_inline)) {
@@ -438,7 +449,57 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     row_stats(sts);
     wait_vmcnt<0>();  // the ring's last (zero-filling) transfers have landed
     __syncthreads();  // every wave is done with the ring and the row totals
-    if constexpr (EPI == EPI_ROPE) {
+    if constexpr (kRopeF32) {
+      // Read in the matrix-core layout, a lane's 16 rows are 16 tokens, so every angle
+      // load would touch 16 table rows.  Here the fp32 accumulators go through LDS
+      // and the copy to HBM rotates them: a thread takes 8 consecutive columns of one
+      // row, and the threads of a row read its angles contiguously.
+      auto f32_pos = [](int r, int u) { return kF32Xor ? r * F32U + (u ^ (r & 15)) : r * (F32U + 1) + u; };
+      constexpr int U8 = OUT_COLS / 8;  // 8-column output units per row
+#pragma unroll
+      for (int pass = 0; pass < BM / RP; ++pass) {
+        if (pass > 0) __syncthreads();  // the previous pass's rows have been copied out
+        if (wm * TM / RP == pass) {
+#pragma unroll
+          for (int j = 0; j < FM; ++j) {
+            const int r = wm * TM + j * 16 + lrow - pass * RP;  // row within the pass
+            write_inv_rms(j, sts[j]);
+            if (wn == 0 && lane < 16) {
+              rope_s[r + pass * RP] = sts[j].s;
+              rope_p[r + pass * RP] = sts[j].pos;
+            }
+#pragma unroll
+            for (int i = 0; i < FN; ++i) {
+              const int u = (wn * TN + i * 16 + n_lane) / 4;
+              *reinterpret_cast<f32x4*>(smem + f32_pos(r, u) * 16) = acc[i][j];
+            }
+          }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = threadIdx.x; q < RP * U8; q += NW * 64) {
+          const int r = q / U8, v = q % U8;
+          const int row = pass * RP + r;
+          const RowStat st{rope_s[row], 0.0f, rope_p[row]};
+          float o[8];
+#pragma unroll
+          for (int hlf = 0; hlf < 2; ++hlf) {
+            const int n = n0 + v * 8 + hlf * 4;
+            const f32x4 a4 = *reinterpret_cast<const f32x4*>(smem + f32_pos(r, 2 * v + hlf) * 16);
+            f32x4 vec = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (VEC) vec = *reinterpret_cast<const f32x4*>(ep.bias + n);
+            float h4[4];
+            rope_apply<VEC>(n, a4, vec, st, rope_tab(n, st, ep), ep, h4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[hlf * 4 + e] = h4[e];
+          }
+          const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
+          const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
+          *reinterpret_cast<u32x4*>(y + (int64_t)(m0 + row) * ldy + n0 + v * 8) = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        }
+      }
+      return;
+    } else if constexpr (EPI == EPI_ROPE) {
       // The angles of RB rows at a time are loaded before any of them is used, so
       // their latencies overlap (the lane's rows hold different tokens).
       constexpr int RB = FM >= 2 ? 2 : FM;
@@ -596,7 +657,7 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
         else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI>(p);
     }
     return hipErrorInvalidValue;
-  }
+  } else {
   switch (tile) {
     case TILE_256x256: return launch_prefill_cfg<256, 256, 2, 2, 4, true, EPI>(p);
     case TILE_128x128: return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
@@ -624,6 +685,7 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
       else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI, true>(p);
   }
   return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_prefill_bf16(const PrefillArgs& p) {
