@@ -433,19 +433,15 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // statistics of all the lane's rows first, so that every such load is in flight
   // at once; the others compute them row by row (fewer live registers).
   constexpr bool kRowData = EPI == EPI_ROWSCALE || EPI == EPI_ROPE;
-  auto row_stats = [&](RowStat (&sts)[FM]) __attribute__((always_inline)) {
+  auto row_stats = [&](RowStat (&sts)[kRowData ? FM : 1]) __attribute__((always_inline)) {
     if constexpr (kRowData) {
 #pragma unroll
       for (int j = 0; j < FM; ++j) sts[j] = row_stat_at<EPI>(ss[j], sa[j], ep, m0 + wm * TM + j * 16 + lrow, M);
     }
   };
-  auto row_stat_j = [&](const RowStat (&sts)[FM], int j) __attribute__((always_inline)) {
-    if constexpr (kRowData) return sts[j];
-    else return row_stat_at<EPI>(ss[j], sa[j], ep, m0 + wm * TM + j * 16 + lrow, M);
-  };
   auto staged = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
-    RowStat sts[FM];
+    RowStat sts[kRowData ? FM : 1];
     row_stats(sts);
     wait_vmcnt<0>();  // the ring's last (zero-filling) transfers have landed
     __syncthreads();  // every wave is done with the ring and the row totals
@@ -533,7 +529,9 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       const int r = wm * TM + j * 16 + lrow;
-      const RowStat st = row_stat_j(sts, j);
+      RowStat st;
+      if constexpr (kRowData) st = sts[j];
+      else st = row_stat_at<EPI>(ss[j], sa[j], ep, m0 + r, M);
       write_inv_rms(j, st);
       if constexpr (epi_is_glu(EPI)) {
 #pragma unroll
@@ -554,13 +552,15 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   };
   auto direct = [&](auto vec_tag) __attribute__((always_inline)) {
     constexpr bool VEC = decltype(vec_tag)::value;
-    RowStat sts[FM];
+    RowStat sts[kRowData ? FM : 1];
     row_stats(sts);
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       const int mb = m0 + wm * TM + j * 16;
       const int m = mb + lrow;
-      const RowStat st = row_stat_j(sts, j);
+      RowStat st;
+      if constexpr (kRowData) st = sts[j];
+      else st = row_stat_at<EPI>(ss[j], sa[j], ep, m, M);
       write_inv_rms(j, st);
       const bool rows_full = mb + 16 <= M;
       if constexpr (epi_is_glu(EPI)) {
