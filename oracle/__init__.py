@@ -264,6 +264,65 @@ def qkv_rope_deferred(a, g, W, eps, Hq, Hkv, h, pos, cos_tab, sin_tab, q_scale, 
     return out
 
 
+def _head_rmsnorm(t, h, w, eps_head):
+    """RMSNorm of every h-wide head of each row of t (the QK-norm / QKV-norm of Sec. 4.3 and
+    Sec. 3.3's QKV-normalization): t_head / sqrt(eps_head + mean(t_head^2)) * w, w of length h."""
+    t, w = _f64(t), _f64(w)
+    M, N = t.shape
+    heads = t.reshape(M, N // h, h)
+    ms = np.mean(heads * heads, axis=2, keepdims=True)
+    return (heads / np.sqrt(_eps(eps_head) + ms) * w).reshape(M, N)
+
+
+def rmsnorm_qkv_headnorm(a, g, W, eps, Hq, Hkv, h, gq, gk, gv, eps_head, pos=None, cos_tab=None, sin_tab=None,
+                         q_scale=1.0, rows=None) -> np.ndarray:
+    """Standard form (Fig. 6(a) with per-head second norms): x = RMSNorm(a; g), t = x W with
+    W = [Wq | Wk | Wv]; every Q head RMS-normalised with weight gq, every K head with gk (QK-norm),
+    every V head with gv when gv is given (QKV-normalization), else V = t; then RoPE on Q and K
+    when positions are given, and Q times q_scale."""
+    qe, ke = Hq * h, (Hq + Hkv) * h
+    if _f64(W).shape[1] != (Hq + 2 * Hkv) * h:
+        raise ValueError("W must have (Hq + 2 Hkv) h columns")
+    t = rmsnorm_linear(a, g, W, eps, rows=rows)
+    out = t.copy()
+    out[:, :qe] = _head_rmsnorm(t[:, :qe], h, gq, eps_head)
+    out[:, qe:ke] = _head_rmsnorm(t[:, qe:ke], h, gk, eps_head)
+    if gv is not None:
+        out[:, ke:] = _head_rmsnorm(t[:, ke:], h, gv, eps_head)
+    if pos is not None:
+        p = np.asarray(pos).ravel()
+        if rows is not None:
+            p = p[np.asarray(rows, dtype=np.int64)]
+        out[:, :ke] = rope(out[:, :ke], h, p, cos_tab, sin_tab)
+    out[:, :qe] *= float(np.float32(q_scale))
+    return out
+
+
+def qkv_headnorm_cancelled(a, g, W, eps, Hq, Hkv, h, gq, gk, gv, eps_head, pos=None, cos_tab=None,
+                           sin_tab=None, q_scale=1.0, rows=None) -> np.ndarray:
+    """Prop. 3 form (Fig. 6(b)): the per-head norms act on z = a W* (W* = diag(g) W) directly,
+    the input RMSNorm's scale dropped; V without gv keeps z / RMSe(a). Equal to the standard
+    form when eps_head = 0 (the epsilon caveat otherwise). Self-check."""
+    a, g, W = _f64(a), _f64(g), _f64(W)
+    r, nr = _rows(rows, a.shape[0])
+    if r is None:
+        r = np.arange(nr)
+    a = a[r]
+    qe, ke = Hq * h, (Hq + Hkv) * h
+    z = a @ (g[:, None] * W)
+    out = z.copy()
+    out[:, :qe] = _head_rmsnorm(z[:, :qe], h, gq, eps_head)
+    out[:, qe:ke] = _head_rmsnorm(z[:, qe:ke], h, gk, eps_head)
+    if gv is not None:
+        out[:, ke:] = _head_rmsnorm(z[:, ke:], h, gv, eps_head)
+    else:
+        out[:, ke:] = z[:, ke:] / np.array([rms(row, _eps(eps)) for row in a])[:, None]
+    if pos is not None:
+        out[:, :ke] = rope(out[:, :ke], h, np.asarray(pos).ravel()[r], cos_tab, sin_tab)
+    out[:, :qe] *= float(np.float32(q_scale))
+    return out
+
+
 def _ln_like(fn, a, g, beta, W, eps, bias, rows):
     a, g, beta, W, bias = _f64(a), _f64(g), _f64(beta), _f64(W), _f64(bias)
     M, K = a.shape

@@ -557,3 +557,60 @@ def test_qkv_rope_position_outside_table_is_nan_in_q_and_k_only():
     assert np.isfinite(y[0]).all()
     for r in (1, 2):
         assert np.isnan(y[r, :12]).all() and np.isfinite(y[r, 12:]).all()
+
+
+# ---------------------------------------------------------------- per-head norms after the projection (Sec. 3.3, 4.3)
+def test_qkv_headnorm_exact_worked_example():
+    fx = _read_fixture("qkv_headnorm_worked_example.txt")
+    h, Hq, Hkv = int(fx["h"][0][0]), int(fx["Hq"][0][0]), int(fx["Hkv"][0][0])
+    qs = float(_frac(fx["q_scale"][0][0]))
+    vec = lambda k: np.array([float(_frac(v)) for v in fx[k][0]])
+    mat = lambda k: np.array([[float(_frac(v)) for v in r] for r in fx[k]])
+    a, g, W, gq, gk, gv = vec("a")[None, :], vec("g"), mat("W"), vec("gq"), vec("gk"), vec("gv")
+    cos, sin = mat("cos"), mat("sin")
+    for eps_s, eh_s, pos_s, gv_s, *vals in fx["case"]:
+        eps, eh, pos = float(_frac(eps_s)), float(_frac(eh_s)), int(pos_s)
+        kw = dict(pos=[pos], cos_tab=cos, sin_tab=sin) if pos >= 0 else {}
+        want = np.array([float(_frac(v)) for v in vals])
+        args = (a, g, W, eps, Hq, Hkv, h, gq, gk, gv if gv_s == "1" else None, eh)
+        np.testing.assert_allclose(oracle.rmsnorm_qkv_headnorm(*args, q_scale=qs, **kw)[0], want,
+                                   rtol=1e-14, atol=1e-14)
+        if eh == 0:  # Prop. 3: the input norm cancels exactly without a head epsilon
+            np.testing.assert_allclose(oracle.qkv_headnorm_cancelled(*args, q_scale=qs, **kw)[0], want,
+                                       rtol=1e-14, atol=1e-14)
+
+
+@pytest.mark.parametrize("with_gv", [False, True])
+def test_qkv_headnorm_matches_torch_and_cancellation(with_gv):
+    # The standard form rebuilt from torch rms_norm (input and per head), a matmul and
+    # complex rotation; Prop. 3 at eps_head = 0 for any input eps; the epsilon caveat
+    # (Sec. 3.3) bounded for a small head epsilon; Q and K independent of the input scale.
+    M, K, Hq, Hkv, h = 6, 48, 2, 1, 8
+    N = (Hq + 2 * Hkv) * h
+    a, g, W = _rand_case(M, K, N, 17, neg_g=True)
+    rng = np.random.default_rng(18)
+    gq, gk, gv = (rng.uniform(0.5, 1.5, h) for _ in range(3))
+    gv = gv if with_gv else None
+    cos, sin = (t.double().numpy() for t in workloads.rope_tables(32, h))
+    pos = rng.integers(0, 32, M)
+    eps, eh, qs = 1e-5, 1e-6, 1.0 / math.sqrt(h)
+    std = oracle.rmsnorm_qkv_headnorm(a, g, W, eps, Hq, Hkv, h, gq, gk, gv, eh, pos, cos, sin, qs)
+    x = F.rms_norm(torch.from_numpy(a), (K,), weight=torch.from_numpy(g), eps=float(np.float32(eps)))
+    t = (x @ torch.from_numpy(W)).reshape(M, N // h, h)
+    e32 = float(np.float32(eh))
+    ref = torch.cat([F.rms_norm(t[:, :Hq], (h,), weight=torch.from_numpy(gq), eps=e32),
+                     F.rms_norm(t[:, Hq:Hq + Hkv], (h,), weight=torch.from_numpy(gk), eps=e32),
+                     F.rms_norm(t[:, Hq + Hkv:], (h,), weight=torch.from_numpy(gv), eps=e32) if with_gv
+                     else t[:, Hq + Hkv:]], dim=1).reshape(M, N).numpy()
+    qk = (Hq + Hkv) * h
+    ref[:, :qk] = _complex_rope(ref[:, :qk], h, pos, cos, sin)
+    ref[:, :Hq * h] *= float(np.float32(qs))
+    np.testing.assert_allclose(std, ref, rtol=1e-12, atol=1e-13)
+    args = (a, g, W, eps, Hq, Hkv, h, gq, gk, gv)
+    np.testing.assert_allclose(oracle.qkv_headnorm_cancelled(*args, 0.0, pos, cos, sin, qs),
+                               oracle.rmsnorm_qkv_headnorm(*args, 0.0, pos, cos, sin, qs), rtol=1e-12, atol=1e-13)
+    canc = oracle.qkv_headnorm_cancelled(*args, eh, pos, cos, sin, qs)
+    assert 0 < np.max(np.abs(canc - std)) < 1e-4 * np.max(np.abs(std))
+    scaled = oracle.rmsnorm_qkv_headnorm(7.0 * a, g, W, 0.0, Hq, Hkv, h, gq, gk, gv, 0.0, pos, cos, sin, qs)
+    base = oracle.rmsnorm_qkv_headnorm(a, g, W, 0.0, Hq, Hkv, h, gq, gk, gv, 0.0, pos, cos, sin, qs)
+    np.testing.assert_allclose(scaled[:, :qk], base[:, :qk], rtol=1e-12, atol=1e-13)
