@@ -44,10 +44,11 @@ def parse_args():
                    choices=["tiny_fp32", "smollm2_prefill", "llama7b_qkv_prefill", "llama7b_swiglu_decode",
                             "layernorm_linear"])
     p.add_argument("--decode-m", type=int, default=16, choices=[1, 4, 16])
-    p.add_argument("--variant", default="folded", choices=["folded", "unfolded", "qkv_rope"],
+    p.add_argument("--variant", default="folded", choices=["folded", "unfolded", "qkv_rope", "qkv_headnorm"],
                    help="folded: W* = diag(g) W folded offline (the default path); unfolded: g applied at "
                         "run time to an unfolded W (linear and GLU workloads); qkv_rope: the projection as "
-                        "fused Q|K|V heads with RoPE on Q and K (linear workloads)")
+                        "fused Q|K|V heads with RoPE on Q and K; qkv_headnorm: the same with QK-norm (per-head "
+                        "RMSNorm of Q and K, Prop. 3) before RoPE (linear workloads)")
     p.add_argument("--rope-h", type=int, default=0,
                    help="qkv_rope head width (default 128 for Llama-7B, else 64); Hq = Hkv = N / (3 h)")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -104,9 +105,9 @@ class Setup:
         self.variant = variant
         if variant == "unfolded" and w.kind == "layernorm":
             raise SystemExit("--variant unfolded covers the RMSNorm workloads")
-        if variant == "qkv_rope":
+        if variant in ("qkv_rope", "qkv_headnorm"):
             if w.kind != "linear":
-                raise SystemExit("--variant qkv_rope covers the linear workloads")
+                raise SystemExit(f"--variant {variant} covers the linear workloads")
             h = rope_h or (128 if name == "llama7b_qkv_prefill" else 64)
             if w.N % (3 * h):
                 raise SystemExit(f"N = {w.N} is not 3 x heads x {h}")
@@ -116,6 +117,10 @@ class Setup:
             self.rope_pos_cpu = workloads.positions(M, 2048)  # sequences of 2048 tokens
             self.rope_pos = self.rope_pos_cpu.to(dev)
             self.rope_qs = h ** -0.5
+            gen_hn = torch.Generator().manual_seed(1)
+            self.hn_gq_cpu = torch.rand(h, generator=gen_hn) + 0.5  # per-head norm weights
+            self.hn_gk_cpu = torch.rand(h, generator=gen_hn) + 0.5
+            self.hn_gq, self.hn_gk = self.hn_gq_cpu.to(dev), self.hn_gk_cpu.to(dev)
 
     def run(self, i):
         fn, w = self.fn, self.w
@@ -129,6 +134,11 @@ class Setup:
             Hq, Hkv, h = self.rope
             fn.flashnorm_qkv_rope(a, Ws, Hq, Hkv, h, w.eps, self.rope_pos, self.rope_cos, self.rope_sin,
                                   self.rope_qs, out=y)
+        elif self.variant == "qkv_headnorm":
+            Hq, Hkv, h = self.rope
+            fn.flashnorm_qkv_headnorm(a, Ws, Hq, Hkv, h, w.eps, self.hn_gq, self.hn_gk, None, 1e-6,
+                                      positions=self.rope_pos, cos_tab=self.rope_cos, sin_tab=self.rope_sin,
+                                      q_scale=self.rope_qs, out=y)
         elif self.kind == "glu":
             fn.flashnorm_glu(a, Ws, self.ncols, w.eps, out=y)
         elif self.kind == "layernorm":
@@ -148,6 +158,10 @@ class Setup:
         if self.variant == "qkv_rope":
             Hq, Hkv, h = self.rope
             fn.baseline_rope(y, Hq, Hkv, h, self.rope_pos, self.rope_cos, self.rope_sin, self.rope_qs)
+        elif self.variant == "qkv_headnorm":
+            Hq, Hkv, h = self.rope
+            fn.baseline_qkv_headnorm(y, Hq, Hkv, h, self.hn_gq, self.hn_gk, None, 1e-6, self.rope_pos,
+                                     self.rope_cos, self.rope_sin, self.rope_qs)
 
     def flops(self):
         return 2.0 * self.M * self.K * self.N
@@ -204,13 +218,17 @@ def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total, s=None):
     a = w.a.double().numpy()
     g, W = w.g.double().numpy(), w.W.double().numpy()
     beta = w.beta.double().numpy() if w.beta is not None else None
-    rope = s is not None and s.variant == "qkv_rope"
+    rope = s is not None and s.variant in ("qkv_rope", "qkv_headnorm")
     if rope:
         Hq, Hkv, h = s.rope
         rope_args = (Hq, Hkv, h, s.rope_pos_cpu.numpy(), s.rope_cos.cpu(), s.rope_sin.cpu(), s.rope_qs)
 
     def call(rows):
-        if rope:
+        if rope and s.variant == "qkv_headnorm":
+            Hq, Hkv, h, pos, cos, sin, qs = rope_args
+            oracle.rmsnorm_qkv_headnorm(a, g, W, w.eps, Hq, Hkv, h, s.hn_gq_cpu, s.hn_gk_cpu, None, 1e-6, pos=pos,
+                                        cos_tab=cos, sin_tab=sin, q_scale=qs, rows=rows)
+        elif rope:
             oracle.rmsnorm_qkv_rope(a, g, W, w.eps, *rope_args, rows=rows)
         elif w.kind == "glu":
             oracle.rmsnorm_swiglu(a, g, W, w.eps, rows=rows)
@@ -319,9 +337,9 @@ def main():
     if args.variant == "unfolded":
         config["op"] = config["op"].replace("flashnorm_linear", "flashnorm_linear_unfolded").replace(
             "flashnorm_glu", "flashnorm_glu_unfolded")
-    elif args.variant == "qkv_rope":
+    elif args.variant in ("qkv_rope", "qkv_headnorm"):
         Hq, Hkv, h = s.rope
-        config.update(op="flashnorm_qkv_rope", heads={"Hq": Hq, "Hkv": Hkv, "h": h},
+        config.update(op="flashnorm_" + args.variant, heads={"Hq": Hq, "Hkv": Hkv, "h": h},
                       positions="sequences of 2048 tokens")
     if prof is not None:
         config["traffic_profile"] = prof["path"]

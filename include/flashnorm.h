@@ -281,6 +281,33 @@ int baseline_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, 
                               const float* g, const float* beta, const void* W_packed, int64_t N,
                               float eps, void* x_ws, void* y, int64_t ldy, int path, void* stream);
 
+/* RMSNorm -> fused QKV projection -> per-head RMSNorm of the Q and K heads (QK-norm,
+ * Sec. 4.3) or of Q, K and V (QKV-normalization, Sec. 3.3) -> RoPE on Q and K.
+ * By Prop. 3 ("RMSNorm cancellation") the input norm's scale cancels in every
+ * normalised head, so those heads are normalised straight from t = a W*
+ * (W_star_qkv folded with the input g, FN_LAYOUT_LINEAR, heads ordered as for
+ * flashnorm_qkv_rope):
+ *   Q head:  y = RoPE(t_head / sqrt(eps_head + mean(t_head^2)) * gq) * q_scale
+ *   K head:  y = RoPE(t_head / sqrt(eps_head + mean(t_head^2)) * gk)
+ *   V head:  with gv, as K without the rotation (the input RMSNorm is then
+ *            eliminated entirely); without gv (QK-norm), y = t_head * s_m with
+ *            s_m = 1/RMSe(a_m) as in flashnorm_linear.
+ * With eps_head > 0 this differs from the standard form (input RMSNorm first) by
+ * the epsilon caveat of Sec. 3.3, negligible unless a head's energy is tiny.
+ *   gq, gk     [h] fp32 (required), shared by all heads; gv [h] or NULL.  16-byte aligned.
+ *   eps_head   >= 0, finite.  h in {8, 16, 32, 64, 128, 256}.
+ *   positions  [M] int32 or NULL (no rotation); cos_tab, sin_tab, P as for
+ *              flashnorm_qkv_rope (required with positions).
+ *   inv_rms    optional [M] output of s_m.
+ * bf16 only (fp32: FN_ERR_UNSUPPORTED); every M runs on the tile kernel (a
+ * workgroup must hold whole heads); path as for flashnorm_glu_act. */
+int flashnorm_qkv_headnorm(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                           const void* W_star_qkv, int64_t Hq, int64_t Hkv, int64_t h, float eps,
+                           const float* gq, const float* gk, const float* gv, float eps_head,
+                           const int32_t* positions, const float* cos_tab, const float* sin_tab,
+                           int64_t P, float q_scale, void* y, int64_t ldy, int y_dtype,
+                           float* inv_rms, int path, void* stream);
+
 /* Unfused baseline of flashnorm_qkv_rope's rotation (Fig. 5(a)): RoPE applied in
  * place to the first (Hq + Hkv) h columns of y (the Q and K heads of a QKV
  * projection output, leading dimension ldy), Q also times q_scale; arguments as
@@ -289,6 +316,15 @@ int baseline_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, 
 int baseline_rope(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t Hq, int64_t Hkv, int64_t h,
                   const int32_t* positions, const float* cos_tab, const float* sin_tab, int64_t P,
                   float q_scale, void* stream);
+
+/* Unfused baseline of flashnorm_qkv_headnorm's per-head stage (the standard form:
+ * input RMSNorm -> projection -> per-head norms -> RoPE): applied in place to the
+ * Q and K heads of y (and V heads when gv is given), Q times q_scale; arguments as
+ * for flashnorm_qkv_headnorm; bf16 only.  Run after baseline_rmsnorm_linear. */
+int baseline_qkv_headnorm(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t Hq, int64_t Hkv,
+                          int64_t h, const float* gq, const float* gk, const float* gv, float eps_head,
+                          const int32_t* positions, const float* cos_tab, const float* sin_tab,
+                          int64_t P, float q_scale, void* stream);
 
 /* Human-readable name of a status code (static string; never NULL). */
 const char* flashnorm_status_string(int status);

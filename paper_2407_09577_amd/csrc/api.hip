@@ -107,7 +107,9 @@ int run_op(const OpDesc& d) {
     return status_of(fn::launch_f32(p));
   }
   const int base_path = d.path & 0xff;
-  const bool decode = base_path == FN_PATH_DECODE || (base_path == FN_PATH_AUTO && d.M <= FN_DECODE_MAX_M);
+  // The per-head norms need whole heads in one workgroup: always the tile kernel.
+  const bool decode = d.epi != fn::EPI_HEADNORM &&
+                      (base_path == FN_PATH_DECODE || (base_path == FN_PATH_AUTO && d.M <= FN_DECODE_MAX_M));
   if (decode) {
     fn::DecodeArgs p{(const __bf16*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const __bf16*)d.ws, NP, KP,
                      (int)d.ncols, (__bf16*)d.y, (int)d.ldy, d.epi, d.path >> FN_PATH_TILE_SHIFT, d.ep,
@@ -317,6 +319,53 @@ int flashnorm_qkv_rope(const void* a, int64_t M, int64_t K, int64_t lda, int a_d
   return run_op(d);
 }
 
+// Fused QKV projection with per-head RMSNorm of Q and K (and V), Prop. 3 / Sec. 4.3.
+int flashnorm_qkv_headnorm(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star_qkv,
+                           int64_t Hq, int64_t Hkv, int64_t h, float eps, const float* gq, const float* gk,
+                           const float* gv, float eps_head, const int32_t* positions, const float* cos_tab,
+                           const float* sin_tab, int64_t P, float q_scale, void* y, int64_t ldy, int y_dtype,
+                           float* inv_rms, int path, void* stream) {
+  if (Hq < 1 || Hkv < 0 || Hq > kMaxRows || Hkv > kMaxRows) return FN_ERR_SHAPE;
+  if (h != 8 && h != 16 && h != 32 && h != 64 && h != 128 && h != 256) return FN_ERR_SHAPE;
+  if (positions && (P < 1 || P > INT32_MAX / h)) return P < 1 ? FN_ERR_SHAPE : FN_ERR_SIZE;
+  if (!isfinite(q_scale) || !(eps_head >= 0.0f) || !isfinite(eps_head)) return FN_ERR_VALUE;
+  const int64_t N = (Hq + 2 * Hkv) * h;
+  if (N >= (int64_t(1) << 24)) return FN_ERR_SHAPE;
+  OpDesc d{a, M, K, lda, a_dtype, W_star_qkv, N, 0, y, ldy, fn::EPI_HEADNORM, make_ep(eps, K), path,
+           (hipStream_t)stream};
+  d.ep.inv_rms = inv_rms;
+  d.ep.rope_pos = positions;
+  d.ep.rope_cos = cos_tab;
+  d.ep.rope_sin = sin_tab;
+  d.ep.rope_h = (int)h;
+  d.ep.rope_inv_h = 1.0f / (float)h;
+  d.ep.rope_P = positions ? (int)P : 0;
+  d.ep.rope_q_end = (int)(Hq * h);
+  d.ep.rope_k_end = (int)((Hq + Hkv) * h);
+  d.ep.rope_q_scale = q_scale;
+  d.ep.hn_gq = gq;
+  d.ep.hn_gk = gk;
+  d.ep.hn_gv = gv;
+  d.ep.hn_eps = eps_head;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  if (a_dtype != FN_BF16) return FN_ERR_UNSUPPORTED;
+  if ((s = check_auto_config(path))) return s;
+  if (M == 0) return FN_OK;
+  if (!gq || !gk) return FN_ERR_NULL;
+  if (positions && (!cos_tab || !sin_tab)) return FN_ERR_NULL;
+  if (!aligned16(gq) || !aligned16(gk) || !aligned16(gv) || !aligned16(positions) || !aligned16(cos_tab) ||
+      !aligned16(sin_tab))
+    return FN_ERR_ALIGN;
+  const int64_t ybytes = extent_bytes(M, N, ldy, a_dtype), wb = h * (int64_t)sizeof(float);
+  const int64_t tbytes = positions ? P * (h / 2) * (int64_t)sizeof(float) : 0;
+  if (overlaps(y, ybytes, gq, wb) || overlaps(y, ybytes, gk, wb) || (gv && overlaps(y, ybytes, gv, wb)) ||
+      (positions && (overlaps(y, ybytes, cos_tab, tbytes) || overlaps(y, ybytes, sin_tab, tbytes) ||
+                     overlaps(y, ybytes, positions, M * (int64_t)sizeof(int32_t)))))
+    return FN_ERR_ALIAS;
+  return run_op(d);
+}
+
 // Run-time g (unfolded W): g must be given, 16-byte aligned; the bf16 tile path
 // stages g in LDS and takes K <= fn::kGsMaxK.
 static int check_runtime_g(const OpDesc& d, const float* g) {
@@ -420,6 +469,42 @@ int baseline_rope(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t Hq, int6
     return FN_ERR_ALIAS;
   return fn::launch_rope_rows(y, (int)M, (int)ldy, y_dtype, (int)qk, (int)(Hq * h), (int)h, positions, cos_tab,
                               sin_tab, (int)P, q_scale, (hipStream_t)stream) == hipSuccess
+             ? FN_OK
+             : FN_ERR_HIP;
+}
+
+int baseline_qkv_headnorm(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t Hq, int64_t Hkv, int64_t h,
+                          const float* gq, const float* gk, const float* gv, float eps_head, const int32_t* positions,
+                          const float* cos_tab, const float* sin_tab, int64_t P, float q_scale, void* stream) {
+  if (y_dtype != FN_BF16) return dtype_ok(y_dtype) ? FN_ERR_UNSUPPORTED : FN_ERR_DTYPE;
+  if (Hq < 1 || Hkv < 0 || Hq > kMaxRows || Hkv > kMaxRows) return FN_ERR_SHAPE;
+  if (h != 8 && h != 16 && h != 32 && h != 64 && h != 128 && h != 256) return FN_ERR_SHAPE;
+  if (positions && (P < 1 || P > INT32_MAX / h)) return P < 1 ? FN_ERR_SHAPE : FN_ERR_SIZE;
+  if (!isfinite(q_scale) || !(eps_head >= 0.0f) || !isfinite(eps_head)) return FN_ERR_VALUE;
+  const int64_t ncols = (Hq + Hkv + (gv ? Hkv : 0)) * h;
+  if ((Hq + 2 * Hkv) * h >= (int64_t(1) << 24)) return FN_ERR_SHAPE;
+  int s = check_matrix(y, M, ncols, ldy, y_dtype, true);
+  if (s) return s;
+  if (M == 0) return FN_OK;
+  if (!gq || !gk || (positions && (!cos_tab || !sin_tab))) return FN_ERR_NULL;
+  if (!aligned16(gq) || !aligned16(gk) || !aligned16(gv) || !aligned16(positions) || !aligned16(cos_tab) ||
+      !aligned16(sin_tab))
+    return FN_ERR_ALIGN;
+  EpiArgs ep{};
+  ep.rope_pos = positions;
+  ep.rope_cos = cos_tab;
+  ep.rope_sin = sin_tab;
+  ep.rope_h = (int)h;
+  ep.rope_inv_h = 1.0f / (float)h;
+  ep.rope_P = positions ? (int)P : 0;
+  ep.rope_q_end = (int)(Hq * h);
+  ep.rope_k_end = (int)((Hq + Hkv) * h);
+  ep.rope_q_scale = q_scale;
+  ep.hn_gq = gq;
+  ep.hn_gk = gk;
+  ep.hn_gv = gv;
+  ep.hn_eps = eps_head;
+  return fn::launch_headnorm_rows(y, (int)M, (int)ldy, (int)ncols, ep, (hipStream_t)stream) == hipSuccess
              ? FN_OK
              : FN_ERR_HIP;
 }

@@ -7,6 +7,7 @@
 // the epilogue scale.  Memory-bound: 16-byte accesses, the row re-reads hit L2.
 #include "fn_device.h"
 #include "fn_launch.h"
+#include "fn_epilogue.h"
 
 namespace fn {
 
@@ -165,6 +166,35 @@ hipError_t launch_rope_rows(void* y, int M, int ldy, int dtype, int qk, int q_en
   else
     hipLaunchKernelGGL(rope_rows_kernel<float>, grid, block, 0, stream, (float*)y, M, ldy, qk, q_end, h, pos,
                        cos_tab, sin_tab, P, q_scale);
+  return hipGetLastError();
+}
+
+// Stand-alone per-head RMSNorm (QK-norm / QKV-normalization) with RoPE over the
+// normalised output of the unfused chain, in place: one thread per 8 columns of a
+// row; a head's h/8 threads are consecutive lanes (rows hold whole heads), so the
+// head's squares are summed by butterfly exchange.  The same per-unit arithmetic
+// as the fused epilogue, with the input scale already applied (s = 1).
+__global__ __launch_bounds__(256) void headnorm_rows_kernel(__bf16* __restrict__ y, int M, int ldy, int ncols,
+                                                            EpiArgs ep) {
+  const int U = ncols / 8;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)M * U) return;  // whole heads leave together
+  const int m = (int)(idx / U), v = (int)(idx % U);
+  __bf16* p = y + (int64_t)m * ldy + v * 8;
+  const u32x4 w = *reinterpret_cast<const u32x4*>(p);
+  const f32x4 a0 = {bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+  const f32x4 a1 = {bf16_lo(w[2]), bf16_hi(w[2]), bf16_lo(w[3]), bf16_hi(w[3])};
+  const RowStat st{1.0f, 0.0f, ep.rope_pos ? ep.rope_pos[m] : 0};
+  float o[8];
+  headnorm8(v * 8, a0, a1, st, ep, o);
+  *reinterpret_cast<u32x4*>(p) = u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
+                                       pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])};
+}
+
+hipError_t launch_headnorm_rows(void* y, int M, int ldy, int ncols, const EpiArgs& ep, hipStream_t stream) {
+  const int64_t threads = (int64_t)M * (ncols / 8);
+  const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+  hipLaunchKernelGGL(headnorm_rows_kernel, grid, block, 0, stream, (__bf16*)y, M, ldy, ncols, ep);
   return hipGetLastError();
 }
 

@@ -176,6 +176,7 @@ enum Epi : int {
   EPI_RELU_DEFER = 8,   // y = relu(acc), s exported                    (Fig. 2(b))
   EPI_ROWSCALE = 9,     // y = acc * row_scale[m]   (applies a deferred scale)
   EPI_ROPE = 10,        // fused QKV: RoPE on Q and K with s folded into the tables (Fig. 5(b))
+  EPI_HEADNORM = 11,    // fused QKV: per-head RMSNorm of Q, K (and V), input scale dropped (Prop. 3)
 };
 
 constexpr bool epi_is_glu(int e) {
@@ -183,11 +184,12 @@ constexpr bool epi_is_glu(int e) {
 }
 constexpr bool epi_needs_ss(int e) {
   return e == EPI_RMS || e == EPI_GLU || e == EPI_LN || e == EPI_REGLU || e == EPI_BILINEAR ||
-         e == EPI_GLU_DEFER || e == EPI_RELU_DEFER || e == EPI_ROPE;
+         e == EPI_GLU_DEFER || e == EPI_RELU_DEFER || e == EPI_ROPE || e == EPI_HEADNORM;
 }
 // Kinds whose per-row scale s = 1/RMSe(a) can be written to the inv_rms output.
 constexpr bool epi_exports_s(int e) {
-  return e == EPI_RMS || e == EPI_GLU || e == EPI_GLU_DEFER || e == EPI_RELU_DEFER || e == EPI_ROPE;
+  return e == EPI_RMS || e == EPI_GLU || e == EPI_GLU_DEFER || e == EPI_RELU_DEFER || e == EPI_ROPE ||
+         e == EPI_HEADNORM;
 }
 
 struct EpiArgs {
@@ -207,6 +209,12 @@ struct EpiArgs {
   const float* rope_sin;
   int rope_h, rope_P, rope_q_end, rope_k_end;
   float rope_inv_h;  // 1/h in fp32
+  // EPI_HEADNORM: per-head norm weights [h] of Q, K and (optional, QKV-normalization) V,
+  // the heads' epsilon; rope_pos == nullptr turns the rotation off.
+  const float* hn_gq;
+  const float* hn_gk;
+  const float* hn_gv;
+  float hn_eps;
   float rope_q_scale;
 };
 

@@ -23,7 +23,7 @@ template <int EPI>
 __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& ep) {
   RowStat st{1.0f, 0.0f, 0};
   if constexpr (EPI == EPI_RMS || EPI == EPI_GLU || EPI == EPI_GLU_DEFER || EPI == EPI_RELU_DEFER ||
-                EPI == EPI_ROPE) {
+                EPI == EPI_ROPE || EPI == EPI_HEADNORM) {
     // RMSe(a) = sqrt(eps + ss/K)  (App. "RMS with epsilon")
     st.s = rsqrtf(fmaf(ss, ep.inv_k, ep.eps));
   } else if constexpr (EPI == EPI_REGLU || EPI == EPI_BILINEAR) {
@@ -49,6 +49,7 @@ __device__ __forceinline__ RowStat row_stat_at(float ss, float sa, const EpiArgs
   RowStat st = row_stat<EPI>(ss, sa, ep);
   if constexpr (EPI == EPI_ROWSCALE) st.s = m < M ? ep.row_scale[m] : 0.0f;
   if constexpr (EPI == EPI_ROPE) st.pos = m < M ? ep.rope_pos[m] : 0;
+  if constexpr (EPI == EPI_HEADNORM) st.pos = (m < M && ep.rope_pos) ? ep.rope_pos[m] : 0;
   return st;
 }
 
@@ -63,7 +64,7 @@ __device__ __forceinline__ u32x2 pack4_bf16(const float (&o)[4]) {
 // bias, added after the scaling; LN: c*), 0 when absent; cs: colsum (LN).
 template <int EPI>
 __device__ __forceinline__ float epi_value(float v, float u, RowStat st, float vec, float cs) {
-  static_assert(EPI != EPI_ROPE, "RoPE outputs come in pairs: rope4 / rope1");
+  static_assert(EPI != EPI_ROPE && EPI != EPI_HEADNORM, "per-pair / per-head kinds: rope4, rope1, headnorm8");
   if constexpr (EPI == EPI_RMS) return fmaf(v, st.s, vec);
   else if constexpr (EPI == EPI_GLU) return silu(v * st.s) * (u * st.s);
   else if constexpr (EPI == EPI_LN) return fmaf(fmaf(-st.mu, cs, v), st.s, vec);
@@ -188,6 +189,50 @@ __device__ __forceinline__ u32x2 epi4_bf16(int n, f32x4 v, f32x4 u, RowStat st, 
   float o[4];
   epi4_values<EPI, VEC>(n, v, u, st, ep, o);
   return pack4_bf16(o);
+}
+
+// EPI_HEADNORM: the 8 columns n .. n+7 of one row, held by one lane; a head's h/8
+// such units sit in h/8 consecutive lanes of the wave, which sum their squares by
+// butterfly exchange (every lane of the wave takes part).  By Prop. 3 the input
+// norm's scale cancels in a normalised head, so Q and K heads (and V heads when gv
+// is given: QKV-normalization) are normalised straight from a W*: t / sqrt(eps_h +
+// mean(t^2)) * w, then RoPE on Q and K when positions are given, and Q times the
+// score scale.  V heads without gv take the input scale s.
+__device__ __forceinline__ void headnorm8(int n, f32x4 a0, f32x4 a1, RowStat st, const EpiArgs& ep,
+                                          float (&o)[8]) {
+  float ss = ((a0[0] * a0[0] + a0[1] * a0[1]) + (a0[2] * a0[2] + a0[3] * a0[3])) +
+             ((a1[0] * a1[0] + a1[1] * a1[1]) + (a1[2] * a1[2] + a1[3] * a1[3]));
+  for (int off = 1; off < (ep.rope_h >> 3); off <<= 1) ss += __shfl_xor(ss, off);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = a0[e], o[4 + e] = a1[e];
+  const bool is_q = n < ep.rope_q_end, is_k = !is_q && n < ep.rope_k_end;
+  const float* w = is_q ? ep.hn_gq : is_k ? ep.hn_gk : ep.hn_gv;
+  const int c = rope_col_in_head(n, ep);
+  if (w) {
+    const float sc = rsqrtf(fmaf(ss, ep.rope_inv_h, ep.hn_eps));
+    const f32x4 w0 = *reinterpret_cast<const f32x4*>(w + c), w1 = *reinterpret_cast<const f32x4*>(w + c + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] *= sc * w0[e], o[4 + e] *= sc * w1[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] *= st.s;
+  }
+  if ((is_q || is_k) && ep.rope_pos) {
+    const bool valid = (unsigned)st.pos < (unsigned)ep.rope_P;
+    const int64_t off = (int64_t)(valid ? st.pos : 0) * (ep.rope_h >> 1) + (c >> 1);
+    const f32x4 cs = *reinterpret_cast<const f32x4*>(ep.rope_cos + off);
+    const f32x4 sn = *reinterpret_cast<const f32x4*>(ep.rope_sin + off);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float x0 = o[2 * q], x1 = o[2 * q + 1];
+      o[2 * q] = valid ? x0 * cs[q] - x1 * sn[q] : __builtin_nanf("");
+      o[2 * q + 1] = valid ? x0 * sn[q] + x1 * cs[q] : __builtin_nanf("");
+    }
+  }
+  if (is_q) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] *= ep.rope_q_scale;
+  }
 }
 
 // EPI_ROPE with the angles (rope_tab) and the bias of the four columns (zeros

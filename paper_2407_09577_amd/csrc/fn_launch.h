@@ -115,6 +115,10 @@ hipError_t launch_unpack(const void* ws, int64_t K, int64_t N, int glu, int ws_d
 hipError_t launch_norm_rows(const void* a, int M, int K, int lda, int dtype, const float* g,
                             const float* beta, float eps, void* x, int ldx, hipStream_t stream);
 
+// Unfused baseline per-head norms (+ RoPE): the first ncols columns of y in place
+// (EPI_HEADNORM arguments in ep; ncols a multiple of the head width).
+hipError_t launch_headnorm_rows(void* y, int M, int ldy, int ncols, const EpiArgs& ep, hipStream_t stream);
+
 // Unfused baseline RoPE: rotate the Q and K heads (first qk columns) of y in place.
 hipError_t launch_rope_rows(void* y, int M, int ldy, int dtype, int qk, int q_end, int h, const int* pos,
                             const float* cos_tab, const float* sin_tab, int P, float q_scale, hipStream_t stream);

@@ -75,8 +75,9 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // Run-time g (GS), staged once: g[k] for k < K, zeros up to kGsMaxK + 64.
   __shared__ __attribute__((aligned(16))) float g_lds[GS ? kGsMaxK + 64 : 4];
   // RoPE: each row's scale and token position, for the rotating copy-out.
-  __shared__ float rope_s[EPI == EPI_ROPE ? BM : 1];
-  __shared__ int rope_p[EPI == EPI_ROPE ? BM : 1];
+  constexpr bool kRowLds = EPI == EPI_ROPE || EPI == EPI_HEADNORM;
+  __shared__ float rope_s[kRowLds ? BM : 1];
+  __shared__ int rope_p[kRowLds ? BM : 1];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -419,8 +420,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   constexpr bool kF32Xor = F32U % 16 == 0;                 // else rows padded by one unit
   constexpr int F32_ROW = (kF32Xor ? F32U : F32U + 1) * 16;  // bytes per staged row
   constexpr int RP = (BM * F32_ROW <= STAGES * STAGE) ? BM : BM / 2;
-  constexpr bool kRopeF32 = EPI == EPI_ROPE && OUT_COLS % 8 == 0 && RP % TM == 0 && BM % RP == 0 &&
-                            RP * F32_ROW <= STAGES * STAGE;
+  constexpr bool kRopeF32 = (EPI == EPI_ROPE || EPI == EPI_HEADNORM) && OUT_COLS % 8 == 0 && RP % TM == 0 &&
+                            BM % RP == 0 && RP * F32_ROW <= STAGES * STAGE;
+  // The per-head norms need whole heads in one tile and the fp32 staging: every tile
+  // (also at the ragged edges, with guarded stores) takes the staged path.
+  static_assert(EPI != EPI_HEADNORM || (kRopeF32 && (RP * (OUT_COLS / 8)) % (NW * 64) == 0),
+                "per-head norms: fp32 staging and a uniform copy-out loop");
   const int n0 = epi_is_glu(EPI) ? p0 / 2 : p0;
   const int n_lane = (lane >> 4) * 4;
   auto write_inv_rms = [&](int j, const RowStat& st) __attribute__((always_inline)) {
@@ -432,7 +437,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // Kinds that read per-row data (a row scale, a token position) take the
   // statistics of all the lane's rows first, so that every such load is in flight
   // at once; the others compute them row by row (fewer live registers).
-  constexpr bool kRowData = EPI == EPI_ROWSCALE || EPI == EPI_ROPE;
+  constexpr bool kRowData = EPI == EPI_ROWSCALE || EPI == EPI_ROPE || EPI == EPI_HEADNORM;
   auto row_stats = [&](RowStat (&sts)[kRowData ? FM : 1]) __attribute__((always_inline)) {
     if constexpr (kRowData) {
 #pragma unroll
@@ -478,20 +483,29 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
           const int row = pass * RP + r;
           const RowStat st{rope_s[row], 0.0f, rope_p[row]};
           float o[8];
+          if constexpr (EPI == EPI_HEADNORM) {
+            headnorm8(n0 + v * 8, *reinterpret_cast<const f32x4*>(smem + f32_pos(r, 2 * v) * 16),
+                      *reinterpret_cast<const f32x4*>(smem + f32_pos(r, 2 * v + 1) * 16), st, ep, o);
+          } else {
 #pragma unroll
-          for (int hlf = 0; hlf < 2; ++hlf) {
-            const int n = n0 + v * 8 + hlf * 4;
-            const f32x4 a4 = *reinterpret_cast<const f32x4*>(smem + f32_pos(r, 2 * v + hlf) * 16);
-            f32x4 vec = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (VEC) vec = *reinterpret_cast<const f32x4*>(ep.bias + n);
-            float h4[4];
-            rope_apply<VEC>(n, a4, vec, st, rope_tab(n, st, ep), ep, h4);
+            for (int hlf = 0; hlf < 2; ++hlf) {
+              const int n = n0 + v * 8 + hlf * 4;
+              const f32x4 a4 = *reinterpret_cast<const f32x4*>(smem + f32_pos(r, 2 * v + hlf) * 16);
+              f32x4 vec = {0.f, 0.f, 0.f, 0.f};
+              if constexpr (VEC) vec = *reinterpret_cast<const f32x4*>(ep.bias + n);
+              float h4[4];
+              rope_apply<VEC>(n, a4, vec, st, rope_tab(n, st, ep), ep, h4);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) o[hlf * 4 + e] = h4[e];
+              for (int e = 0; e < 4; ++e) o[hlf * 4 + e] = h4[e];
+            }
           }
-          const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
-          const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
-          *reinterpret_cast<u32x4*>(y + (int64_t)(m0 + row) * ldy + n0 + v * 8) = u32x4{lo[0], lo[1], hi[0], hi[1]};
+          // whole tiles, or (per-head norms) rows and columns inside the output
+          if (m0 + row < M && n0 + v * 8 < ncols) {
+            const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
+            const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
+            *reinterpret_cast<u32x4*>(y + (int64_t)(m0 + row) * ldy + n0 + v * 8) =
+                u32x4{lo[0], lo[1], hi[0], hi[1]};
+          }
         }
       }
       return;
@@ -585,19 +599,23 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     }
   };
   // Workgroup-uniform: every wave takes the same branch (the staged path has barriers).
-  const bool whole = kStageable && m0 + BM <= M && n0 + OUT_COLS <= ncols && (ldy & 7) == 0;
-  const bool vec = epi_vec<EPI>(ep) != nullptr;
-  if constexpr (kStageable) {
-    if (whole) {
-      if (vec) staged(std::true_type{});
-      else staged(std::false_type{});
-      return;
+  if constexpr (EPI == EPI_HEADNORM) {
+    staged(std::false_type{});
+  } else {
+    const bool whole = kStageable && m0 + BM <= M && n0 + OUT_COLS <= ncols && (ldy & 7) == 0;
+    const bool vec = epi_vec<EPI>(ep) != nullptr;
+    if constexpr (kStageable) {
+      if (whole) {
+        if (vec) staged(std::true_type{});
+        else staged(std::false_type{});
+        return;
+      }
     }
+    if (vec)
+      direct(std::true_type{});
+    else
+      direct(std::false_type{});
   }
-  if (vec)
-    direct(std::true_type{});
-  else
-    direct(std::false_type{});
 }
 
 template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false>
@@ -646,7 +664,13 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   } else {
     if (p.gs) return hipErrorInvalidValue;
   }
-  if constexpr (EPI >= EPI_REGLU) {
+  if constexpr (EPI == EPI_HEADNORM) {
+    // Whole heads per tile: 256 columns, or 128 when that fills the chip better and
+    // holds whole heads.
+    if (tile == TILE_256x256_W8_PF_SP || p.ep.rope_h > 128)
+      return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
+    return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI>(p);
+  } else if constexpr (EPI >= EPI_REGLU) {
     // The epilogue family beyond the core kinds is built for the automatically
     // chosen tiles only.
     switch (tile) {
@@ -701,6 +725,7 @@ hipError_t launch_prefill_bf16(const PrefillArgs& p) {
     case EPI_RELU_DEFER: return launch_prefill_epi<EPI_RELU_DEFER>(p);
     case EPI_ROWSCALE: return launch_prefill_epi<EPI_ROWSCALE>(p);
     case EPI_ROPE: return launch_prefill_epi<EPI_ROPE>(p);
+    case EPI_HEADNORM: return launch_prefill_epi<EPI_HEADNORM>(p);
   }
   return hipErrorInvalidValue;
 }

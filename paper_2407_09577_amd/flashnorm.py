@@ -62,6 +62,9 @@ def _load():
         "flashnorm_qkv_rope": ([P, I64, I64, I64, I, P, I64, I64, I64, F, P, P, P, P, I64, F, P, I64, I, P, I, P],
                                I),
         "baseline_rope": ([P, I64, I64, I, I64, I64, I64, P, P, P, I64, F, P], I),
+        "baseline_qkv_headnorm": ([P, I64, I64, I, I64, I64, I64, P, P, P, F, P, P, P, I64, F, P], I),
+        "flashnorm_qkv_headnorm": ([P, I64, I64, I64, I, P, I64, I64, I64, F, P, P, P, F, P, P, P, I64, F, P, I64,
+                                    I, P, I, P], I),
         "flashnorm_linear_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P, I, P], I),
         "flashnorm_glu_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, I64, I, I, P], I),
         "flashnorm_status_string": ([I], ctypes.c_char_p),
@@ -223,6 +226,41 @@ def flashnorm_qkv_rope(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv: in
                                       cos_tab.shape[0], q_scale, _ptr(y), _ld(y), _dt(y),
                                       _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
            "flashnorm_qkv_rope")
+    return y
+
+
+def flashnorm_qkv_headnorm(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv: int, h: int, eps: float,
+                           gq: torch.Tensor, gk: torch.Tensor, gv, eps_head: float, positions=None, cos_tab=None,
+                           sin_tab=None, q_scale: float = 1.0, out=None, inv_rms=None, path: int = FN_PATH_AUTO,
+                           stream=None) -> torch.Tensor:
+    """Deferred RMSNorm -> fused [Wq|Wk|Wv] -> per-head RMSNorm of Q, K (and V with gv) -> RoPE (Prop. 3)."""
+    M, K = a.shape
+    N = (Hq + 2 * Hkv) * h
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    P_rows = 0
+    if positions is not None:
+        if positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
+            raise ValueError("positions must be a contiguous int32 tensor of M entries")
+        if cos_tab is None or sin_tab is None or cos_tab.shape != sin_tab.shape or cos_tab.shape[1:] != (h // 2,):
+            raise ValueError("cos_tab and sin_tab must be [P, h/2] fp32")
+        P_rows = cos_tab.shape[0]
+    _check(_load().flashnorm_qkv_headnorm(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_packed), Hq, Hkv, h, eps,
+                                          _ptr(_vec(gq, h, "gq")), _ptr(_vec(gk, h, "gk")), _ptr(_vec(gv, h, "gv")),
+                                          eps_head, _ptr(positions), _ptr(cos_tab), _ptr(sin_tab), P_rows, q_scale,
+                                          _ptr(y), _ld(y), _dt(y), _ptr(_vec(inv_rms, M, "inv_rms")), path,
+                                          _stream(stream)), "flashnorm_qkv_headnorm")
+    return y
+
+
+def baseline_qkv_headnorm(y: torch.Tensor, Hq: int, Hkv: int, h: int, gq, gk, gv, eps_head: float, positions=None,
+                          cos_tab=None, sin_tab=None, q_scale: float = 1.0, stream=None) -> torch.Tensor:
+    """Unfused per-head norms (+ RoPE) on the Q and K (and V) heads of y, in place."""
+    M = y.shape[0]
+    P_rows = cos_tab.shape[0] if (positions is not None and cos_tab is not None) else 0
+    _check(_load().baseline_qkv_headnorm(_ptr(y), M, _ld(y), _dt(y), Hq, Hkv, h, _ptr(_vec(gq, h, "gq")),
+                                         _ptr(_vec(gk, h, "gk")), _ptr(_vec(gv, h, "gv")), eps_head, _ptr(positions),
+                                         _ptr(cos_tab), _ptr(sin_tab), P_rows, q_scale, _stream(stream)),
+           "baseline_qkv_headnorm")
     return y
 
 

@@ -223,3 +223,37 @@ def test_baseline_rope_validation(fnlib):
     assert br(pos=Pz + 4) == -4
     assert br(y=T) == -8
     assert br(M=0, pos=0) == 0
+
+
+def test_qkv_headnorm_validation(fnlib):
+    lib = fnlib.lib()
+    G1, G2, T, S, Pz = 0x500000, 0x510000, 0x600000, 0x610000, 0x700000
+
+    def hn(**kw):
+        return lib.flashnorm_qkv_headnorm(A, kw.get("M", 4), 64, 64, kw.get("dt", 1), W, 2, 1, kw.get("h", 8), 1e-6,
+                                          kw.get("gq", G1), kw.get("gk", G2), kw.get("gv", None), kw.get("eh", 1e-6),
+                                          kw.get("pos", Pz), kw.get("cos", T), kw.get("sin", S), 16, 0.5,
+                                          kw.get("y", Y), 32, kw.get("dt", 1), None, kw.get("path", 0), None)
+    assert hn(h=12) == -2 and hn(h=4) == -2        # head width: a power of two from 8 to 256
+    assert hn(dt=0) == -5                           # bf16 only
+    assert hn(eh=-1.0) == -6 and hn(eh=float("nan")) == -6
+    assert hn(gq=0) == -1 and hn(gk=0) == -1
+    assert hn(cos=0) == -1                          # positions need the tables
+    assert hn(pos=0, cos=0, sin=0, y=G1) == -8      # no positions: no tables needed (stops at the alias check)
+    assert hn(gv=G1 + 4) == -4
+    assert hn(y=G1) == -8
+    assert hn(path=1 | (3 << 8)) == -5
+    assert hn(M=0, gq=0) == 0
+
+
+def test_baseline_qkv_headnorm_validation(fnlib):
+    lib = fnlib.lib()
+    G1, G2, T, S, Pz = 0x500000, 0x510000, 0x600000, 0x610000, 0x700000
+
+    def bh(**kw):
+        return lib.baseline_qkv_headnorm(Y, kw.get("M", 4), kw.get("ld", 32), kw.get("dt", 1), 2, 1, kw.get("h", 8),
+                                         kw.get("gq", G1), G2, None, 1e-6, kw.get("pos", Pz), T, S, 16, 0.5, None)
+    assert bh(h=6) == -2 and bh(dt=0) == -5 and bh(dt=7) == -3
+    assert bh(ld=16) == -2                          # ldy below the normalised columns
+    assert bh(gq=0) == -1 and bh(pos=Pz + 4) == -4
+    assert bh(M=0, gq=0) == 0

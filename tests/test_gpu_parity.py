@@ -640,3 +640,91 @@ def test_extended_ops_with_row_pitch(fn, path):
     ref1 = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, Hq, Hkv, h, pos.numpy(), cos, sin, 0.5)
     assert row_err(to_np(y1), ref1) <= TOL[torch.bfloat16]
     assert row_err(to_np(y2), oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
+
+
+# ------------------------------------------- per-head norms after the QKV projection (Prop. 3)
+@pytest.mark.parametrize("M,K,Hq,Hkv,h,with_gv,rope", [(300, 328, 3, 1, 64, False, True), (300, 328, 3, 1, 64, True, True),
+                                                       (5, 520, 2, 2, 128, False, True), (70, 256, 2, 1, 256, True, False),
+                                                       (130, 136, 4, 2, 8, False, False), (1, 1032, 1, 1, 128, True, True)])
+def test_qkv_headnorm(fn, M, K, Hq, Hkv, h, with_gv, rope):
+    N = (Hq + 2 * Hkv) * h
+    w = workloads.make("linear", M, K, N, eps=1e-5, seed=131 + M + h, outlier_frac=0.05)
+    g = torch.Generator().manual_seed(h + M)
+    gq, gk, gv = (torch.rand(h, generator=g) + 0.5 for _ in range(3))
+    gv = gv if with_gv else None
+    cos, sin = workloads.rope_tables(64, h)
+    pos = workloads.positions(M, 50)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    inv = torch.empty(M, dtype=torch.float32, device=DEV)
+    kw = dict(positions=pos.to(DEV), cos_tab=cos.to(DEV), sin_tab=sin.to(DEV)) if rope else {}
+    y = fn.flashnorm_qkv_headnorm(w.a.to(DEV), Ws, Hq, Hkv, h, w.eps, gq.to(DEV), gk.to(DEV),
+                                  gv.to(DEV) if gv is not None else None, 1e-6, q_scale=h ** -0.5, inv_rms=inv,
+                                  **kw)
+    torch.cuda.synchronize()
+    okw = dict(pos=pos.numpy(), cos_tab=cos, sin_tab=sin) if rope else {}
+    ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, Hq, Hkv, h, gq, gk, gv, 1e-6, q_scale=h ** -0.5, **okw)
+    assert row_err(to_np(y), ref) <= TOL[torch.bfloat16]
+    want = np.array([1.0 / oracle.rms(r, w.eps) for r in w.a.double().numpy()])
+    np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
+
+
+def test_llama7b_qkv_headnorm_sampled(fn):
+    # The Llama-7B QKV shape with QK-norm and RoPE (32 + 32 + 32 heads of 128), in the
+    # 256 x 256 tile.
+    w = workloads.llama7b_qkv_prefill()
+    h, H = 128, 32
+    g = torch.Generator().manual_seed(7)
+    gq, gk = torch.rand(h, generator=g) + 0.5, torch.rand(h, generator=g) + 0.5
+    cos, sin = workloads.rope_tables(4096, h)
+    pos = workloads.positions(w.M, 2048)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    y = fn.flashnorm_qkv_headnorm(w.a.to(DEV), Ws, H, H, h, w.eps, gq.to(DEV), gk.to(DEV), None, 1e-6,
+                                  positions=pos.to(DEV), cos_tab=cos.to(DEV), sin_tab=sin.to(DEV), q_scale=h ** -0.5)
+    torch.cuda.synchronize()
+    rows = sample_rows(w.M, n=12)
+    ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, H, H, h, gq, gk, None, 1e-6, pos=pos.numpy(),
+                                      cos_tab=cos, sin_tab=sin, q_scale=h ** -0.5, rows=rows)
+    err = row_err(to_np(y)[rows], ref)
+    assert err <= TOL[torch.bfloat16], err
+
+
+def test_qkv_headnorm_position_outside_table(fn):
+    M, Hq, Hkv, h = 20, 2, 1, 16
+    N = (Hq + 2 * Hkv) * h
+    w = workloads.make("linear", M, 64, N, eps=1e-5, seed=141)
+    ones = torch.ones(h, device=DEV)
+    cos, sin = workloads.rope_tables(8, h)
+    pos = workloads.positions(M, 8)
+    pos[3] = 8
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    y = fn.flashnorm_qkv_headnorm(w.a.to(DEV), Ws, Hq, Hkv, h, w.eps, ones, ones, None, 0.0, positions=pos.to(DEV),
+                                  cos_tab=cos.to(DEV), sin_tab=sin.to(DEV))
+    torch.cuda.synchronize()
+    got = to_np(y)
+    qk = (Hq + Hkv) * h
+    assert np.isnan(got[3, :qk]).all() and np.isfinite(got[3, qk:]).all()
+    good = np.delete(np.arange(M), 3)
+    ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, Hq, Hkv, h, np.ones(h), np.ones(h), None, 0.0,
+                                      pos=pos.numpy(), cos_tab=cos, sin_tab=sin)
+    assert row_err(got[good], ref[good]) <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("with_gv", [False, True])
+def test_baseline_qkv_headnorm_chain(fn, with_gv):
+    # The unfused standard form: normalisation kernel -> projection -> per-head norms + RoPE.
+    M, Hq, Hkv, h = 300, 3, 1, 64
+    N = (Hq + 2 * Hkv) * h
+    w = workloads.make("linear", M, 328, N, eps=1e-5, seed=151)
+    g = torch.Generator().manual_seed(152)
+    gq, gk, gv = (torch.rand(h, generator=g) + 0.5 for _ in range(3))
+    gv = gv if with_gv else None
+    cos, sin = workloads.rope_tables(64, h)
+    pos = workloads.positions(M, 50)
+    Wp, _, _ = fn.fold_weights(w.W.to(DEV), None)
+    y = fn.baseline_rmsnorm_linear(w.a.to(DEV), w.g.to(DEV), Wp, N, w.eps)
+    fn.baseline_qkv_headnorm(y, Hq, Hkv, h, gq.to(DEV), gk.to(DEV), gv.to(DEV) if gv is not None else None, 1e-6,
+                             pos.to(DEV), cos.to(DEV), sin.to(DEV), 0.125)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, Hq, Hkv, h, gq, gk, gv, 1e-6, pos=pos.numpy(),
+                                      cos_tab=cos, sin_tab=sin, q_scale=0.125)
+    assert row_err(to_np(y), ref) <= TOL[torch.bfloat16]
