@@ -300,12 +300,12 @@ int flashnorm_qkv_rope(const void* a, int64_t M, int64_t K, int64_t lda, int a_d
   d.ep.rope_pos = positions;
   d.ep.rope_cos = cos_tab;
   d.ep.rope_sin = sin_tab;
-  d.ep.rope_h = (int)h;
-  d.ep.rope_inv_h = 1.0f / (float)h;
+  d.ep.head_h = (int)h;
+  d.ep.head_inv_h = 1.0f / (float)h;
   d.ep.rope_P = (int)P;
-  d.ep.rope_q_end = (int)(Hq * h);
-  d.ep.rope_k_end = (int)((Hq + Hkv) * h);
-  d.ep.rope_q_scale = q_scale;
+  d.ep.q_end = (int)(Hq * h);
+  d.ep.k_end = (int)((Hq + Hkv) * h);
+  d.ep.q_scale = q_scale;
   int s = validate_op(d, y_dtype);
   if (s) return s;
   if ((s = check_auto_config(path))) return s;
@@ -337,12 +337,12 @@ int flashnorm_qkv_headnorm(const void* a, int64_t M, int64_t K, int64_t lda, int
   d.ep.rope_pos = positions;
   d.ep.rope_cos = cos_tab;
   d.ep.rope_sin = sin_tab;
-  d.ep.rope_h = (int)h;
-  d.ep.rope_inv_h = 1.0f / (float)h;
+  d.ep.head_h = (int)h;
+  d.ep.head_inv_h = 1.0f / (float)h;
   d.ep.rope_P = positions ? (int)P : 0;
-  d.ep.rope_q_end = (int)(Hq * h);
-  d.ep.rope_k_end = (int)((Hq + Hkv) * h);
-  d.ep.rope_q_scale = q_scale;
+  d.ep.q_end = (int)(Hq * h);
+  d.ep.k_end = (int)((Hq + Hkv) * h);
+  d.ep.q_scale = q_scale;
   d.ep.hn_gq = gq;
   d.ep.hn_gk = gk;
   d.ep.hn_gv = gv;
@@ -494,12 +494,12 @@ int baseline_qkv_headnorm(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t 
   ep.rope_pos = positions;
   ep.rope_cos = cos_tab;
   ep.rope_sin = sin_tab;
-  ep.rope_h = (int)h;
-  ep.rope_inv_h = 1.0f / (float)h;
+  ep.head_h = (int)h;
+  ep.head_inv_h = 1.0f / (float)h;
   ep.rope_P = positions ? (int)P : 0;
-  ep.rope_q_end = (int)(Hq * h);
-  ep.rope_k_end = (int)((Hq + Hkv) * h);
-  ep.rope_q_scale = q_scale;
+  ep.q_end = (int)(Hq * h);
+  ep.k_end = (int)((Hq + Hkv) * h);
+  ep.q_scale = q_scale;
   ep.hn_gq = gq;
   ep.hn_gk = gk;
   ep.hn_gv = gv;

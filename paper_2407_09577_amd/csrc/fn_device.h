@@ -201,21 +201,22 @@ struct EpiArgs {
   float* inv_rms;       // optional [M] output of s (kinds with epi_exports_s)
   const float* row_scale;  // EPI_ROWSCALE: [M]
   const float* g_rt;       // run-time normalisation weight [K] (unfolded W), or nullptr
-  // EPI_ROPE: output columns [0, q_end) are Q heads, [q_end, k_end) K heads, the rest V;
-  // heads are rope_h wide; row m is a token at position rope_pos[m], whose angles are
-  // rope_cos / rope_sin [rope_P][rope_h / 2]; Q is also multiplied by rope_q_scale.
+  // Fused QKV kinds (EPI_ROPE, EPI_HEADNORM): output columns [0, q_end) are Q heads,
+  // [q_end, k_end) K heads, the rest V; heads are head_h wide; Q is also multiplied by
+  // q_scale.  Row m is a token at position rope_pos[m], whose angles are rope_cos /
+  // rope_sin [rope_P][head_h / 2] (EPI_HEADNORM: rope_pos == nullptr, no rotation).
   const int* rope_pos;
   const float* rope_cos;
   const float* rope_sin;
-  int rope_h, rope_P, rope_q_end, rope_k_end;
-  float rope_inv_h;  // 1/h in fp32
+  int head_h, rope_P, q_end, k_end;
+  float head_inv_h;  // 1/h in fp32
+  float q_scale;
   // EPI_HEADNORM: per-head norm weights [h] of Q, K and (optional, QKV-normalization) V,
-  // the heads' epsilon; rope_pos == nullptr turns the rotation off.
+  // and the heads' epsilon.
   const float* hn_gq;
   const float* hn_gk;
   const float* hn_gv;
   float hn_eps;
-  float rope_q_scale;
 };
 
 }  // namespace fn

@@ -96,10 +96,10 @@ __device__ __forceinline__ const float* epi_vec(const EpiArgs& ep) {
 // two; otherwise off by at most one for the column counts allowed, n < 2^24), then
 // one correction each way.
 __device__ __forceinline__ int rope_col_in_head(int n, const EpiArgs& ep) {
-  const int q = (int)((float)n * ep.rope_inv_h);
-  int r = n - q * ep.rope_h;
-  r += r < 0 ? ep.rope_h : 0;
-  r -= r >= ep.rope_h ? ep.rope_h : 0;
+  const int q = (int)((float)n * ep.head_inv_h);
+  int r = n - q * ep.head_h;
+  r += r < 0 ? ep.head_h : 0;
+  r -= r >= ep.head_h ? ep.head_h : 0;
   return r;
 }
 
@@ -113,7 +113,7 @@ struct RopeTab {
 __device__ __forceinline__ RopeTab rope_tab(int n, RowStat st, const EpiArgs& ep) {
   const bool valid = (unsigned)st.pos < (unsigned)ep.rope_P;
   const int j = rope_col_in_head(n, ep) >> 1;  // pair of column n (a valid index for V too)
-  const int64_t off = (int64_t)(valid ? st.pos : 0) * (ep.rope_h >> 1) + j;
+  const int64_t off = (int64_t)(valid ? st.pos : 0) * (ep.head_h >> 1) + j;
   const f32x2 c = *reinterpret_cast<const f32x2*>(ep.rope_cos + off);
   const f32x2 sn = *reinterpret_cast<const f32x2*>(ep.rope_sin + off);
   const float nan = __builtin_nanf("");
@@ -123,8 +123,8 @@ __device__ __forceinline__ RopeTab rope_tab(int n, RowStat st, const EpiArgs& ep
 template <bool VEC>
 __device__ __forceinline__ void rope_apply(int n, f32x4 v, f32x4 vec, RowStat st, RopeTab tb, const EpiArgs& ep,
                                            float (&o)[4]) {
-  const bool is_v = n >= ep.rope_k_end;
-  const float qs = n < ep.rope_q_end ? ep.rope_q_scale : 1.0f;
+  const bool is_v = n >= ep.k_end;
+  const float qs = n < ep.q_end ? ep.q_scale : 1.0f;
   float r[4];
   if constexpr (VEC) {
     float t[4];
@@ -158,11 +158,11 @@ __device__ __forceinline__ void rope4(int n, f32x4 v, f32x4 vec, RowStat st, con
 // pair partner w (column c ^ 1), with the per-column bias of each (0 without).
 __device__ __forceinline__ float rope1(int c, float v, float w, float bv, float bw, RowStat st, const EpiArgs& ep) {
   const float tv = fmaf(v, st.s, bv);
-  if (c >= ep.rope_k_end) return tv;
+  if (c >= ep.k_end) return tv;
   if ((unsigned)st.pos >= (unsigned)ep.rope_P) return __builtin_nanf("");
   const float tw = fmaf(w, st.s, bw);
-  const float qs = c < ep.rope_q_end ? ep.rope_q_scale : 1.0f;
-  const int64_t off = (int64_t)st.pos * (ep.rope_h >> 1) + (rope_col_in_head(c, ep) >> 1);
+  const float qs = c < ep.q_end ? ep.q_scale : 1.0f;
+  const int64_t off = (int64_t)st.pos * (ep.head_h >> 1) + (rope_col_in_head(c, ep) >> 1);
   const float cs = ep.rope_cos[off], sn = ep.rope_sin[off];
   return ((c & 1) ? tw * sn + tv * cs : tv * cs - tw * sn) * qs;
 }
@@ -202,14 +202,14 @@ __device__ __forceinline__ void headnorm8(int n, f32x4 a0, f32x4 a1, RowStat st,
                                           float (&o)[8]) {
   float ss = ((a0[0] * a0[0] + a0[1] * a0[1]) + (a0[2] * a0[2] + a0[3] * a0[3])) +
              ((a1[0] * a1[0] + a1[1] * a1[1]) + (a1[2] * a1[2] + a1[3] * a1[3]));
-  for (int off = 1; off < (ep.rope_h >> 3); off <<= 1) ss += __shfl_xor(ss, off);
+  for (int off = 1; off < (ep.head_h >> 3); off <<= 1) ss += __shfl_xor(ss, off);
 #pragma unroll
   for (int e = 0; e < 4; ++e) o[e] = a0[e], o[4 + e] = a1[e];
-  const bool is_q = n < ep.rope_q_end, is_k = !is_q && n < ep.rope_k_end;
+  const bool is_q = n < ep.q_end, is_k = !is_q && n < ep.k_end;
   const float* w = is_q ? ep.hn_gq : is_k ? ep.hn_gk : ep.hn_gv;
   const int c = rope_col_in_head(n, ep);
   if (w) {
-    const float sc = rsqrtf(fmaf(ss, ep.rope_inv_h, ep.hn_eps));
+    const float sc = rsqrtf(fmaf(ss, ep.head_inv_h, ep.hn_eps));
     const f32x4 w0 = *reinterpret_cast<const f32x4*>(w + c), w1 = *reinterpret_cast<const f32x4*>(w + c + 4);
 #pragma unroll
     for (int e = 0; e < 4; ++e) o[e] *= sc * w0[e], o[4 + e] *= sc * w1[e];
@@ -219,7 +219,7 @@ __device__ __forceinline__ void headnorm8(int n, f32x4 a0, f32x4 a1, RowStat st,
   }
   if ((is_q || is_k) && ep.rope_pos) {
     const bool valid = (unsigned)st.pos < (unsigned)ep.rope_P;
-    const int64_t off = (int64_t)(valid ? st.pos : 0) * (ep.rope_h >> 1) + (c >> 1);
+    const int64_t off = (int64_t)(valid ? st.pos : 0) * (ep.head_h >> 1) + (c >> 1);
     const f32x4 cs = *reinterpret_cast<const f32x4*>(ep.rope_cos + off);
     const f32x4 sn = *reinterpret_cast<const f32x4*>(ep.rope_sin + off);
 #pragma unroll
@@ -231,7 +231,7 @@ __device__ __forceinline__ void headnorm8(int n, f32x4 a0, f32x4 a1, RowStat st,
   }
   if (is_q) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] *= ep.rope_q_scale;
+    for (int e = 0; e < 8; ++e) o[e] *= ep.q_scale;
   }
 }
 

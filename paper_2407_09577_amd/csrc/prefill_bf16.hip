@@ -74,10 +74,10 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE + (kUneven ? kFragBytes : 0)];
   // Run-time g (GS), staged once: g[k] for k < K, zeros up to kGsMaxK + 64.
   __shared__ __attribute__((aligned(16))) float g_lds[GS ? kGsMaxK + 64 : 4];
-  // RoPE: each row's scale and token position, for the rotating copy-out.
+  // Fused QKV kinds: each row's scale and token position, for the staged copy-out.
   constexpr bool kRowLds = EPI == EPI_ROPE || EPI == EPI_HEADNORM;
-  __shared__ float rope_s[kRowLds ? BM : 1];
-  __shared__ int rope_p[kRowLds ? BM : 1];
+  __shared__ float row_s[kRowLds ? BM : 1];
+  __shared__ int row_pos[kRowLds ? BM : 1];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -414,17 +414,17 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   constexpr int OUT_COLS = epi_is_glu(EPI) ? BN / 2 : BN;  // output columns of a tile
   constexpr int UPR = OUT_COLS / 8;                       // 16-byte units per output row
   constexpr bool kStageable = OUT_COLS % 8 == 0 && stage_bytes<BM, UPR>() <= STAGES * STAGE;
-  // RoPE whole tiles: the fp32 accumulators are staged (in passes of RP rows when the
-  // tile does not fit the ring at once) and rotated on the way out (rope_copy_out).
+  // Fused QKV kinds: the fp32 accumulators are staged (in passes of RP rows when the
+  // tile does not fit the ring at once) and finished on the copy to HBM.
   constexpr int F32U = OUT_COLS / 4;                       // 16-byte fp32 units per row
   constexpr bool kF32Xor = F32U % 16 == 0;                 // else rows padded by one unit
   constexpr int F32_ROW = (kF32Xor ? F32U : F32U + 1) * 16;  // bytes per staged row
   constexpr int RP = (BM * F32_ROW <= STAGES * STAGE) ? BM : BM / 2;
-  constexpr bool kRopeF32 = (EPI == EPI_ROPE || EPI == EPI_HEADNORM) && OUT_COLS % 8 == 0 && RP % TM == 0 &&
+  constexpr bool kF32Stage = (EPI == EPI_ROPE || EPI == EPI_HEADNORM) && OUT_COLS % 8 == 0 && RP % TM == 0 &&
                             BM % RP == 0 && RP * F32_ROW <= STAGES * STAGE;
   // The per-head norms need whole heads in one tile and the fp32 staging: every tile
   // (also at the ragged edges, with guarded stores) takes the staged path.
-  static_assert(EPI != EPI_HEADNORM || (kRopeF32 && (RP * (OUT_COLS / 8)) % (NW * 64) == 0),
+  static_assert(EPI != EPI_HEADNORM || (kF32Stage && (RP * (OUT_COLS / 8)) % (NW * 64) == 0),
                 "per-head norms: fp32 staging and a uniform copy-out loop");
   const int n0 = epi_is_glu(EPI) ? p0 / 2 : p0;
   const int n_lane = (lane >> 4) * 4;
@@ -450,7 +450,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     row_stats(sts);
     wait_vmcnt<0>();  // the ring's last (zero-filling) transfers have landed
     __syncthreads();  // every wave is done with the ring and the row totals
-    if constexpr (kRopeF32) {
+    if constexpr (kF32Stage) {
       // Read in the matrix-core layout, a lane's 16 rows are 16 tokens, so every angle
       // load would touch 16 table rows.  Here the fp32 accumulators go through LDS
       // and the copy to HBM rotates them: a thread takes 8 consecutive columns of one
@@ -466,8 +466,8 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
             const int r = wm * TM + j * 16 + lrow - pass * RP;  // row within the pass
             write_inv_rms(j, sts[j]);
             if (wn == 0 && lane < 16) {
-              rope_s[r + pass * RP] = sts[j].s;
-              rope_p[r + pass * RP] = sts[j].pos;
+              row_s[r + pass * RP] = sts[j].s;
+              row_pos[r + pass * RP] = sts[j].pos;
             }
 #pragma unroll
             for (int i = 0; i < FN; ++i) {
@@ -481,7 +481,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         for (int q = threadIdx.x; q < RP * U8; q += NW * 64) {
           const int r = q / U8, v = q % U8;
           const int row = pass * RP + r;
-          const RowStat st{rope_s[row], 0.0f, rope_p[row]};
+          const RowStat st{row_s[row], 0.0f, row_pos[row]};
           float o[8];
           if constexpr (EPI == EPI_HEADNORM) {
             headnorm8(n0 + v * 8, *reinterpret_cast<const f32x4*>(smem + f32_pos(r, 2 * v) * 16),
@@ -667,7 +667,7 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   if constexpr (EPI == EPI_HEADNORM) {
     // Whole heads per tile: 256 columns, or 128 when that fills the chip better and
     // holds whole heads.
-    if (tile == TILE_256x256_W8_PF_SP || p.ep.rope_h > 128)
+    if (tile == TILE_256x256_W8_PF_SP || p.ep.head_h > 128)
       return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
     return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI>(p);
   } else if constexpr (EPI >= EPI_REGLU) {

@@ -728,3 +728,54 @@ def test_baseline_qkv_headnorm_chain(fn, with_gv):
     ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, Hq, Hkv, h, gq, gk, gv, 1e-6, pos=pos.numpy(),
                                       cos_tab=cos, sin_tab=sin, q_scale=0.125)
     assert row_err(to_np(y), ref) <= TOL[torch.bfloat16]
+
+
+# ------------------------------------------- seeded random shapes across the entry points
+def _random_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        M = int(rng.choice([1, 2, 7, 16, 17, 63, 129, 300, 513]))
+        K = int(rng.integers(1, 80)) * 8
+        yield M, K, rng
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_random_shapes_all_ops(fn, seed):
+    # Ragged M, K and N drawn from a fixed seed: each op against the oracle's standard form.
+    for M, K, rng in _random_cases(6, seed):
+        N = int(rng.integers(1, 100)) * 4
+        w = workloads.make("linear", M, K, N, eps=1e-5, seed=int(rng.integers(1 << 30)), outlier_frac=0.05)
+        a, W, gg = w.a.to(DEV), w.W.to(DEV), w.g.to(DEV)
+        Ws, _, _ = fn.fold_weights(W, gg)
+        Wp, _, _ = fn.fold_weights(W, None)
+        ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+        y1 = fn.flashnorm_linear(a, Ws, N, w.eps, out=padded_out(M, N, torch.bfloat16))
+        y2 = fn.flashnorm_linear_unfolded(a, gg, Wp, N, w.eps, out=padded_out(M, N, torch.bfloat16))
+        torch.cuda.synchronize()
+        assert row_err(to_np(y1), ref) <= TOL[torch.bfloat16], (M, K, N)
+        assert row_err(to_np(y2), ref) <= TOL[torch.bfloat16], (M, K, N)
+        F_ = int(rng.integers(1, 40)) * 4
+        gw = workloads.make("glu", M, K, F_, eps=1e-6, seed=int(rng.integers(1 << 30)))
+        Wg, _, _ = fn.fold_weights(gw.W.to(DEV), gw.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+        act = int(rng.integers(0, 3))
+        o = fn.flashnorm_glu_act(gw.a.to(DEV), Wg, F_, gw.eps, act, out=padded_out(M, F_, torch.bfloat16))
+        torch.cuda.synchronize()
+        assert row_err(to_np(o), oracle.rmsnorm_glu_act(gw.a, gw.g, gw.W, gw.eps, act)) <= TOL[torch.bfloat16], \
+            (M, K, F_, act)
+        h = int(rng.choice([8, 16, 32, 64]))
+        Hq, Hkv = int(rng.integers(1, 4)), int(rng.integers(0, 3))
+        Nq = (Hq + 2 * Hkv) * h
+        qw = workloads.make("linear", M, K, Nq, eps=1e-5, seed=int(rng.integers(1 << 30)))
+        Wq, _, _ = fn.fold_weights(qw.W.to(DEV), qw.g.to(DEV))
+        cos, sin = workloads.rope_tables(32, h)
+        pos = torch.from_numpy(rng.integers(0, 32, M).astype(np.int32))
+        yr = fn.flashnorm_qkv_rope(qw.a.to(DEV), Wq, Hq, Hkv, h, qw.eps, pos.to(DEV), cos.to(DEV), sin.to(DEV), 0.25)
+        gq, gk = (torch.from_numpy(rng.uniform(0.5, 1.5, h).astype(np.float32)) for _ in range(2))
+        yh = fn.flashnorm_qkv_headnorm(qw.a.to(DEV), Wq, Hq, Hkv, h, qw.eps, gq.to(DEV), gk.to(DEV), None, 1e-6,
+                                       positions=pos.to(DEV), cos_tab=cos.to(DEV), sin_tab=sin.to(DEV), q_scale=0.25)
+        torch.cuda.synchronize()
+        rr = oracle.rmsnorm_qkv_rope(qw.a, qw.g, qw.W, qw.eps, Hq, Hkv, h, pos.numpy(), cos, sin, 0.25)
+        rh = oracle.rmsnorm_qkv_headnorm(qw.a, qw.g, qw.W, qw.eps, Hq, Hkv, h, gq, gk, None, 1e-6, pos=pos.numpy(),
+                                         cos_tab=cos, sin_tab=sin, q_scale=0.25)
+        assert row_err(to_np(yr), rr) <= TOL[torch.bfloat16], (M, K, Hq, Hkv, h)
+        assert row_err(to_np(yh), rh) <= TOL[torch.bfloat16], (M, K, Hq, Hkv, h)
