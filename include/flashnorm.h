@@ -299,8 +299,9 @@ int baseline_layernorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, 
  *   positions  [M] int32 or NULL (no rotation); cos_tab, sin_tab, P as for
  *              flashnorm_qkv_rope (required with positions).
  *   inv_rms    optional [M] output of s_m.
- * bf16 only (fp32: FN_ERR_UNSUPPORTED); every M runs on the tile kernel (a
- * workgroup must hold whole heads); path as for flashnorm_glu_act. */
+ * bf16: every M runs on the tile kernel (a workgroup must hold whole heads).
+ * fp32: h <= 64 (the fp32 tile is 64 columns wide; FN_ERR_UNSUPPORTED beyond).
+ * path as for flashnorm_glu_act. */
 int flashnorm_qkv_headnorm(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
                            const void* W_star_qkv, int64_t Hq, int64_t Hkv, int64_t h, float eps,
                            const float* gq, const float* gk, const float* gv, float eps_head,

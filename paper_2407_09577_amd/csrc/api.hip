@@ -349,7 +349,7 @@ int flashnorm_qkv_headnorm(const void* a, int64_t M, int64_t K, int64_t lda, int
   d.ep.hn_eps = eps_head;
   int s = validate_op(d, y_dtype);
   if (s) return s;
-  if (a_dtype != FN_BF16) return FN_ERR_UNSUPPORTED;
+  if (a_dtype == FN_F32 && h > 64) return FN_ERR_UNSUPPORTED;  // the fp32 tile is 64 columns wide
   if ((s = check_auto_config(path))) return s;
   if (M == 0) return FN_OK;
   if (!gq || !gk) return FN_ERR_NULL;

@@ -109,6 +109,75 @@ __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, i
         yr[c] = rope1(c, acc[i][j], part[i][j], bv, bw, st, ep);
       }
     }
+  } else if constexpr (EPI == EPI_HEADNORM) {
+    // Heads of h | 64 columns: a lane holds columns tx + 16 j of its rows.  A head's
+    // squares are summed over its lanes (xor 1 .. min(h, 16) / 2) and, for h > 16, over
+    // the lane's h / 16 column groups of the head; pair partners sit in lane tx ^ 1.
+    // Every lane takes part in the exchanges before any guard.
+    const int h = ep.head_h;
+    float hs[4][4], part[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float v = acc[i][j] * acc[i][j];
+        for (int off = 1; off < (h < 16 ? h : 16); off <<= 1) v += __shfl_xor(v, off);
+        hs[i][j] = v;
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (h >= 32) {  // combine the column groups of one head: j and j ^ 1 (h = 32), all four (h = 64)
+        const float s01 = hs[i][0] + hs[i][1], s23 = hs[i][2] + hs[i][3];
+        hs[i][0] = hs[i][1] = h == 64 ? s01 + s23 : s01;
+        hs[i][2] = hs[i][3] = h == 64 ? s01 + s23 : s23;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + ty + 16 * i;
+      const RowStat st = row_stat_at<EPI>(row_ss[ty + 16 * i], row_sa[ty + 16 * i], ep, m, M);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c = p0 + tx + 16 * j;
+        const int ch = c & (h - 1);
+        const bool is_q = c < ep.q_end, is_k = !is_q && c < ep.k_end;
+        const float* w = is_q ? ep.hn_gq : is_k ? ep.hn_gk : ep.hn_gv;
+        float v = acc[i][j];
+        if (w && c < ncols) v *= rsqrtf(fmaf(hs[i][j], ep.head_inv_h, ep.hn_eps)) * w[ch];
+        else v *= st.s;
+        part[i][j] = v;  // the normalised value, also the partner of lane tx ^ 1
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) hs[i][j] = __shfl_xor(part[i][j], 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = ty + 16 * i;
+      const int m = m0 + r;
+      if (m >= M) continue;
+      const RowStat st = row_stat_at<EPI>(row_ss[r], row_sa[r], ep, m, M);
+      if (ep.inv_rms && blockIdx.x == 0 && tx == 0) ep.inv_rms[m] = st.s;
+      float* yr = y + (int64_t)m * ldy;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c = p0 + tx + 16 * j;
+        if (c >= ncols) continue;
+        const bool is_q = c < ep.q_end, is_k = !is_q && c < ep.k_end;
+        float v = part[i][j];
+        if ((is_q || is_k) && ep.rope_pos) {
+          if ((unsigned)st.pos < (unsigned)ep.rope_P) {
+            const int64_t off = (int64_t)st.pos * (ep.head_h >> 1) + ((c & (ep.head_h - 1)) >> 1);
+            const float cs = ep.rope_cos[off], sn = ep.rope_sin[off], w2 = hs[i][j];
+            v = (c & 1) ? w2 * sn + v * cs : v * cs - w2 * sn;
+          } else {
+            v = __builtin_nanf("");
+          }
+        }
+        yr[c] = is_q ? v * ep.q_scale : v;
+      }
+    }
   } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -167,6 +236,7 @@ hipError_t launch_f32(const F32Args& p) {
     case EPI_RELU_DEFER: return launch_f32_epi<EPI_RELU_DEFER>(p);
     case EPI_ROWSCALE: return launch_f32_epi<EPI_ROWSCALE>(p);
     case EPI_ROPE: return launch_f32_epi<EPI_ROPE>(p);
+    case EPI_HEADNORM: return launch_f32_epi<EPI_HEADNORM>(p);
   }
   return hipErrorInvalidValue;
 }

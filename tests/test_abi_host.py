@@ -233,9 +233,10 @@ def test_qkv_headnorm_validation(fnlib):
         return lib.flashnorm_qkv_headnorm(A, kw.get("M", 4), 64, 64, kw.get("dt", 1), W, 2, 1, kw.get("h", 8), 1e-6,
                                           kw.get("gq", G1), kw.get("gk", G2), kw.get("gv", None), kw.get("eh", 1e-6),
                                           kw.get("pos", Pz), kw.get("cos", T), kw.get("sin", S), 16, 0.5,
-                                          kw.get("y", Y), 32, kw.get("dt", 1), None, kw.get("path", 0), None)
+                                          kw.get("y", Y), kw.get("ldy", 32), kw.get("dt", 1), None, kw.get("path", 0),
+                                          None)
     assert hn(h=12) == -2 and hn(h=4) == -2        # head width: a power of two from 8 to 256
-    assert hn(dt=0) == -5                           # bf16 only
+    assert hn(dt=0, h=128, ldy=512) == -5           # fp32: heads up to 64 wide
     assert hn(eh=-1.0) == -6 and hn(eh=float("nan")) == -6
     assert hn(gq=0) == -1 and hn(gk=0) == -1
     assert hn(cos=0) == -1                          # positions need the tables

@@ -779,3 +779,24 @@ def test_random_shapes_all_ops(fn, seed):
                                          cos_tab=cos, sin_tab=sin, q_scale=0.25)
         assert row_err(to_np(yr), rr) <= TOL[torch.bfloat16], (M, K, Hq, Hkv, h)
         assert row_err(to_np(yh), rh) <= TOL[torch.bfloat16], (M, K, Hq, Hkv, h)
+
+
+@pytest.mark.parametrize("M,K,Hq,Hkv,h,with_gv,rope", [(37, 96, 2, 1, 16, True, True), (20, 64, 1, 1, 64, False, True),
+                                                       (9, 64, 3, 1, 8, False, False), (70, 128, 1, 2, 32, True, True)])
+def test_qkv_headnorm_fp32(fn, M, K, Hq, Hkv, h, with_gv, rope):
+    N = (Hq + 2 * Hkv) * h
+    w = workloads.make("linear", M, K, N, dtype=torch.float32, eps=1e-5, seed=171 + M + h)
+    g = torch.Generator().manual_seed(h)
+    gq, gk, gv = (torch.rand(h, generator=g) + 0.5 for _ in range(3))
+    gv = gv if with_gv else None
+    cos, sin = workloads.rope_tables(64, h)
+    pos = workloads.positions(M, 50)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), ws_dtype=fn.FN_F32)
+    kw = dict(positions=pos.to(DEV), cos_tab=cos.to(DEV), sin_tab=sin.to(DEV)) if rope else {}
+    y = fn.flashnorm_qkv_headnorm(w.a.to(DEV), Ws, Hq, Hkv, h, w.eps, gq.to(DEV), gk.to(DEV),
+                                  gv.to(DEV) if gv is not None else None, 0.0, q_scale=0.5,
+                                  out=padded_out(M, N, torch.float32, align=4), **kw)
+    torch.cuda.synchronize()
+    okw = dict(pos=pos.numpy(), cos_tab=cos, sin_tab=sin) if rope else {}
+    ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, Hq, Hkv, h, gq, gk, gv, 0.0, q_scale=0.5, **okw)
+    assert row_err(to_np(y), ref) <= TOL[torch.float32]
