@@ -800,3 +800,28 @@ def test_qkv_headnorm_fp32(fn, M, K, Hq, Hkv, h, with_gv, rope):
     okw = dict(pos=pos.numpy(), cos_tab=cos, sin_tab=sin) if rope else {}
     ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, Hq, Hkv, h, gq, gk, gv, 0.0, q_scale=0.5, **okw)
     assert row_err(to_np(y), ref) <= TOL[torch.float32]
+
+
+def test_concurrent_streams_match_serial(fn):
+    # The library keeps no mutable global state: calls on two streams that run
+    # concurrently give the bits of the same calls made one after the other.
+    lin = workloads.make("linear", 600, 576, 1536, eps=1e-5, seed=181)
+    dec = workloads.make("glu", 8, 2048, 512, eps=1e-6, seed=182)
+    Wl, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
+    Wg, _, _ = fn.fold_weights(dec.W.to(DEV), dec.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    al, ad = lin.a.to(DEV), dec.a.to(DEV)
+    ref_l = fn.flashnorm_linear(al, Wl, lin.N, lin.eps)
+    ref_g = fn.flashnorm_glu(ad, Wg, 512, dec.eps)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs_l = [torch.empty_like(ref_l) for _ in range(4)]
+    outs_g = [torch.empty_like(ref_g) for _ in range(4)]
+    for k in range(4):
+        with torch.cuda.stream(s1):
+            fn.flashnorm_linear(al, Wl, lin.N, lin.eps, out=outs_l[k], stream=s1)
+        with torch.cuda.stream(s2):
+            fn.flashnorm_glu(ad, Wg, 512, dec.eps, out=outs_g[k], stream=s2)
+    torch.cuda.synchronize()
+    for k in range(4):
+        assert torch.equal(outs_l[k].view(torch.int16), ref_l.view(torch.int16))
+        assert torch.equal(outs_g[k].view(torch.int16), ref_g.view(torch.int16))
