@@ -1,7 +1,7 @@
 // fp32 fused norm-then-project kernel (small fp32 problems; exact fp32 products,
 // no reduced-precision matrix-core modes).
 //
-// A 256-thread workgroup owns a 64 x 64 output tile and walks K in steps of 16,
+// A 256-thread workgroup owns a 64 x 64 output tile and walks K in steps of 64,
 // staging the activation and weight tiles in LDS.  The threads that stage an
 // activation row also accumulate its sum of squares (and sum, for LayerNorm)
 // from the values they just loaded, alongside the products (Cor. 1); the
@@ -19,7 +19,7 @@ __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, i
                                                   const float* __restrict__ ws, int NP, int KP,
                                                   int ncols, float* __restrict__ y, int ldy,
                                                   EpiArgs ep) {
-  constexpr int BM = 64, BN = 64, BK = 16;
+  constexpr int BM = 64, BN = 64, BK = 64, Q = BK / 16;  // Q quads of each operand per thread and step
   __shared__ float As[BK][BM + 4];
   __shared__ float Wsh[BK][BN];
   __shared__ float row_ss[BM], row_sa[BM];
@@ -28,41 +28,54 @@ __global__ __launch_bounds__(256) void f32_kernel(const float* __restrict__ a, i
   const int tx = t & 15, ty = t >> 4;
   const int m0 = blockIdx.y * BM, p0 = blockIdx.x * BN;
 
-  const int lr = t >> 2, lkq = (t & 3) * 4;       // activation staging: row, k quad
-  const int wk = t >> 4, wc = (t & 15) * 4;        // weight staging: k row, column quad
+  const int lr = t >> 2, lkq = (t & 3) * 4;       // activation staging: row, k quads lkq + 16 q
+  const int wk = t >> 4, wc = (t & 15) * 4;        // weight staging: k rows wk + 16 q, column quad
   const bool lr_ok = m0 + lr < M;
   const bool wc_ok = p0 + wc < NP;
 
   float acc[4][4] = {};
   float ss = 0.f, sa = 0.f;
   for (int k0 = 0; k0 < K; k0 += BK) {
-    float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (lr_ok && k0 + lkq < K)
-      av = *reinterpret_cast<const float4*>(a + (int64_t)(m0 + lr) * lda + k0 + lkq);
-    ss = fmaf(av.x, av.x, ss);
-    ss = fmaf(av.y, av.y, ss);
-    ss = fmaf(av.z, av.z, ss);
-    ss = fmaf(av.w, av.w, ss);
-    sa += (av.x + av.y) + (av.z + av.w);
-    if constexpr (GS) {  // run-time g (unfolded W): a_k g_k in fp32
-      if (lr_ok && k0 + lkq < K) {
-        const float4 gv = *reinterpret_cast<const float4*>(ep.g_rt + k0 + lkq);
-        av.x *= gv.x;
-        av.y *= gv.y;
-        av.z *= gv.z;
-        av.w *= gv.w;
+    // All of the step's loads first (K is a multiple of 4: a quad is wholly inside
+    // or outside; the packed weight has KP >= k0 + BK rows, zero past K).
+    float4 av[Q], wv[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int k = k0 + lkq + 16 * q;
+      av[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (lr_ok && k < K) av[q] = *reinterpret_cast<const float4*>(a + (int64_t)(m0 + lr) * lda + k);
+      wv[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (wc_ok) wv[q] = *reinterpret_cast<const float4*>(ws + (int64_t)(k0 + wk + 16 * q) * NP + p0 + wc);
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      ss = fmaf(av[q].x, av[q].x, ss);
+      ss = fmaf(av[q].y, av[q].y, ss);
+      ss = fmaf(av[q].z, av[q].z, ss);
+      ss = fmaf(av[q].w, av[q].w, ss);
+      sa += (av[q].x + av[q].y) + (av[q].z + av[q].w);
+      if constexpr (GS) {  // run-time g (unfolded W): a_k g_k in fp32
+        const int k = k0 + lkq + 16 * q;
+        if (lr_ok && k < K) {
+          const float4 gv = *reinterpret_cast<const float4*>(ep.g_rt + k);
+          av[q].x *= gv.x;
+          av[q].y *= gv.y;
+          av[q].z *= gv.z;
+          av[q].w *= gv.w;
+        }
       }
     }
-    float4 wv = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (wc_ok) wv = *reinterpret_cast<const float4*>(ws + (int64_t)(k0 + wk) * NP + p0 + wc);
-    __syncthreads();
-    As[lkq + 0][lr] = av.x;
-    As[lkq + 1][lr] = av.y;
-    As[lkq + 2][lr] = av.z;
-    As[lkq + 3][lr] = av.w;
-    *reinterpret_cast<float4*>(&Wsh[wk][wc]) = wv;
     __syncthreads();
 #pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      As[lkq + 16 * q + 0][lr] = av[q].x;
+      As[lkq + 16 * q + 1][lr] = av[q].y;
+      As[lkq + 16 * q + 2][lr] = av[q].z;
+      As[lkq + 16 * q + 3][lr] = av[q].w;
+      *reinterpret_cast<float4*>(&Wsh[wk + 16 * q][wc]) = wv[q];
+    }
+    __syncthreads();
+#pragma unroll 16
     for (int kk = 0; kk < BK; ++kk) {
       float ar[4], wr[4];
 #pragma unroll
