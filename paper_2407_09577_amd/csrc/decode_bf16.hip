@@ -211,26 +211,46 @@ static hipError_t launch_decode_cfg(const DecodeArgs& p) {
   return hipGetLastError();
 }
 
+// Automatic work split, from the number of packed 16-column blocks (npb) and
+// the row count.  Measured on MI355X (bf16, K = 576 .. 8192): about 600-1000
+// waves in flight over the chip stream the weights fastest, so narrow outputs
+// split K over more waves of one workgroup (combined in LDS in a fixed order)
+// instead of leaving most compute units idle:
+//   npb >= 1088          8 blocks x 2 waves x 2 per set (M <= 8), else 2 x 1 x 2
+//   544 <= npb < 1088    4 blocks x 4 waves x 1
+//   272 <= npb < 544     2 blocks x 4 waves x 2
+//   npb < 272            2 blocks x 8 waves x 1
+// With run-time g the wide case keeps 2 x 1 x 4 for M > 8 (the g loads want
+// four blocks per set).
+template <int EPI, bool GS>
+static hipError_t launch_decode_auto(const DecodeArgs& p) {
+  const int npb = p.NP / 16;
+  if (npb >= 1088) {
+    if (p.M <= 8) return launch_decode_cfg<8, 2, 2, EPI, true, kCachePolicyNT, GS>(p);
+    if constexpr (GS) return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT, GS>(p);
+    else return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT, GS>(p);
+  }
+  if (npb >= 544) return launch_decode_cfg<4, 4, 1, EPI, true, kCachePolicyNT, GS>(p);
+  if (npb >= 272) return launch_decode_cfg<2, 4, 2, EPI, true, kCachePolicyNT, GS>(p);
+  return launch_decode_cfg<2, 8, 1, EPI, true, kCachePolicyNT, GS>(p);
+}
+
 template <int EPI>
 static hipError_t launch_decode_epi(const DecodeArgs& p) {
-  if (p.gs) {  // run-time g: RMS kinds, the automatic configuration
-    // Four blocks per load set: measured on MI355X (Llama-7B SwiGLU decode) the
-    // fastest with the g loads added, ~5% behind the folded weight.
+  if (p.gs) {  // run-time g: RMS kinds, the automatic configuration only
     if constexpr (EPI == EPI_RMS || EPI == EPI_GLU)
-      if (p.cfg == 0 || p.cfg == 1) return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT, true>(p);
+      if (p.cfg == 0) return launch_decode_auto<EPI, true>(p);
     return hipErrorInvalidValue;
   }
+  if (p.cfg == 0) return launch_decode_auto<EPI, false>(p);
   if constexpr (EPI >= EPI_REGLU) {
     // The epilogue family beyond the core kinds: the automatic configuration only.
-    if (p.cfg == 0 || p.cfg == 1) return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT>(p);
     return hipErrorInvalidValue;
   } else {
-  // Configurations (NCB column blocks per workgroup, KSPLIT waves, U k blocks
-  // per load set, double-buffered sets, non-temporal weight loads).  Measured on
-  // MI355X (Llama-7B SwiGLU decode, 180 MB of weights): one wave per workgroup,
-  // two blocks per set, double buffered, non-temporal is the fastest for M = 1..16.
+  // Forced configurations (NCB column blocks per workgroup, KSPLIT waves, U k
+  // blocks per load set, double-buffered sets, non-temporal weight loads), for
+  // tuning and tests.
   switch (p.cfg) {
-    case 0:
     case 1: return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT>(p);
     case 2: return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT>(p);
     case 3: return launch_decode_cfg<2, 2, 2, EPI, true, kCachePolicyNT>(p);
@@ -243,6 +263,12 @@ static hipError_t launch_decode_epi(const DecodeArgs& p) {
     case 10: return launch_decode_cfg<2, 4, 4, EPI, true, kCachePolicyNT>(p);
     case 11: return launch_decode_cfg<8, 1, 2, EPI, true, kCachePolicyNT>(p);
     case 12: return launch_decode_cfg<2, 1, 1, EPI, true, kCachePolicyNT>(p);
+    case 13: return launch_decode_cfg<2, 4, 2, EPI, true, kCachePolicyNT>(p);
+    case 14: return launch_decode_cfg<8, 4, 1, EPI, true, kCachePolicyNT>(p);
+    case 15: return launch_decode_cfg<8, 2, 2, EPI, true, kCachePolicyNT>(p);
+    case 16: return launch_decode_cfg<2, 8, 2, EPI, true, kCachePolicyNT>(p);
+    case 17: return launch_decode_cfg<4, 4, 1, EPI, true, kCachePolicyNT>(p);
+    case 18: return launch_decode_cfg<2, 8, 1, EPI, true, kCachePolicyNT>(p);
   }
   return hipErrorInvalidValue;
   }

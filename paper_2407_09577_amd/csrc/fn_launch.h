@@ -76,7 +76,7 @@ struct DecodeArgs {
   bool gs;  // run-time g (ep.g_rt) applied to the activations; unfolded W
 };
 hipError_t launch_decode_bf16(const DecodeArgs& p);
-constexpr int kDecodeCfgCount = 13;
+constexpr int kDecodeCfgCount = 19;
 
 struct F32Args {
   const float* a;

@@ -287,7 +287,7 @@ def test_non_contiguous_activation_rows(fn):
 
 # ------------------------------------------------------------------ every kernel configuration
 PREFILL_TILES = list(range(1, 18))   # forced through the high byte of the path argument
-DECODE_CFGS = list(range(1, 13))
+DECODE_CFGS = list(range(1, 19))
 
 
 @pytest.mark.parametrize("tile", PREFILL_TILES)
@@ -327,6 +327,59 @@ def test_every_decode_config(fn, cfg, M):
     torch.cuda.synchronize()
     assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
     assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
+
+
+# The automatic decode split changes with the number of packed 16-column blocks
+# (npb < 272, 272..543, 544..1087, >= 1088; the widest case also with M <= 8 or
+# not): one output width per branch, for every kind the decode path runs.
+DECODE_WIDTHS = [96, 4400, 8800, 17424]          # npb 6, 275, 550, 1089 (GLU: F = N / 2)
+
+
+@pytest.mark.parametrize("N", DECODE_WIDTHS)
+@pytest.mark.parametrize("M", [1, 5, 16])
+@pytest.mark.parametrize("kind", ["linear", "glu", "layernorm", "reglu", "unfolded_linear", "unfolded_glu", "rope"])
+def test_decode_automatic_split(fn, kind, M, N):
+    K, seed = 200, 7 * M + N % 97
+    if kind == "rope":
+        h = 8
+        Hkv = N // (3 * h)
+        Hq = N // h - 2 * Hkv
+        w, y, _, (pos, cos, sin, qs, _) = _qkv_rope_case(fn, M, K, Hq, Hkv, h, torch.bfloat16, P=97, seq=61,
+                                                         seed=seed, path=0)
+        ref = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, Hq, Hkv, h, pos.numpy(), cos, sin, qs)
+        assert row_err(to_np(y), ref) <= TOL[torch.bfloat16]
+        return
+    glu = kind in ("glu", "reglu", "unfolded_glu")
+    w = workloads.make("glu" if glu else ("layernorm" if kind == "layernorm" else "linear"), M, K,
+                       N // 2 if glu else N, eps=1e-6, seed=seed)
+    a, W, g = w.a.to(DEV), w.W.to(DEV), w.g.to(DEV)
+    layout = fn.FN_LAYOUT_GLU if glu else fn.FN_LAYOUT_LINEAR
+    if kind == "linear":
+        Ws, _, _ = fn.fold_weights(W, g)
+        out = fn.flashnorm_linear(a, Ws, w.N, w.eps)
+        ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+    elif kind == "glu":
+        Ws, _, _ = fn.fold_weights(W, g, layout=layout)
+        out = fn.flashnorm_glu(a, Ws, w.out_features, w.eps)
+        ref = oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)
+    elif kind == "layernorm":
+        Ws, cs, cb = fn.fold_weights(W, g, beta=w.beta.to(DEV), colsum=True, c_star=True)
+        out = fn.flashnorm_layernorm_linear(a, Ws, cs, cb, w.N, w.eps)
+        ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps)
+    elif kind == "reglu":
+        Ws, _, _ = fn.fold_weights(W, g, layout=layout)
+        out = fn.flashnorm_glu_act(a, Ws, w.out_features, w.eps, fn.FN_GLU_REGLU)
+        ref = oracle.rmsnorm_glu_act(w.a, w.g, w.W, w.eps, oracle.GLU_REGLU)
+    elif kind == "unfolded_linear":
+        Wp, _, _ = fn.fold_weights(W, None)
+        out = fn.flashnorm_linear_unfolded(a, g, Wp, w.N, w.eps)
+        ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+    else:
+        Wp, _, _ = fn.fold_weights(W, None, layout=layout)
+        out = fn.flashnorm_glu_unfolded(a, g, Wp, w.out_features, w.eps)
+        ref = oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)
+    torch.cuda.synchronize()
+    assert row_err(to_np(out), ref) <= TOL[torch.bfloat16]
 
 
 def test_graph_replay_matches_eager(fn):
