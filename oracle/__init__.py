@@ -323,6 +323,49 @@ def qkv_headnorm_cancelled(a, g, W, eps, Hq, Hkv, h, gq, gk, gv, eps_head, pos=N
     return out
 
 
+def rmsnorm_mla_latent(a, g, W, eps, L, g_lat, eps_lat, pos=None, cos_tab=None, sin_tab=None,
+                       rows=None) -> np.ndarray:
+    """Standard form of the MLA down-projection with latent normalization (Sec. 3.3, the
+    paragraph on MLA): x = RMSNorm(a; g), t = x W with W = [W_lat | W_rope]; the first L
+    columns (the latent) are RMS-normalised over their whole width with weight g_lat:
+    t_lat / sqrt(eps_lat + mean(t_lat^2)) * g_lat; the remaining R columns (the shared
+    rotary key, one head of width R; R may be 0) are rotated by RoPE at each row's
+    position and carry no second norm."""
+    t = rmsnorm_linear(a, g, W, eps, rows=rows)
+    R = t.shape[1] - L
+    if L < 1 or R < 0 or R % 2:
+        raise ValueError("need 0 < L <= N and an even N - L")
+    out = t.copy()
+    out[:, :L] = _head_rmsnorm(t[:, :L], L, g_lat, eps_lat)
+    if R:
+        p = np.asarray(pos).ravel()
+        if rows is not None:
+            p = p[np.asarray(rows, dtype=np.int64)]
+        out[:, L:] = rope(t[:, L:], R, p, cos_tab, sin_tab)
+    return out
+
+
+def mla_latent_cancelled(a, g, W, eps, L, g_lat, eps_lat, pos=None, cos_tab=None, sin_tab=None,
+                         rows=None) -> np.ndarray:
+    """Prop. 3 form (Fig. 6(b)) of rmsnorm_mla_latent: the latent norm acts on z = a W*
+    (W* = diag(g) W) directly, the input RMSNorm dropped; the rotary columns, which no norm
+    follows, keep z / RMSe(a). Equal to the standard form when eps_lat = 0 (the epsilon
+    caveat otherwise). Self-check."""
+    a, g, W = _f64(a), _f64(g), _f64(W)
+    r, nr = _rows(rows, a.shape[0])
+    if r is None:
+        r = np.arange(nr)
+    a = a[r]
+    z = a @ (g[:, None] * W)
+    R = z.shape[1] - L
+    out = z.copy()
+    out[:, :L] = _head_rmsnorm(z[:, :L], L, g_lat, eps_lat)
+    if R:
+        s = np.array([1.0 / rms(row, _eps(eps)) for row in a])
+        out[:, L:] = rope(z[:, L:] * s[:, None], R, np.asarray(pos).ravel()[r], cos_tab, sin_tab)
+    return out
+
+
 def _ln_like(fn, a, g, beta, W, eps, bias, rows):
     a, g, beta, W, bias = _f64(a), _f64(g), _f64(beta), _f64(W), _f64(bias)
     M, K = a.shape

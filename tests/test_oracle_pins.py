@@ -614,3 +614,68 @@ def test_qkv_headnorm_matches_torch_and_cancellation(with_gv):
     scaled = oracle.rmsnorm_qkv_headnorm(7.0 * a, g, W, 0.0, Hq, Hkv, h, gq, gk, gv, 0.0, pos, cos, sin, qs)
     base = oracle.rmsnorm_qkv_headnorm(a, g, W, 0.0, Hq, Hkv, h, gq, gk, gv, 0.0, pos, cos, sin, qs)
     np.testing.assert_allclose(scaled[:, :qk], base[:, :qk], rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- MLA latent norm after the down-projection (Sec. 3.3)
+def test_mla_latent_exact_worked_example():
+    fx = _read_fixture("mla_latent_worked_example.txt")
+    L = int(fx["L"][0][0])
+    vec = lambda k: np.array([float(_frac(v)) for v in fx[k][0]])
+    mat = lambda k: np.array([[float(_frac(v)) for v in r] for r in fx[k]])
+    a, g, W, g_lat = vec("a")[None, :], vec("g"), mat("W"), vec("g_lat")
+    cos, sin = mat("cos"), mat("sin")
+    seen = set()
+    for eps_s, el_s, pos_s, form, *vals in fx["case"]:
+        eps, el, pos = float(_frac(eps_s)), float(_frac(el_s)), int(pos_s)
+        want = np.array([float(_frac(v)) for v in vals])
+        args = (a, g, W, eps, L, g_lat, el, [pos], cos, sin)
+        if form in ("std", "both"):
+            np.testing.assert_allclose(oracle.rmsnorm_mla_latent(*args)[0], want, rtol=1e-14, atol=1e-14)
+        if form in ("canc", "both"):
+            np.testing.assert_allclose(oracle.mla_latent_cancelled(*args)[0], want, rtol=1e-14, atol=1e-14)
+        seen.add(form)
+    assert seen == {"std", "canc", "both"}
+
+
+@pytest.mark.parametrize("L,R", [(16, 8), (24, 0), (64, 16)])
+def test_mla_latent_matches_torch_and_cancellation(L, R):
+    # The standard form rebuilt from torch rms_norm (input and latent), a matmul and complex
+    # rotation of the rotary key; Prop. 3 at eps_lat = 0 for any input eps; the epsilon
+    # caveat bounded for a small latent epsilon; the latent independent of the input scale
+    # and of unit RMS (before g_lat) without a latent epsilon.
+    M, K = 7, 40
+    a, g, W = _rand_case(M, K, L + R, 23 + L, neg_g=True)
+    rng = np.random.default_rng(24 + R)
+    g_lat = rng.uniform(0.5, 1.5, L)
+    P = 20
+    cos, sin = (t.double().numpy() for t in workloads.rope_tables(P, max(R, 2)))
+    pos = rng.integers(0, P, M)
+    eps, el = 1e-5, 1e-6
+    std = oracle.rmsnorm_mla_latent(a, g, W, eps, L, g_lat, el, pos, cos, sin)
+    x = F.rms_norm(torch.from_numpy(a), (K,), weight=torch.from_numpy(g), eps=float(np.float32(eps)))
+    t = (x @ torch.from_numpy(W)).numpy()
+    ref = t.copy()
+    ref[:, :L] = F.rms_norm(torch.from_numpy(t[:, :L]), (L,), weight=torch.from_numpy(g_lat),
+                            eps=float(np.float32(el))).numpy()
+    if R:
+        ref[:, L:] = _complex_rope(t[:, L:], R, pos, cos, sin)
+    np.testing.assert_allclose(std, ref, rtol=1e-12, atol=1e-13)
+    args = (a, g, W, eps, L, g_lat)
+    np.testing.assert_allclose(oracle.mla_latent_cancelled(*args, 0.0, pos, cos, sin),
+                               oracle.rmsnorm_mla_latent(*args, 0.0, pos, cos, sin), rtol=1e-12, atol=1e-13)
+    canc = oracle.mla_latent_cancelled(*args, el, pos, cos, sin)
+    assert 0 < np.max(np.abs(canc[:, :L] - std[:, :L])) < 1e-4 * np.max(np.abs(std[:, :L]))
+    np.testing.assert_allclose(canc[:, L:], std[:, L:], rtol=1e-12, atol=1e-13)
+    base = oracle.rmsnorm_mla_latent(a, g, W, 0.0, L, g_lat, 0.0, pos, cos, sin)
+    scaled = oracle.rmsnorm_mla_latent(7.0 * a, g, W, 0.0, L, g_lat, 0.0, pos, cos, sin)
+    np.testing.assert_allclose(scaled, base, rtol=1e-12, atol=1e-13)
+    unit = oracle.rmsnorm_mla_latent(a, g, W, eps, L, np.ones(L), 0.0, pos, cos, sin)[:, :L]
+    np.testing.assert_allclose(np.sqrt(np.mean(unit * unit, axis=1)), 1.0, rtol=1e-13)
+
+
+def test_mla_latent_position_outside_table():
+    a, g, W = _rand_case(3, 16, 12, 31)
+    cos, sin = (t.double().numpy() for t in workloads.rope_tables(4, 4))
+    y = oracle.rmsnorm_mla_latent(a, g, W, 1e-6, 8, np.ones(8), 1e-6, [0, 4, -1], cos, sin)
+    assert np.isfinite(y[:, :8]).all() and np.isfinite(y[0]).all()
+    assert np.isnan(y[1:, 8:]).all()
