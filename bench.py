@@ -42,13 +42,14 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="smollm2_prefill",
                    choices=["tiny_fp32", "smollm2_prefill", "llama7b_qkv_prefill", "llama7b_swiglu_decode",
-                            "layernorm_linear"])
+                            "layernorm_linear", "mla_kv_down"])
     p.add_argument("--decode-m", type=int, default=16, choices=[1, 4, 16])
-    p.add_argument("--variant", default="folded", choices=["folded", "unfolded", "qkv_rope", "qkv_headnorm"],
+    p.add_argument("--variant", default="folded", choices=["folded", "unfolded", "qkv_rope", "qkv_headnorm", "mla"],
                    help="folded: W* = diag(g) W folded offline (the default path); unfolded: g applied at "
                         "run time to an unfolded W (linear and GLU workloads); qkv_rope: the projection as "
                         "fused Q|K|V heads with RoPE on Q and K; qkv_headnorm: the same with QK-norm (per-head "
-                        "RMSNorm of Q and K, Prop. 3) before RoPE (linear workloads)")
+                        "RMSNorm of Q and K, Prop. 3) before RoPE (linear workloads); mla: the projection as an MLA "
+                        "latent (RMS-normalised, Prop. 3) plus a 64-wide rotary key (--workload mla_kv_down)")
     p.add_argument("--rope-h", type=int, default=0,
                    help="qkv_rope head width (default 128 for Llama-7B, else 64); Hq = Hkv = N / (3 h)")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -122,6 +123,22 @@ class Setup:
             self.hn_gk_cpu = torch.rand(h, generator=gen_hn) + 0.5
             self.hn_gq, self.hn_gk = self.hn_gq_cpu.to(dev), self.hn_gk_cpu.to(dev)
 
+        if variant == "mla":
+            if w.kind != "linear":
+                raise SystemExit("--variant mla covers the linear workloads")
+            R = rope_h or 64
+            if w.N <= R or (w.N - R) % 8 or w.N - R > 2048:
+                raise SystemExit(f"N = {w.N} is not a latent (multiple of 8, <= 2048) plus {R} rotary columns")
+            self.mla = (w.N - R, R)  # L, R
+            cos, sin = workloads.rope_tables(4096, R)
+            self.rope_cos, self.rope_sin = cos.to(dev), sin.to(dev)
+            self.rope_pos_cpu = workloads.positions(M, 2048)
+            self.rope_pos = self.rope_pos_cpu.to(dev)
+            gen_l = torch.Generator().manual_seed(2)
+            self.g_lat_cpu = torch.rand(w.N - R, generator=gen_l) + 0.5  # latent norm weight
+            self.g_lat = self.g_lat_cpu.to(dev)
+            self.mla_inv = torch.empty(M, dtype=torch.float32, device=dev)
+
     def run(self, i):
         fn, w = self.fn, self.w
         a, Ws, Wp, y, _ = self.sets[i % self.nsets]
@@ -139,6 +156,10 @@ class Setup:
             fn.flashnorm_qkv_headnorm(a, Ws, Hq, Hkv, h, w.eps, self.hn_gq, self.hn_gk, None, 1e-6,
                                       positions=self.rope_pos, cos_tab=self.rope_cos, sin_tab=self.rope_sin,
                                       q_scale=self.rope_qs, out=y)
+        elif self.variant == "mla":
+            L, R = self.mla
+            fn.flashnorm_mla_latent(a, Ws, L, R, self.g_lat, 1e-6, w.eps, self.rope_pos, self.rope_cos,
+                                    self.rope_sin, out=y, inv_rms=self.mla_inv)
         elif self.kind == "glu":
             fn.flashnorm_glu(a, Ws, self.ncols, w.eps, out=y)
         elif self.kind == "layernorm":
@@ -162,6 +183,9 @@ class Setup:
             Hq, Hkv, h = self.rope
             fn.baseline_qkv_headnorm(y, Hq, Hkv, h, self.hn_gq, self.hn_gk, None, 1e-6, self.rope_pos,
                                      self.rope_cos, self.rope_sin, self.rope_qs)
+        elif self.variant == "mla":
+            L, R = self.mla
+            fn.baseline_mla_latent(y, L, R, self.g_lat, 1e-6, self.rope_pos, self.rope_cos, self.rope_sin)
 
     def flops(self):
         return 2.0 * self.M * self.K * self.N
@@ -224,7 +248,11 @@ def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total, s=None):
         rope_args = (Hq, Hkv, h, s.rope_pos_cpu.numpy(), s.rope_cos.cpu(), s.rope_sin.cpu(), s.rope_qs)
 
     def call(rows):
-        if rope and s.variant == "qkv_headnorm":
+        if s is not None and s.variant == "mla":
+            L, R = s.mla
+            oracle.rmsnorm_mla_latent(a, g, W, w.eps, L, s.g_lat_cpu, 1e-6, s.rope_pos_cpu.numpy(), s.rope_cos.cpu(),
+                                      s.rope_sin.cpu(), rows=rows)
+        elif rope and s.variant == "qkv_headnorm":
             Hq, Hkv, h, pos, cos, sin, qs = rope_args
             oracle.rmsnorm_qkv_headnorm(a, g, W, w.eps, Hq, Hkv, h, s.hn_gq_cpu, s.hn_gk_cpu, None, 1e-6, pos=pos,
                                         cos_tab=cos, sin_tab=sin, q_scale=qs, rows=rows)
@@ -341,6 +369,11 @@ def main():
         Hq, Hkv, h = s.rope
         config.update(op="flashnorm_" + args.variant, heads={"Hq": Hq, "Hkv": Hkv, "h": h},
                       positions="sequences of 2048 tokens")
+    elif args.variant == "mla":
+        L, R = s.mla
+        config.update(op="flashnorm_mla_latent", mla={"L": L, "R": R, "eps_lat": 1e-6},
+                      positions="sequences of 2048 tokens",
+                      kernels_per_step="2 (fused projection, latent pass); roofline.achieved uses the whole step")
     if prof is not None:
         config["traffic_profile"] = prof["path"]
     if ms_unf is not None:

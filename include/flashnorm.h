@@ -309,6 +309,45 @@ int flashnorm_qkv_headnorm(const void* a, int64_t M, int64_t K, int64_t lda, int
                            int64_t P, float q_scale, void* y, int64_t ldy, int y_dtype,
                            float* inv_rms, int path, void* stream);
 
+/* MLA down-projection with latent normalization (Sec. 3.3, the paragraph on
+ * multi-head latent attention; Prop. 3, Fig. 6(b)).  W_star is the down-projection
+ * [W_lat | W_rope] folded with the input norm's g (fold_weights, linear layout,
+ * N = L + R columns).  With t = a W*, row m of y gets
+ *   y[m, 0:L)     = t / sqrt(eps_lat + mean(t^2)) * g_lat      (the latent RMSNorm)
+ *   y[m, L:L+R)   = RoPE(t * s_m) at positions[m]               (the rotary key)
+ * where s_m = 1/RMSe(a_m).  By Prop. 3 the input RMSNorm cancels in the normalised
+ * latent (exactly when eps_lat = 0; with eps_lat > 0 this is the cancelled form,
+ * which differs from input RMSNorm -> projection -> latent RMSNorm by the epsilon
+ * caveat of Sec. 3.3).  The rotary key is followed by no norm and keeps s_m; it is
+ * one head of width R, pairs (2j, 2j+1) turned by cos_tab/sin_tab [P][R/2] as in
+ * flashnorm_qkv_rope; a position outside [0, P) makes it NaN.  With R = 0 no
+ * statistics of a are taken at all: the input norm is gone.
+ *   L          latent width, a multiple of 8, 8 <= L <= 2048.
+ *   R          rotary width, a multiple of 8, 0 <= R <= 512.
+ *   g_lat      [L] fp32 latent norm weight (required), 16-byte aligned.
+ *   eps_lat    latent epsilon, >= 0 and finite; eps is the input norm's.
+ *   positions, cos_tab, sin_tab, P: required when R > 0 (16-byte aligned).
+ *   inv_rms    [M] fp32, required when R > 0: receives s_m, which the latent pass
+ *              reads; ignored (may be NULL) when R = 0.
+ *   y          [M, L + R], leading dimension ldy; dtype of a.
+ *   path       as for flashnorm_linear (it selects the projection's kernel).
+ * Two launches on the stream: the fused projection, then one wave per row for the
+ * latent norm and the rotation (in place in y). */
+int flashnorm_mla_latent(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                         const void* W_star, int64_t L, int64_t R, const float* g_lat, float eps_lat,
+                         float eps, const int32_t* positions, const float* cos_tab,
+                         const float* sin_tab, int64_t P, void* y, int64_t ldy, int y_dtype,
+                         float* inv_rms, int path, void* stream);
+
+/* Unfused baseline of the MLA latent stage (the standard form: input RMSNorm ->
+ * projection -> latent RMSNorm, rotary key rotated): applied in place to y [M, L + R]
+ * holding the projection of the normalised input; y[:, 0:L) becomes
+ * y / sqrt(eps_lat + mean(y^2)) * g_lat and y[:, L:L+R) is turned by RoPE.
+ * Arguments as for flashnorm_mla_latent.  Run after baseline_rmsnorm_linear. */
+int baseline_mla_latent(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t L, int64_t R,
+                        const float* g_lat, float eps_lat, const int32_t* positions,
+                        const float* cos_tab, const float* sin_tab, int64_t P, void* stream);
+
 /* Unfused baseline of flashnorm_qkv_rope's rotation (Fig. 5(a)): RoPE applied in
  * place to the first (Hq + Hkv) h columns of y (the Q and K heads of a QKV
  * projection output, leading dimension ldy), Q also times q_scale; arguments as

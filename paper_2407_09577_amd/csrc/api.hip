@@ -366,6 +366,53 @@ int flashnorm_qkv_headnorm(const void* a, int64_t M, int64_t K, int64_t lda, int
   return run_op(d);
 }
 
+// Arguments of the MLA latent pass over y [M, L + R] (latent, then rotary key).
+static int check_mla_pass(const void* y, int64_t M, int64_t ldy, int dtype, int64_t L, int64_t R,
+                          const float* g_lat, float eps_lat, const int32_t* positions, const float* cos_tab,
+                          const float* sin_tab, int64_t P, const float* s_row) {
+  if (L < 8 || L % 8 || L > 2048 || R < 0 || R % 8 || R > 512) return FN_ERR_SHAPE;
+  if (R > 0 && P < 1) return FN_ERR_SHAPE;
+  if (R > 0 && P > INT32_MAX / R) return FN_ERR_SIZE;
+  int s = check_eps(eps_lat);
+  if (s) return s;
+  if (M == 0) return FN_OK;
+  if (!g_lat || (R > 0 && (!positions || !cos_tab || !sin_tab))) return FN_ERR_NULL;
+  if (!aligned16(g_lat) || !aligned16(positions) || !aligned16(cos_tab) || !aligned16(sin_tab)) return FN_ERR_ALIGN;
+  const int64_t ybytes = extent_bytes(M, L + R, ldy, dtype), tbytes = P * (R / 2) * (int64_t)sizeof(float);
+  if (overlaps(y, ybytes, g_lat, L * (int64_t)sizeof(float)) ||
+      (s_row && overlaps(y, ybytes, s_row, M * (int64_t)sizeof(float))) ||
+      (R > 0 && (overlaps(y, ybytes, cos_tab, tbytes) || overlaps(y, ybytes, sin_tab, tbytes) ||
+                 overlaps(y, ybytes, positions, M * (int64_t)sizeof(int32_t)))))
+    return FN_ERR_ALIAS;
+  return FN_OK;
+}
+
+// MLA down-projection with latent normalization (Sec. 3.3; Prop. 3): the fused
+// projection (with the deferred scale when a rotary key needs it, none otherwise),
+// then the latent pass.
+int flashnorm_mla_latent(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const void* W_star,
+                         int64_t L, int64_t R, const float* g_lat, float eps_lat, float eps, const int32_t* positions,
+                         const float* cos_tab, const float* sin_tab, int64_t P, void* y, int64_t ldy, int y_dtype,
+                         float* inv_rms, int path, void* stream) {
+  if (L < 8 || R < 0 || L > kMaxRows || R > kMaxRows) return FN_ERR_SHAPE;
+  OpDesc d{a, M, K, lda, a_dtype, W_star, L + R, 0, y, ldy, R > 0 ? fn::EPI_RMS : fn::EPI_NONE, make_ep(eps, K),
+           path, (hipStream_t)stream};
+  d.ep.inv_rms = R > 0 ? inv_rms : nullptr;
+  int s = validate_op(d, y_dtype);
+  if (s) return s;
+  if ((s = check_mla_pass(y, M, ldy, a_dtype, L, R, g_lat, eps_lat, positions, cos_tab, sin_tab, P,
+                          R > 0 ? inv_rms : nullptr)))
+    return s;
+  if (M == 0) return FN_OK;
+  if (R > 0 && !inv_rms) return FN_ERR_NULL;
+  if ((s = run_op(d))) return s;
+  return fn::launch_mla_latent_rows(y, (int)M, (int)ldy, a_dtype, (int)L, (int)R, g_lat, eps_lat,
+                                    R > 0 ? inv_rms : nullptr, positions, cos_tab, sin_tab, (int)P,
+                                    (hipStream_t)stream) == hipSuccess
+             ? FN_OK
+             : FN_ERR_HIP;
+}
+
 // Run-time g (unfolded W): g must be given, 16-byte aligned; the bf16 tile path
 // stages g in LDS and takes K <= fn::kGsMaxK.
 static int check_runtime_g(const OpDesc& d, const float* g) {
@@ -469,6 +516,21 @@ int baseline_rope(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t Hq, int6
     return FN_ERR_ALIAS;
   return fn::launch_rope_rows(y, (int)M, (int)ldy, y_dtype, (int)qk, (int)(Hq * h), (int)h, positions, cos_tab,
                               sin_tab, (int)P, q_scale, (hipStream_t)stream) == hipSuccess
+             ? FN_OK
+             : FN_ERR_HIP;
+}
+
+int baseline_mla_latent(void* y, int64_t M, int64_t ldy, int y_dtype, int64_t L, int64_t R, const float* g_lat,
+                        float eps_lat, const int32_t* positions, const float* cos_tab, const float* sin_tab,
+                        int64_t P, void* stream) {
+  if (!dtype_ok(y_dtype)) return FN_ERR_DTYPE;
+  int s = check_matrix(y, M, L + R, ldy, y_dtype, true);
+  if (s) return s;
+  if ((s = check_mla_pass(y, M, ldy, y_dtype, L, R, g_lat, eps_lat, positions, cos_tab, sin_tab, P, nullptr)))
+    return s;
+  if (M == 0) return FN_OK;
+  return fn::launch_mla_latent_rows(y, (int)M, (int)ldy, y_dtype, (int)L, (int)R, g_lat, eps_lat, nullptr,
+                                    positions, cos_tab, sin_tab, (int)P, (hipStream_t)stream) == hipSuccess
              ? FN_OK
              : FN_ERR_HIP;
 }

@@ -123,4 +123,12 @@ hipError_t launch_headnorm_rows(void* y, int M, int ldy, int ncols, const EpiArg
 hipError_t launch_rope_rows(void* y, int M, int ldy, int dtype, int qk, int q_end, int h, const int* pos,
                             const float* cos_tab, const float* sin_tab, int P, float q_scale, hipStream_t stream);
 
+// MLA latent pass (Sec. 3.3): in place over y after the projection, the latent
+// RMSNorm of the first L columns (u * rsqrt(mean(u^2) + eps_lat s^2) * g_lat, s from
+// s_row or 1 without it) and RoPE of the R columns after them (one head of width R).
+// L % 8 == 0, L <= 2048; R % 8 == 0, R <= 512; y rows 16-byte aligned.
+hipError_t launch_mla_latent_rows(void* y, int M, int ldy, int dtype, int L, int R, const float* g_lat,
+                                  float eps_lat, const float* s_row, const int* pos, const float* cos_tab,
+                                  const float* sin_tab, int P, hipStream_t stream);
+
 }  // namespace fn

@@ -65,6 +65,8 @@ def _load():
         "baseline_qkv_headnorm": ([P, I64, I64, I, I64, I64, I64, P, P, P, F, P, P, P, I64, F, P], I),
         "flashnorm_qkv_headnorm": ([P, I64, I64, I64, I, P, I64, I64, I64, F, P, P, P, F, P, P, P, I64, F, P, I64,
                                     I, P, I, P], I),
+        "flashnorm_mla_latent": ([P, I64, I64, I64, I, P, I64, I64, P, F, F, P, P, P, I64, P, I64, I, P, I, P], I),
+        "baseline_mla_latent": ([P, I64, I64, I, I64, I64, P, F, P, P, P, I64, P], I),
         "flashnorm_linear_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P, I, P], I),
         "flashnorm_glu_unfolded": ([P, I64, I64, I64, I, P, P, I64, F, P, I64, I, I, P], I),
         "flashnorm_status_string": ([I], ctypes.c_char_p),
@@ -272,6 +274,48 @@ def baseline_rope(y: torch.Tensor, Hq: int, Hkv: int, h: int, positions: torch.T
         raise ValueError("positions must be a contiguous int32 tensor of M entries")
     _check(_load().baseline_rope(_ptr(y), M, _ld(y), _dt(y), Hq, Hkv, h, _ptr(positions), _ptr(cos_tab),
                                  _ptr(sin_tab), cos_tab.shape[0], q_scale, _stream(stream)), "baseline_rope")
+    return y
+
+
+def _rotary_args(M, R, positions, cos_tab, sin_tab):
+    if R == 0:
+        return None, None, None, 0
+    if positions is None or positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
+        raise ValueError("positions must be a contiguous int32 tensor of M entries")
+    for name, t in (("cos_tab", cos_tab), ("sin_tab", sin_tab)):
+        if t is None or t.dtype != torch.float32 or not t.is_contiguous() or t.dim() != 2 or t.shape[1] != R // 2:
+            raise ValueError(f"{name} must be a contiguous fp32 [P, R/2] tensor")
+    if cos_tab.shape != sin_tab.shape:
+        raise ValueError("cos_tab and sin_tab differ in shape")
+    return positions, cos_tab, sin_tab, cos_tab.shape[0]
+
+
+def flashnorm_mla_latent(a: torch.Tensor, W_packed: torch.Tensor, L: int, R: int, g_lat: torch.Tensor,
+                         eps_lat: float, eps: float, positions=None, cos_tab=None, sin_tab=None, out=None,
+                         inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
+    """MLA down-projection [latent | rotary key] with the latent RMSNorm (Prop. 3: the input
+    norm cancels in the latent) and RoPE on the R rotary columns."""
+    M, K = a.shape
+    y = out if out is not None else torch.empty(M, L + R, dtype=a.dtype, device=a.device)
+    pos, cos_t, sin_t, P_rows = _rotary_args(M, R, positions, cos_tab, sin_tab)
+    if R > 0 and inv_rms is None:
+        inv_rms = torch.empty(M, dtype=torch.float32, device=a.device)
+    _check(_load().flashnorm_mla_latent(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_packed), L, R,
+                                        _ptr(_vec(g_lat, L, "g_lat")), eps_lat, eps, _ptr(pos), _ptr(cos_t),
+                                        _ptr(sin_t), P_rows, _ptr(y), _ld(y), _dt(y),
+                                        _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
+           "flashnorm_mla_latent")
+    return y
+
+
+def baseline_mla_latent(y: torch.Tensor, L: int, R: int, g_lat: torch.Tensor, eps_lat: float, positions=None,
+                        cos_tab=None, sin_tab=None, stream=None) -> torch.Tensor:
+    """Unfused latent RMSNorm + rotary key RoPE on y = [latent | key], in place."""
+    M = y.shape[0]
+    pos, cos_t, sin_t, P_rows = _rotary_args(M, R, positions, cos_tab, sin_tab)
+    _check(_load().baseline_mla_latent(_ptr(y), M, _ld(y), _dt(y), L, R, _ptr(_vec(g_lat, L, "g_lat")), eps_lat,
+                                       _ptr(pos), _ptr(cos_t), _ptr(sin_t), P_rows, _stream(stream)),
+           "baseline_mla_latent")
     return y
 
 

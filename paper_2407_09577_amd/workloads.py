@@ -149,10 +149,18 @@ def layernorm_linear(seed: int = 0) -> Workload:
                 a_mean=0.5, name="layernorm_linear_4096x4096x4096")
 
 
+def mla_kv_down(seed: int = 0) -> Workload:
+    """MLA down-projection at DeepSeek-V2 width: bf16 a[4096,5120] ~ N(0,1), W[5120,576] ~ N(0,1/5120)
+    = a 512-wide latent and a 64-wide rotary key, g ~ U(0.5,1.5), eps 1e-6."""
+    return make(KIND_LINEAR, 4096, 5120, 576, dtype=torch.bfloat16, eps=1e-6, seed=seed,
+                name="mla_kv_down_4096x5120x(512+64)")
+
+
 WORKLOADS = {
     "tiny_fp32": tiny_fp32,
     "smollm2_prefill": smollm2_prefill,
     "llama7b_qkv_prefill": llama7b_qkv_prefill,
     "llama7b_swiglu_decode": llama7b_swiglu_decode,
     "layernorm_linear": layernorm_linear,
+    "mla_kv_down": mla_kv_down,
 }

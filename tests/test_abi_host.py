@@ -258,3 +258,33 @@ def test_baseline_qkv_headnorm_validation(fnlib):
     assert bh(ld=16) == -2                          # ldy below the normalised columns
     assert bh(gq=0) == -1 and bh(pos=Pz + 4) == -4
     assert bh(M=0, gq=0) == 0
+
+
+def test_mla_latent_validation(fnlib):
+    lib = fnlib.lib()
+    T, S, Pz, G = 0x500000, 0x600000, 0x700000, 0x800000   # tables, positions, g_lat (never dereferenced)
+
+    def ml(**kw):
+        return lib.flashnorm_mla_latent(A, kw.get("M", 4), 64, 64, kw.get("dt", 1), W, kw.get("L", 16),
+                                        kw.get("R", 8), kw.get("g", G), kw.get("el", 1e-6), 1e-6, kw.get("pos", Pz),
+                                        kw.get("cos", T), kw.get("sin", S), kw.get("P", 16), kw.get("y", Y), 32,
+                                        kw.get("dt", 1), kw.get("inv", X), kw.get("path", 0), None)
+    assert ml(L=12) == -2 and ml(L=0) == -2 and ml(L=2056) == -2   # latent: multiple of 8, <= 2048
+    assert ml(R=4) == -2 and ml(R=-8) == -2 and ml(R=520) == -2    # rotary: multiple of 8, <= 512
+    assert ml(P=0) == -2
+    assert ml(el=-1.0) == -6 and ml(el=float("nan")) == -6
+    assert ml(g=0) == -1 and ml(pos=0) == -1 and ml(cos=0) == -1 and ml(inv=0) == -1
+    assert ml(g=G + 4) == -4 and ml(cos=T + 8) == -4 and ml(pos=Pz + 4) == -4
+    assert ml(y=T) == -8                            # output overlaps a table
+    assert ml(y=G) == -8                            # output overlaps g_lat
+    assert ml(dt=7) == -3
+    assert ml(M=0, g=0, pos=0) == 0                 # M == 0: no-op
+    assert ml(R=0, P=0, M=0) == 0 and ml(R=8, P=0, M=0) == -2   # the tables matter only with a rotary part
+    bl = lambda **kw: lib.baseline_mla_latent(kw.get("y", Y), kw.get("M", 4), 32, kw.get("dt", 1), kw.get("L", 16),
+                                              kw.get("R", 8), kw.get("g", G), 1e-6, kw.get("pos", Pz), T, S,
+                                              kw.get("P", 16), None)
+    assert bl(L=10) == -2 and bl(R=6) == -2 and bl(L=32, R=8) == -2   # L + R wider than ldy
+    assert bl(g=0) == -1 and bl(pos=0) == -1
+    assert bl(y=Y + 4) == -4
+    assert bl(dt=5) == -3
+    assert bl(M=0) == 0

@@ -878,3 +878,104 @@ def test_concurrent_streams_match_serial(fn):
     for k in range(4):
         assert torch.equal(outs_l[k].view(torch.int16), ref_l.view(torch.int16))
         assert torch.equal(outs_g[k].view(torch.int16), ref_g.view(torch.int16))
+
+
+# ------------------------------------------- MLA down-projection with latent norm (Sec. 3.3)
+def _mla_case(fn, M, K, L, R, dtype, seed, path=0, P=97, seq=61, pos=None, g_lat=None, eps_lat=1e-6):
+    w = workloads.make("linear", M, K, L + R, dtype=dtype, eps=1e-5, seed=seed, outlier_frac=0.05)
+    gen = torch.Generator().manual_seed(seed + 1)
+    g_lat = torch.rand(L, generator=gen) + 0.5 if g_lat is None else g_lat
+    cos, sin = workloads.rope_tables(P, max(R, 2))
+    pos = workloads.positions(M, seq) if pos is None else pos
+    ws_dt = fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), ws_dtype=ws_dt)
+    inv = torch.empty(M, dtype=torch.float32, device=DEV)
+    kw = dict(positions=pos.to(DEV), cos_tab=cos.to(DEV), sin_tab=sin.to(DEV)) if R else {}
+    y = fn.flashnorm_mla_latent(w.a.to(DEV), Ws, L, R, g_lat.to(DEV), eps_lat, w.eps, inv_rms=inv, path=path,
+                                **kw)
+    torch.cuda.synchronize()
+    return w, y, inv, (g_lat, pos, cos, sin)
+
+
+@pytest.mark.parametrize("dtype,M,K,L,R,path", [(torch.bfloat16, 300, 328, 64, 16, 1),
+                                                (torch.bfloat16, 260, 1032, 512, 64, 0),
+                                                (torch.bfloat16, 200, 264, 1536, 0, 0),
+                                                (torch.bfloat16, 130, 136, 2048, 512, 0),
+                                                (torch.bfloat16, 5, 520, 512, 64, 0),
+                                                (torch.bfloat16, 16, 1032, 1536, 0, 2),
+                                                (torch.bfloat16, 1, 264, 8, 8, 0),
+                                                (torch.float32, 37, 96, 24, 8, 0),
+                                                (torch.float32, 6, 64, 16, 0, 0)])
+def test_mla_latent(fn, dtype, M, K, L, R, path):
+    w, y, inv, (g_lat, pos, cos, sin) = _mla_case(fn, M, K, L, R, dtype, seed=151 + M + L, path=path)
+    ref = oracle.mla_latent_cancelled(w.a, w.g, w.W, w.eps, L, g_lat, 1e-6, pos.numpy(), cos, sin)
+    assert row_err(to_np(y), ref) <= TOL[dtype]
+    # the latent alone too (its values are O(g_lat); the row metric above mixes in the key)
+    assert row_err(to_np(y)[:, :L], ref[:, :L]) <= TOL[dtype]
+    if R:
+        want = np.array([1.0 / oracle.rms(r, w.eps) for r in w.a.double().numpy()])
+        np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
+
+
+def test_mla_latent_standard_form_without_latent_eps(fn):
+    # eps_lat = 0: by Prop. 3 the cancelled form the kernels compute is the standard form
+    # (input RMSNorm -> projection -> latent RMSNorm) exactly.
+    M, K, L, R = 70, 520, 512, 64
+    w, y, _, (g_lat, pos, cos, sin) = _mla_case(fn, M, K, L, R, torch.bfloat16, seed=5, eps_lat=0.0)
+    ref = oracle.rmsnorm_mla_latent(w.a, w.g, w.W, w.eps, L, g_lat, 0.0, pos.numpy(), cos, sin)
+    assert row_err(to_np(y), ref) <= TOL[torch.bfloat16]
+
+
+def test_mla_latent_unit_rms_at_full_size(fn):
+    # DeepSeek-V2 width (K = 5120 -> 512 + 64) in the launch configuration the benchmark
+    # times: sampled rows against the oracle, and at every row the latent divided by g_lat
+    # has RMS 1 (eps_lat = 0) up to the bf16 rounding of the output.
+    w = workloads.mla_kv_down()
+    L, R = 512, 64
+    g_lat = torch.rand(L, generator=torch.Generator().manual_seed(2)) + 0.5
+    cos, sin = workloads.rope_tables(4096, R)
+    pos = workloads.positions(w.M, 2048)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    y = fn.flashnorm_mla_latent(w.a.to(DEV), Ws, L, R, g_lat.to(DEV), 0.0, w.eps, pos.to(DEV), cos.to(DEV),
+                                sin.to(DEV))
+    torch.cuda.synchronize()
+    rows = sample_rows(w.M, n=16)
+    ref = oracle.rmsnorm_mla_latent(w.a, w.g, w.W, w.eps, L, g_lat, 0.0, pos.numpy(), cos, sin, rows=rows)
+    got = to_np(y)
+    assert row_err(got[rows], ref) <= TOL[torch.bfloat16]
+    lat = got[:, :L] / g_lat.double().numpy()
+    np.testing.assert_allclose(np.sqrt(np.mean(lat * lat, axis=1)), 1.0, atol=4e-3)
+
+
+@pytest.mark.parametrize("dtype,M,path", [(torch.bfloat16, 40, 1), (torch.bfloat16, 3, 2), (torch.float32, 6, 0)])
+def test_mla_latent_position_outside_table(fn, dtype, M, path):
+    pos = workloads.positions(M, 5)
+    pos[1], pos[-1] = 8, -3                         # outside a table of 8 positions
+    L, R = 32, 16
+    w, y, _, (g_lat, pos, cos, sin) = _mla_case(fn, M, 64, L, R, dtype, seed=9, path=path, P=8, seq=5, pos=pos)
+    got = to_np(y)
+    bad = [1, M - 1]
+    assert np.isnan(got[bad, L:]).all()
+    assert np.isfinite(got[:, :L]).all() and np.isfinite(np.delete(got, bad, axis=0)).all()
+    ref = oracle.mla_latent_cancelled(w.a, w.g, w.W, w.eps, L, g_lat, 1e-6, pos.numpy(), cos, sin)
+    good = np.delete(np.arange(M), bad)
+    assert row_err(got[good], ref[good]) <= TOL[dtype]
+    assert row_err(got[:, :L], ref[:, :L]) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,M,L,R", [(torch.bfloat16, 300, 512, 64), (torch.bfloat16, 4, 1536, 0),
+                                         (torch.float32, 37, 64, 16)])
+def test_baseline_mla_latent_chain(fn, dtype, M, L, R):
+    # The unfused chain: normalisation kernel -> projection -> latent norm + rotation pass.
+    w = workloads.make("linear", M, 264, L + R, dtype=dtype, eps=1e-5, seed=57 + M)
+    g_lat = torch.rand(L, generator=torch.Generator().manual_seed(M)) + 0.5
+    cos, sin = workloads.rope_tables(97, max(R, 2))
+    pos = workloads.positions(M, 61)
+    ws_dt = fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32
+    Wp, _, _ = fn.fold_weights(w.W.to(DEV), None, ws_dtype=ws_dt)
+    y = fn.baseline_rmsnorm_linear(w.a.to(DEV), w.g.to(DEV), Wp, L + R, w.eps)
+    kw = dict(positions=pos.to(DEV), cos_tab=cos.to(DEV), sin_tab=sin.to(DEV)) if R else {}
+    fn.baseline_mla_latent(y, L, R, g_lat.to(DEV), 1e-6, **kw)
+    torch.cuda.synchronize()
+    ref = oracle.rmsnorm_mla_latent(w.a, w.g, w.W, w.eps, L, g_lat, 1e-6, pos.numpy(), cos, sin)
+    assert row_err(to_np(y), ref) <= TOL[dtype]
