@@ -40,7 +40,12 @@ __device__ __forceinline__ void wait_ahead(int ahead) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false>
+// KCHK: activation transfers check k < K lane by lane.  Only needed when K is
+// not a multiple of 64: otherwise every k of a block that is multiplied lies
+// below K, and the transfers of the blocks past the end (never multiplied) are
+// range-checked reads that stay inside the activation buffer or return zeros.
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false,
+          bool KCHK = true>
 __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep, int tiles_m, int tiles_n) {
@@ -124,22 +129,26 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   }
 
   // Transfer i of block kb into its ring slot.  Every wave issues exactly LOADS
-  // transfers per block, also for blocks past the end of K (they read as
-  // zeros), so the outstanding-transfer count of every step is the same.
-  // When the activation fragments split evenly over the waves, transfer i is an
-  // activation fragment exactly when i < A_FRAGS / NW (known at compile time).
+  // transfers per block, also for blocks past the end of K (their slots are
+  // never multiplied), so the outstanding-transfer count of every step is the
+  // same.  When the activation fragments split evenly over the waves, transfer i
+  // is an activation fragment exactly when i < A_FRAGS / NW (known at compile
+  // time).  The ring is addressed by 32-bit LDS offsets from one base, so a
+  // transfer costs one scalar add for its destination and one vector add for
+  // its source: weight offsets past the packed buffer read zeros, and the
+  // activations need a lane check only with KCHK.
   constexpr bool kSplitA = A_FRAGS % NW == 0;
+  const unsigned lds_ring = lds_addr(smem);
   auto load_one = [&](int kb, int i) __attribute__((always_inline)) {
-    char* st = smem + (kb % STAGES) * STAGE;
+    const unsigned st = lds_ring + (unsigned)((kb % STAGES) * STAGE);
     const int f = wave + NW * i;
     if (kSplitA ? i < A_FRAGS / NW : f < A_FRAGS) {
-      const bool ok = kb * kKB + lk < K;
-      load_lds16(rs_a, st + f * kFragBytes, ok ? off0[i] + kb * (kKB * 2) : kOobOffset);
+      const unsigned off = off0[i] + (unsigned)(kb * (kKB * 2));
+      load_lds16_at(rs_a, st + f * kFragBytes, (!KCHK || kb * kKB + lk < K) ? off : kOobOffset);
     } else if (!kUneven || f < T_FRAGS) {
-      load_lds16(rs_w, st + f * kFragBytes,
-                 kb < nkb ? off0[i] + (unsigned)(kb * npb) * kFragBytes : kOobOffset);
+      load_lds16_at(rs_w, st + f * kFragBytes, off0[i] + (unsigned)(kb * npb) * kFragBytes);
     } else {
-      load_lds16(rs_w, smem + STAGES * STAGE, kOobOffset);
+      load_lds16_at(rs_w, lds_ring + STAGES * STAGE, kOobOffset);
     }
   };
 
@@ -618,15 +627,33 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false>
+// LEAN: the automatically chosen tiles also have an instantiation without the
+// activation lane check (KCHK = false), launched when K is a multiple of 64.
+template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false,
+          bool LEAN = false>
 static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = (p.NP + BN - 1) / BN;
   const int nblocks = tiles_m * tiles_n;
-  hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI, SPREAD, GS>), dim3(nblocks),
-                     dim3(WM * WN * 64), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y,
-                     p.ldy, p.ep, tiles_m, tiles_n);
+  auto go = [&](auto kchk) {
+    hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI, SPREAD, GS, decltype(kchk)::value>),
+                       dim3(nblocks), dim3(WM * WN * 64), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP,
+                       p.ncols, p.y, p.ldy, p.ep, tiles_m, tiles_n);
+  };
+  if constexpr (LEAN) {
+    if (p.K % kKPad == 0) {
+      go(std::false_type{});
+      return hipGetLastError();
+    }
+  }
+  go(std::true_type{});
   return hipGetLastError();
+}
+
+// The automatically chosen configurations.
+template <int BM, int BN, int WM, int WN, int EPI, bool SPREAD = false, bool GS = false>
+static hipError_t launch_auto_cfg(const PrefillArgs& p) {
+  return launch_prefill_cfg<BM, BN, WM, WN, 4, true, EPI, SPREAD, GS, true>(p);
 }
 
 // Shape-specialised tile choice (measured on MI355X).  The 256 x 256 tile with 8
@@ -653,11 +680,11 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   if constexpr (EPI == EPI_RMS || EPI == EPI_GLU) {
     if (p.gs) {  // run-time g: the automatically chosen tiles only
       switch (tile) {
-        case TILE_256x256_W8_PF_SP: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true, true>(p);
-        case TILE_128x128_W8T: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, false, true>(p);
+        case TILE_256x256_W8_PF_SP: return launch_auto_cfg<256, 256, 2, 4, EPI, true, true>(p);
+        case TILE_128x128_W8T: return launch_auto_cfg<128, 128, 4, 2, EPI, false, true>(p);
         case TILE_128x96_W8:
-          if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, false, true>(p);
-          else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI, false, true>(p);
+          if constexpr (epi_is_glu(EPI)) return launch_auto_cfg<128, 128, 4, 2, EPI, false, true>(p);
+          else return launch_auto_cfg<128, 96, 4, 2, EPI, false, true>(p);
       }
       return hipErrorInvalidValue;
     }
@@ -668,17 +695,17 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
     // Whole heads per tile: 256 columns, or 128 when that fills the chip better and
     // holds whole heads.
     if (tile == TILE_256x256_W8_PF_SP || p.ep.head_h > 128)
-      return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
-    return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI>(p);
+      return launch_auto_cfg<256, 256, 2, 4, EPI, true>(p);
+    return launch_auto_cfg<128, 128, 4, 2, EPI>(p);
   } else if constexpr (EPI >= EPI_REGLU) {
     // The epilogue family beyond the core kinds is built for the automatically
     // chosen tiles only.
     switch (tile) {
-      case TILE_256x256_W8_PF_SP: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
-      case TILE_128x128_W8T: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI>(p);
+      case TILE_256x256_W8_PF_SP: return launch_auto_cfg<256, 256, 2, 4, EPI, true>(p);
+      case TILE_128x128_W8T: return launch_auto_cfg<128, 128, 4, 2, EPI>(p);
       case TILE_128x96_W8:
-        if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
-        else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI>(p);
+        if constexpr (epi_is_glu(EPI)) return launch_auto_cfg<128, 128, 2, 2, EPI>(p);
+        else return launch_auto_cfg<128, 96, 4, 2, EPI>(p);
     }
     return hipErrorInvalidValue;
   } else {
@@ -687,8 +714,8 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
     case TILE_128x128: return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
     case TILE_256x256_W8: return launch_prefill_cfg<256, 256, 2, 4, 4, false, EPI>(p);
     case TILE_128x96_W8:
-      if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
-      else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI>(p);
+      if constexpr (epi_is_glu(EPI)) return launch_auto_cfg<128, 128, 2, 2, EPI>(p);
+      else return launch_auto_cfg<128, 96, 4, 2, EPI>(p);
     case TILE_256x128: return launch_prefill_cfg<256, 128, 2, 2, 4, true, EPI>(p);
     case TILE_128x256: return launch_prefill_cfg<128, 256, 2, 2, 4, true, EPI>(p);
     case TILE_128x64: return launch_prefill_cfg<128, 64, 2, 2, 4, true, EPI>(p);
@@ -697,12 +724,12 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
     case TILE_256x256_W8_PF: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI>(p);
     case TILE_256x256_W8_PF5: return launch_prefill_cfg<256, 256, 2, 4, 5, true, EPI>(p);
     case TILE_128x128_W8: return launch_prefill_cfg<128, 128, 2, 4, 4, true, EPI>(p);
-    case TILE_128x128_W8T: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI>(p);
+    case TILE_128x128_W8T: return launch_auto_cfg<128, 128, 4, 2, EPI>(p);
     case TILE_128x96:
       // 48-column wave tiles cannot hold whole gate/up pairs: a GLU takes 128 x 128.
       if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
       else return launch_prefill_cfg<128, 96, 2, 2, 4, true, EPI>(p);
-    case TILE_256x256_W8_PF_SP: return launch_prefill_cfg<256, 256, 2, 4, 4, true, EPI, true>(p);
+    case TILE_256x256_W8_PF_SP: return launch_auto_cfg<256, 256, 2, 4, EPI, true>(p);
     case TILE_128x128_W8T_SP: return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, true>(p);
     case TILE_128x96_W8_SP:
       if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, true>(p);

@@ -285,6 +285,35 @@ def test_non_contiguous_activation_rows(fn):
     assert row_err(to_np(y), oracle.rmsnorm_linear(w.a[:12], w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
 
 
+@pytest.mark.parametrize("K", [192, 200, 576, 1032])
+def test_row_pitch_padding_never_enters(fn, K):
+    # The bytes between rows (lda > K) hold NaN.  With K a multiple of 64 the
+    # prefill transfers skip the per-lane k check, so this pins that no k >= K of
+    # a multiplied block is ever read; ragged K pins the check itself.
+    M, N, F = 300, 136, 48
+    pad = 64
+    lin = workloads.make("linear", M, K, N, eps=1e-5, seed=K)
+    glu = workloads.make("glu", M, K, F, eps=1e-5, seed=K + 1)
+    ln = workloads.make("layernorm", M, K, N, eps=1e-5, seed=K + 2, a_mean=0.5)
+
+    def padded(x):
+        big = torch.full((M, K + pad), float("nan"), dtype=torch.bfloat16)
+        big[:, :K] = x
+        return big.to(DEV)[:, :K]
+
+    Ws, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
+    Wg, _, _ = fn.fold_weights(glu.W.to(DEV), glu.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    Wl, cs, cb = fn.fold_weights(ln.W.to(DEV), ln.g.to(DEV), ln.beta.to(DEV), colsum=True, c_star=True)
+    for path in (0, fn.FN_PATH_PREFILL | (15 << 8), fn.FN_PATH_PREFILL | (4 << 8), fn.FN_PATH_PREFILL | (13 << 8)):
+        y = fn.flashnorm_linear(padded(lin.a), Ws, N, lin.eps, path=path)
+        o = fn.flashnorm_glu(padded(glu.a), Wg, F, glu.eps, path=path)
+        z = fn.flashnorm_layernorm_linear(padded(ln.a), Wl, cs, cb, N, ln.eps, path=path)
+        torch.cuda.synchronize()
+        assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
+        assert row_err(to_np(o), oracle.rmsnorm_swiglu(glu.a, glu.g, glu.W, glu.eps)) <= TOL[torch.bfloat16]
+        assert row_err(to_np(z), oracle.layernorm_linear(ln.a, ln.g, ln.beta, ln.W, ln.eps)) <= TOL[torch.bfloat16]
+
+
 # ------------------------------------------------------------------ every kernel configuration
 PREFILL_TILES = list(range(1, 18))   # forced through the high byte of the path argument
 DECODE_CFGS = list(range(1, 19))
