@@ -30,6 +30,8 @@ enum Tile : int {
   TILE_256x256_W8_PF_SP = 15,  // TILE_256x256_W8_PF, transfers spread over the k block
   TILE_128x128_W8T_SP = 16,    // TILE_128x128_W8T, transfers spread over the k block
   TILE_128x96_W8_SP = 17,      // TILE_128x96_W8, transfers spread over the k block
+  TILE_128x96_W8_K64 = 18,     // TILE_128x96_W8 with 64-deep ring steps (GLU: 128 x 128)
+  TILE_128x128_W8T_K64 = 19,   // TILE_128x128_W8T with 64-deep ring steps
   TILE_COUNT
 };
 

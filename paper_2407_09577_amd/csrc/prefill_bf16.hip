@@ -44,22 +44,28 @@ __device__ __forceinline__ void wait_ahead(int ahead) {
 // not a multiple of 64: otherwise every k of a block that is multiplied lies
 // below K, and the transfers of the blocks past the end (never multiplied) are
 // range-checked reads that stay inside the activation buffer or return zeros.
+// KD: 32-deep k fragments per ring step (1, or 2 for 64-deep steps: half the
+// barriers and waits per k; the accumulation order is unchanged).
 template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false,
-          bool KCHK = true>
+          bool KCHK = true, int KD = 1>
 __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep, int tiles_m, int tiles_n) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;  // wave sub-tile
   constexpr int FM = TM / 16, FN = TN / 16;  // fragments per wave along rows / columns
-  constexpr int A_FRAGS = BM / 16, W_FRAGS = BN / 16;  // per 32-deep k block
+  constexpr int A_RB = BM / 16, W_CB = BN / 16;     // row / column blocks of the tile
+  constexpr int A_FRAGS = A_RB * KD, W_FRAGS = W_CB * KD;  // per ring step (KD x 32 deep)
   constexpr int T_FRAGS = A_FRAGS + W_FRAGS;
   constexpr int A_BYTES = A_FRAGS * kFragBytes;
   constexpr int STAGE = T_FRAGS * kFragBytes;
   constexpr int LOADS = (T_FRAGS + NW - 1) / NW;     // loads per wave per stage
   constexpr bool kUneven = T_FRAGS % NW != 0;        // some waves pad with a dummy load
-  constexpr int NMF = FN * FM;                       // matrix-core ops per wave per k block
-  constexpr int NRD = FN + FM;                       // LDS fragment reads per wave per k block
+  constexpr int FMK = FM * KD, FNK = FN * KD;        // operand fragments per wave per step
+  constexpr int NMF = FN * FM * KD;                  // matrix-core ops per wave per step
+  constexpr int NRD = FNK + FMK;                     // LDS fragment reads per wave per step
+  static_assert(KD == 1 || (KD == 2 && !GS && FM % WN == 0),
+                "64-deep steps: no run-time g; each row block's statistics stay with one wave");
   static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be whole fragments");
   static_assert(!epi_is_glu(EPI) || TN % 32 == 0, "GLU needs whole gate/up block pairs per wave");
   static_assert(STAGES >= 3 && (STAGES - 2) * LOADS < 64, "ring depth / vmcnt range");
@@ -92,7 +98,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   tile_of_block(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM;
   const int p0 = tn * BN;
-  const int nkb = KP / kKB;  // k blocks (even: KP is a multiple of 64)
+  const int nkb = KP / (kKB * KD);  // ring steps (KP is a multiple of 64: even for KD = 1)
 
   // Range-checked views of this tile's activation rows and weight column blocks.
   const int rows_valid = min(BM, M - m0);
@@ -101,7 +107,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   const int cb0 = p0 / 16;
   const int npb = NP / 16;  // column blocks per k block of the packed weight
   const i32x4 rs_w = make_rsrc_sgpr(ws + (int64_t)cb0 * (kFragBytes / 2),
-                                    (uint32_t)(((int64_t)nkb * npb - cb0) * kFragBytes));
+                                    (uint32_t)(((int64_t)(KP / kKB) * npb - cb0) * kFragBytes));
 
   // Fragment f of a stage: f < A_FRAGS is activation row block f, otherwise weight
   // column block f - A_FRAGS.  Wave w moves fragments w, w + NW, ...
@@ -118,14 +124,21 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // Weight column blocks past the packed width (last column tile only) read the
   // next k block's fragments, or zeros past the buffer's end; the columns they
   // feed lie beyond every output column and are never stored.
+  // With KD = 2, fragment f covers k half f / A_RB (activations) or
+  // (f - A_FRAGS) / W_CB (weights) of the 64-deep step.
   unsigned off0[LOADS];
+  int lkh[LOADS];  // k offset of this lane's activation chunk within the step
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
     const int f = wave + NW * i;
-    if (A_FRAGS % NW == 0 ? i < A_FRAGS / NW : f < A_FRAGS)
-      off0[i] = (unsigned)((f * 16 + t_row) * lda * 2 + lk * 2);
-    else
-      off0[i] = (unsigned)((f - A_FRAGS) * kFragBytes + lane * 16);
+    if (A_FRAGS % NW == 0 ? i < A_FRAGS / NW : f < A_FRAGS) {
+      lkh[i] = (f / A_RB) * kKB + lk;
+      off0[i] = (unsigned)(((f % A_RB) * 16 + t_row) * lda * 2 + lkh[i] * 2);
+    } else {
+      const int wf = f - A_FRAGS;
+      lkh[i] = 0;
+      off0[i] = (unsigned)(((wf / W_CB) * npb + wf % W_CB) * kFragBytes + lane * 16);
+    }
   }
 
   // Transfer i of block kb into its ring slot.  Every wave issues exactly LOADS
@@ -143,10 +156,10 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     const unsigned st = lds_ring + (unsigned)((kb % STAGES) * STAGE);
     const int f = wave + NW * i;
     if (kSplitA ? i < A_FRAGS / NW : f < A_FRAGS) {
-      const unsigned off = off0[i] + (unsigned)(kb * (kKB * 2));
-      load_lds16_at(rs_a, st + f * kFragBytes, (!KCHK || kb * kKB + lk < K) ? off : kOobOffset);
+      const unsigned off = off0[i] + (unsigned)(kb * (KD * kKB * 2));
+      load_lds16_at(rs_a, st + f * kFragBytes, (!KCHK || kb * (KD * kKB) + lkh[i] < K) ? off : kOobOffset);
     } else if (!kUneven || f < T_FRAGS) {
-      load_lds16_at(rs_w, st + f * kFragBytes, off0[i] + (unsigned)(kb * npb) * kFragBytes);
+      load_lds16_at(rs_w, st + f * kFragBytes, off0[i] + (unsigned)(kb * KD * npb) * kFragBytes);
     } else {
       load_lds16_at(rs_w, lds_ring + STAGES * STAGE, kOobOffset);
     }
@@ -161,23 +174,28 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 #pragma unroll
   for (int j = 0; j < FM; ++j) ss[j] = sa[j] = 0.f;
 
-  bf16x8 af0[FM], wf0[FN];
-  bf16x8 af1[PF ? FM : 1], wf1[PF ? FN : 1];
+  bf16x8 af0[FMK], wf0[FNK];
+  bf16x8 af1[PF ? FMK : 1], wf1[PF ? FNK : 1];
 
-  // Fragment r of block kb (r < FM: activations, else weights) into registers.
-  auto read_one = [&](int kb, int r, bf16x8 (&af)[FM], bf16x8 (&wf)[FN]) __attribute__((always_inline)) {
+  // Fragment r of step kb (r < FMK: activations, else weights; k half r / FM or
+  // (r - FMK) / FN) into registers.
+  auto read_one = [&](int kb, int r, bf16x8 (&af)[FMK], bf16x8 (&wf)[FNK]) __attribute__((always_inline)) {
     const char* st = smem + (kb % STAGES) * STAGE;
-    if (r < FM)
-      af[r] = *reinterpret_cast<const bf16x8*>(st + (wm * FM + r) * kFragBytes + a_rd);
-    else
-      wf[r - FM] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + (wn * FN + r - FM) * kFragBytes + lane * 16);
+    if (r < FMK) {
+      af[r] = *reinterpret_cast<const bf16x8*>(st + ((r / FM) * A_RB + wm * FM + r % FM) * kFragBytes + a_rd);
+    } else {
+      const int q = r - FMK;
+      wf[q] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + ((q / FN) * W_CB + wn * FN + q % FN) * kFragBytes +
+                                               lane * 16);
+    }
   };
 
-  // Row statistics of fragment j: squares (and sums, for LayerNorm) of its 8
-  // elements per lane, as packed bf16 dot products accumulated in fp32.
-  auto stats_one = [&](int j, const bf16x8 (&af)[FM]) __attribute__((always_inline)) {
-    if constexpr (kSS) ss[j] = sumsq8(af[j], ss[j]);
-    if constexpr (kSA) sa[j] = sum8(af[j], sa[j]);
+  // Row statistics of fragment j (row block j % FM): squares (and sums, for
+  // LayerNorm) of its 8 elements per lane, as packed bf16 dot products
+  // accumulated in fp32.
+  auto stats_one = [&](int j, const bf16x8 (&af)[FMK]) __attribute__((always_inline)) {
+    if constexpr (kSS) ss[j % FM] = sumsq8(af[j], ss[j % FM]);
+    if constexpr (kSA) sa[j % FM] = sum8(af[j], sa[j % FM]);
   };
 
   // GS: scale the activation fragments of block b in place, g applied per k
@@ -241,21 +259,21 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // block (PF) and, spread over the block, transfer i of block kb+STAGES.  The
   // scheduling fences keep this interleaving, so memory traffic overlaps the
   // matrix cores.
-  auto multiply_interleaved = [&](auto wnc, int kb, const bf16x8 (&afc)[FM], const bf16x8 (&wfc)[FN],
-                                  bf16x8 (&afn)[FM], bf16x8 (&wfn)[FN], bool more, bool scale = false)
+  auto multiply_interleaved = [&](auto wnc, int kb, const bf16x8 (&afc)[FMK], const bf16x8 (&wfc)[FNK],
+                                  bf16x8 (&afn)[FMK], bf16x8 (&wfn)[FNK], bool more, bool scale = false)
                                   __attribute__((always_inline)) {
     constexpr int WNC = decltype(wnc)::value;
     if constexpr (!GS) {
 #pragma unroll
-      for (int j = WNC; j < FM; j += WN) stats_one(j, afc);
+      for (int j = WNC; j < FMK; j += WN) stats_one(j, afc);
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int g = 0; g < NRD; ++g) {
 #pragma unroll
       for (int t = g * NMF / NRD; t < (g + 1) * NMF / NRD; ++t) {
-        const int i = t / FM, j = t % FM;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wfc[i], afc[j], acc[i][j], 0, 0, 0);
+        const int h = t / (FN * FM), i = t % (FN * FM) / FM, j = t % FM;  // k half, column, row
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wfc[h * FN + i], afc[h * FM + j], acc[i][j], 0, 0, 0);
       }
       // GS: fragment t of the block being scaled is finished in group t + 1.
       if constexpr (GS) {
@@ -322,11 +340,23 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         scale_fetch(kb + 3);
         multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true, true);
       }
-      wait_vmcnt<kAheadWait>();
-      sync_block();
-      multiply_interleaved(wnc, nkb - 2, af0, wf0, af1, wf1, true);
-      __builtin_amdgcn_s_waitcnt(0xc07f);
-      multiply_interleaved(wnc, nkb - 1, af1, wf1, af0, wf0, false);
+      auto tail_even = [&]() __attribute__((always_inline)) {
+        wait_vmcnt<kAheadWait>();
+        sync_block();
+        multiply_interleaved(wnc, nkb - 2, af0, wf0, af1, wf1, true);
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        multiply_interleaved(wnc, nkb - 1, af1, wf1, af0, wf0, false);
+      };
+      if constexpr (KD == 1) {
+        tail_even();  // nkb is even
+      } else if (nkb % 2 == 0) {
+        tail_even();
+      } else {
+        // Odd step count: the loop (or, for one step, the prologue) has read the
+        // last step into af0.
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        multiply_interleaved(wnc, nkb - 1, af0, wf0, af1, wf1, false);
+      }
     } else {
       for (int kb = 0; kb < nkb; ++kb) {
         wait_vmcnt<(STAGES - 2) * LOADS>();
@@ -336,11 +366,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 #pragma unroll
         for (int r = 0; r < NRD; ++r) read_one(kb, r, af0, wf0);
 #pragma unroll
-        for (int j = WNC; j < FM; j += WN) stats_one(j, af0);
+        for (int j = WNC; j < FMK; j += WN) stats_one(j, af0);
 #pragma unroll
-        for (int t = 0; t < NMF; ++t)
-          acc[t / FM][t % FM] =
-              __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[t / FM], af0[t % FM], acc[t / FM][t % FM], 0, 0, 0);
+        for (int t = 0; t < NMF; ++t) {
+          const int h = t / (FN * FM), i = t % (FN * FM) / FM, j = t % FM;
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[h * FN + i], af0[h * FM + j], acc[i][j], 0, 0, 0);
+        }
       }
     }
   };
@@ -630,13 +661,13 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 // LEAN: the automatically chosen tiles also have an instantiation without the
 // activation lane check (KCHK = false), launched when K is a multiple of 64.
 template <int BM, int BN, int WM, int WN, int STAGES, bool PF, int EPI, bool SPREAD = false, bool GS = false,
-          bool LEAN = false>
+          bool LEAN = false, int KD = 1>
 static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = (p.NP + BN - 1) / BN;
   const int nblocks = tiles_m * tiles_n;
   auto go = [&](auto kchk) {
-    hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI, SPREAD, GS, decltype(kchk)::value>),
+    hipLaunchKernelGGL((prefill_bf16_kernel<BM, BN, WM, WN, STAGES, PF, EPI, SPREAD, GS, decltype(kchk)::value, KD>),
                        dim3(nblocks), dim3(WM * WN * 64), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP,
                        p.ncols, p.y, p.ldy, p.ep, tiles_m, tiles_n);
   };
@@ -651,9 +682,9 @@ static hipError_t launch_prefill_cfg(const PrefillArgs& p) {
 }
 
 // The automatically chosen configurations.
-template <int BM, int BN, int WM, int WN, int EPI, bool SPREAD = false, bool GS = false>
+template <int BM, int BN, int WM, int WN, int EPI, bool SPREAD = false, bool GS = false, int KD = 1>
 static hipError_t launch_auto_cfg(const PrefillArgs& p) {
-  return launch_prefill_cfg<BM, BN, WM, WN, 4, true, EPI, SPREAD, GS, true>(p);
+  return launch_prefill_cfg<BM, BN, WM, WN, 4, true, EPI, SPREAD, GS, true, KD>(p);
 }
 
 // Shape-specialised tile choice (measured on MI355X).  The 256 x 256 tile with 8
@@ -673,10 +704,24 @@ static int auto_tile(int M, int NP, bool glu) {
   return t96 * r128 > t128 * r96 ? TILE_128x96_W8 : TILE_128x128_W8T;
 }
 
+// 64-deep ring steps on the 128-row tiles, for the core non-GLU kinds with long
+// K.  Measured on MI355X (one interleaved run): 2048 x 4096 -> 1024 -2.3%,
+// 1024 x 4096 -> 4096 -4%, 4096 x 5120 -> 576 -1.6%; at K = 576 within +-1%
+// (128 x 96) or slower (128 x 128 +1%, and a GLU +13%).
+constexpr int kK64MinK = 2048;
+
 template <int EPI>
 static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   int tile = p.tile;
-  if (tile == TILE_AUTO) tile = auto_tile(p.M, p.NP, epi_is_glu(EPI));
+  if (tile == TILE_AUTO) {
+    tile = auto_tile(p.M, p.NP, epi_is_glu(EPI));
+    if constexpr (EPI == EPI_RMS || EPI == EPI_LN || EPI == EPI_NONE) {
+      if (!p.gs && p.K >= kK64MinK) {
+        if (tile == TILE_128x96_W8) tile = TILE_128x96_W8_K64;
+        else if (tile == TILE_128x128_W8T) tile = TILE_128x128_W8T_K64;
+      }
+    }
+  }
   if constexpr (EPI == EPI_RMS || EPI == EPI_GLU) {
     if (p.gs) {  // run-time g: the automatically chosen tiles only
       switch (tile) {
@@ -734,6 +779,10 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
     case TILE_128x96_W8_SP:
       if constexpr (epi_is_glu(EPI)) return launch_prefill_cfg<128, 128, 4, 2, 4, true, EPI, true>(p);
       else return launch_prefill_cfg<128, 96, 4, 2, 4, true, EPI, true>(p);
+    case TILE_128x96_W8_K64:
+      if constexpr (epi_is_glu(EPI)) return launch_auto_cfg<128, 128, 4, 2, EPI, false, false, 2>(p);
+      else return launch_auto_cfg<128, 96, 4, 2, EPI, false, false, 2>(p);
+    case TILE_128x128_W8T_K64: return launch_auto_cfg<128, 128, 4, 2, EPI, false, false, 2>(p);
   }
   return hipErrorInvalidValue;
   }

@@ -285,6 +285,25 @@ def test_non_contiguous_activation_rows(fn):
     assert row_err(to_np(y), oracle.rmsnorm_linear(w.a[:12], w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
 
 
+@pytest.mark.parametrize("K", [2048, 2088, 2112])
+def test_long_k_automatic_64_deep_steps(fn, K):
+    # K >= 2048 on the 128-row tiles takes 64-deep ring steps automatically:
+    # 32 (even) steps, 33 (odd) with the lane check (2088) and without it (2112).
+    M, N = 260, 200
+    lin = workloads.make("linear", M, K, N, eps=1e-5, seed=K, outlier_frac=0.05)
+    ln = workloads.make("layernorm", M, K, N, eps=1e-5, seed=K + 1, a_mean=0.5)
+    Ws, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
+    Wl, cs, cb = fn.fold_weights(ln.W.to(DEV), ln.g.to(DEV), ln.beta.to(DEV), colsum=True, c_star=True)
+    y = fn.flashnorm_linear(lin.a.to(DEV), Ws, N, lin.eps)
+    z = fn.flashnorm_layernorm_linear(ln.a.to(DEV), Wl, cs, cb, N, ln.eps)
+    y32 = fn.flashnorm_linear(lin.a.to(DEV), Ws, N, lin.eps, path=fn.FN_PATH_PREFILL | (4 << 8))
+    torch.cuda.synchronize()
+    assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
+    assert row_err(to_np(z), oracle.layernorm_linear(ln.a, ln.g, ln.beta, ln.W, ln.eps)) <= TOL[torch.bfloat16]
+    # same accumulation order as the 32-deep steps: identical bits
+    assert torch.equal(y.cpu().view(torch.int16), y32.cpu().view(torch.int16))
+
+
 @pytest.mark.parametrize("K", [192, 200, 576, 1032])
 def test_row_pitch_padding_never_enters(fn, K):
     # The bytes between rows (lda > K) hold NaN.  With K a multiple of 64 the
@@ -315,7 +334,7 @@ def test_row_pitch_padding_never_enters(fn, K):
 
 
 # ------------------------------------------------------------------ every kernel configuration
-PREFILL_TILES = list(range(1, 18))   # forced through the high byte of the path argument
+PREFILL_TILES = list(range(1, 20))   # forced through the high byte of the path argument
 DECODE_CFGS = list(range(1, 19))
 
 
