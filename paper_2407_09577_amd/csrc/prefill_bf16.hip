@@ -704,11 +704,13 @@ static int auto_tile(int M, int NP, bool glu) {
   return t96 * r128 > t128 * r96 ? TILE_128x96_W8 : TILE_128x128_W8T;
 }
 
-// 64-deep ring steps on the 128-row tiles, for the core non-GLU kinds with long
-// K.  Measured on MI355X (one interleaved run): 2048 x 4096 -> 1024 -2.3%,
-// 1024 x 4096 -> 4096 -4%, 4096 x 5120 -> 576 -1.6%; at K = 576 within +-1%
-// (128 x 96) or slower (128 x 128 +1%, and a GLU +13%).
-constexpr int kK64MinK = 2048;
+// 64-deep ring steps on the 128-row tiles, for the core non-GLU kinds.
+// Measured on MI355X (interleaved runs): 128 x 96 tiles 2048 x 4096 -> 1024
+// -2.3%, 4096 x 5120 -> 576 -1.6%, 2048 x 576 -> 1536 -0.6%; 128 x 128 tiles
+// 1024 x 4096 -> 4096 -4%, 512 x 8192 -> 8192 -6.6%, but 2048 x 576 -> 1536 +1%
+// (and a GLU +2..+14% at any K).
+constexpr int kK64MinK96 = 512;
+constexpr int kK64MinK128 = 2048;
 
 template <int EPI>
 static hipError_t launch_prefill_epi(const PrefillArgs& p) {
@@ -716,10 +718,8 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   if (tile == TILE_AUTO) {
     tile = auto_tile(p.M, p.NP, epi_is_glu(EPI));
     if constexpr (EPI == EPI_RMS || EPI == EPI_LN || EPI == EPI_NONE) {
-      if (!p.gs && p.K >= kK64MinK) {
-        if (tile == TILE_128x96_W8) tile = TILE_128x96_W8_K64;
-        else if (tile == TILE_128x128_W8T) tile = TILE_128x128_W8T_K64;
-      }
+      if (!p.gs && tile == TILE_128x96_W8 && p.K >= kK64MinK96) tile = TILE_128x96_W8_K64;
+      if (!p.gs && tile == TILE_128x128_W8T && p.K >= kK64MinK128) tile = TILE_128x128_W8T_K64;
     }
   }
   if constexpr (EPI == EPI_RMS || EPI == EPI_GLU) {
