@@ -285,10 +285,11 @@ def test_non_contiguous_activation_rows(fn):
     assert row_err(to_np(y), oracle.rmsnorm_linear(w.a[:12], w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
 
 
-@pytest.mark.parametrize("K", [2048, 2088, 2112])
+@pytest.mark.parametrize("K", [576, 1032, 2048, 2088, 2112])
 def test_long_k_automatic_64_deep_steps(fn, K):
-    # K >= 2048 on the 128-row tiles takes 64-deep ring steps automatically:
-    # 32 (even) steps, 33 (odd) with the lane check (2088) and without it (2112).
+    # The 128 x 96 tile takes 64-deep ring steps automatically from K = 512:
+    # 9 (odd) steps at 576, 17 (odd, lane check) at 1032, 32 (even) at 2048,
+    # 33 (odd) with the lane check (2088) and without it (2112).
     M, N = 260, 200
     lin = workloads.make("linear", M, K, N, eps=1e-5, seed=K, outlier_frac=0.05)
     ln = workloads.make("layernorm", M, K, N, eps=1e-5, seed=K + 1, a_mean=0.5)
