@@ -88,7 +88,12 @@ size_t fold_weights_size(int64_t K, int64_t N, int layout, int ws_dtype);
 
 /* Fold the normalisation weights into the linear layer, once, offline
  * (Prop. 1: W*[k,n] = g_k W[k,n]; Sec. 3.4: c* = beta W).
- *   W       [K, N] row-major, leading dimension ldw >= N, dtype w_dtype (fp32 or bf16).
+ *   W       logical [K, N] weight, dtype w_dtype (fp32 or bf16): element (k, n) is at
+ *           W[k * stride_k + n * stride_n] (strides in elements, each >= 0, stride_k
+ *           below 2^40 and stride_n below 2^31, else FN_ERR_SIZE; negative: FN_ERR_SHAPE).
+ *           A row-major [K, N] tensor has (stride_k, stride_n) = (ld, 1); a framework's
+ *           [N, K] linear-layer weight is folded in place, with no transposed copy,
+ *           as (1, ld).  Only read; views whose elements overlap are allowed.
  *           For FN_LAYOUT_GLU, N = 2F and W = [Wg | Wu].
  *   g       [K] fp32, or NULL for g = 1 (plain packing of W, used by the unfused baseline).
  *   beta    [K] fp32 LayerNorm bias, or NULL; needed only for c_star.
@@ -101,9 +106,9 @@ size_t fold_weights_size(int64_t K, int64_t N, int layout, int ws_dtype);
  *   c_star  optional [N] fp32: sum over k of beta_k W[k,n] with the unfolded W,
  *           accumulated in fp64 and rounded once; requires beta.
  *   colsum and c_star are available for FN_LAYOUT_LINEAR only. */
-int fold_weights(const void* W, int64_t ldw, int w_dtype, const float* g, const float* beta,
-                 int64_t K, int64_t N, int layout, void* W_star, int ws_dtype, float* colsum,
-                 float* c_star, void* stream);
+int fold_weights(const void* W, int64_t stride_k, int64_t stride_n, int w_dtype, const float* g,
+                 const float* beta, int64_t K, int64_t N, int layout, void* W_star, int ws_dtype,
+                 float* colsum, float* c_star, void* stream);
 
 /* Inverse of the packing: write the logical [K, N] weight held in W_star (as
  * written by fold_weights with the same K, N, layout, ws_dtype) to out, row-major

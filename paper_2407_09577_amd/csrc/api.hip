@@ -16,6 +16,10 @@ constexpr int64_t kMaxRows = int64_t(1) << 30;  // M, N
 // Packed weight buffer: the matrix-core kernels address it with 32-bit byte
 // offsets and use offsets >= 2^31 as out-of-range (zero-returning) loads.
 constexpr int64_t kMaxPackedBytes = (int64_t(1) << 31) - 1;
+// Strides of the weight view fold_weights reads: with K <= 2^21 and N <= 2^30 every
+// element offset stays below 2^62.
+constexpr int64_t kMaxFoldStrideK = int64_t(1) << 40;
+constexpr int64_t kMaxFoldStrideN = int64_t(1) << 31;
 
 int64_t packed_bytes(int64_t K, int64_t N, bool glu, int64_t elem) {
   return fn::packed_rows(K) * fn::packed_cols(N, glu) * elem;
@@ -141,22 +145,26 @@ size_t fold_weights_size(int64_t K, int64_t N, int layout, int ws_dtype) {
   return bytes > kMaxPackedBytes ? 0 : (size_t)bytes;
 }
 
-int fold_weights(const void* W, int64_t ldw, int w_dtype, const float* g, const float* beta, int64_t K,
-                 int64_t N, int layout, void* W_star, int ws_dtype, float* colsum, float* c_star,
-                 void* stream) {
+int fold_weights(const void* W, int64_t stride_k, int64_t stride_n, int w_dtype, const float* g,
+                 const float* beta, int64_t K, int64_t N, int layout, void* W_star, int ws_dtype,
+                 float* colsum, float* c_star, void* stream) {
   if (!dtype_ok(w_dtype) || !dtype_ok(ws_dtype)) return FN_ERR_DTYPE;
   if (layout != FN_LAYOUT_LINEAR && layout != FN_LAYOUT_GLU) return FN_ERR_VALUE;
-  if (K <= 0 || N <= 0 || ldw < N || (layout == FN_LAYOUT_GLU && N % 2)) return FN_ERR_SHAPE;
-  if (K > kMaxLd || N > kMaxRows) return FN_ERR_SIZE;
+  if (K <= 0 || N <= 0 || stride_k < 0 || stride_n < 0 || (layout == FN_LAYOUT_GLU && N % 2))
+    return FN_ERR_SHAPE;
+  if (K > kMaxLd || N > kMaxRows || stride_k >= kMaxFoldStrideK || stride_n >= kMaxFoldStrideN)
+    return FN_ERR_SIZE;
   if (packed_bytes(K, N, layout == FN_LAYOUT_GLU, elem_size(ws_dtype)) > kMaxPackedBytes) return FN_ERR_SIZE;
   if (!W || !W_star) return FN_ERR_NULL;
   if (c_star && !beta) return FN_ERR_NULL;
   if (layout == FN_LAYOUT_GLU && (colsum || c_star)) return FN_ERR_UNSUPPORTED;
   if (!aligned16(W_star) || (reinterpret_cast<uintptr_t>(W) % elem_size(w_dtype))) return FN_ERR_ALIGN;
   const int64_t wsb = (int64_t)fold_weights_size(K, N, layout, ws_dtype);
-  if (overlaps(W_star, wsb, W, extent_bytes(K, N, ldw, w_dtype))) return FN_ERR_ALIAS;
-  fn::FoldArgs p{W, ldw, w_dtype, g, beta, K, N, layout == FN_LAYOUT_GLU, W_star, ws_dtype, colsum,
-                 c_star, (hipStream_t)stream};
+  // Bytes spanned by the strided view (the largest element offset is below 2^62).
+  const int64_t wext = ((K - 1) * stride_k + (N - 1) * stride_n + 1) * elem_size(w_dtype);
+  if (overlaps(W_star, wsb, W, wext)) return FN_ERR_ALIAS;
+  fn::FoldArgs p{W, stride_k, stride_n, w_dtype, g, beta, K, N, layout == FN_LAYOUT_GLU, W_star, ws_dtype,
+                 colsum, c_star, (hipStream_t)stream};
   return status_of(fn::launch_fold(p));
 }
 

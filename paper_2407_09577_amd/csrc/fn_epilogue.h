@@ -32,7 +32,10 @@ __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& e
     st.s = 1.0f / fmaf(ss, ep.inv_k, ep.eps);
   } else if constexpr (EPI == EPI_LN) {
     float mu = sa * ep.inv_k;
-    float var = fmaxf(fmaf(ss, ep.inv_k, -mu * mu), 0.0f);
+    // one-pass variance, clamped at 0 against cancellation; a NaN (a row holding NaN or
+    // Inf) stays NaN, so that row's outputs are NaN as in the standard form
+    float var = fmaf(ss, ep.inv_k, -mu * mu);
+    var = var < 0.0f ? 0.0f : var;
     st.mu = mu;
     st.s = rsqrtf(var + ep.eps);
   }

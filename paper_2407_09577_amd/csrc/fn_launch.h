@@ -97,7 +97,7 @@ hipError_t launch_f32(const F32Args& p);
 
 struct FoldArgs {
   const void* W;
-  int64_t ldw;
+  int64_t sk, sn;  // element (k, n) of the logical weight is W[k * sk + n * sn]
   int w_dtype;  // 0 fp32, 1 bf16
   const float* g;
   const float* beta;

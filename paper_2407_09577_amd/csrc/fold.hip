@@ -48,7 +48,7 @@ __device__ __forceinline__ double load_w(const void* W, int64_t idx, int w_dtype
 
 // One thread per 16-byte chunk (8 consecutive k of one packed column) of the
 // fragment-major bf16 layout.
-__global__ void fold_pack_bf16_kernel(const void* __restrict__ W, int64_t ldw, int w_dtype,
+__global__ void fold_pack_bf16_kernel(const void* __restrict__ W, int64_t sk, int64_t sn, int w_dtype,
                                       const float* __restrict__ g, int64_t K, int64_t N, int glu,
                                       int64_t NPB, int64_t nchunks, u32x4* __restrict__ out) {
   const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -64,7 +64,7 @@ __global__ void fold_pack_bf16_kernel(const void* __restrict__ W, int64_t ldw, i
   for (int e = 0; e < 8; ++e) {
     const int64_t k = k0 + e;
     double v = 0.0;
-    if (n >= 0 && k < K) v = (g ? (double)g[k] : 1.0) * load_w(W, k * ldw + n, w_dtype);
+    if (n >= 0 && k < K) v = (g ? (double)g[k] : 1.0) * load_w(W, k * sk + n * sn, w_dtype);
     h[e] = dbl_to_bf16_rne(v);
   }
   out[c] = u32x4{h[0] | ((unsigned)h[1] << 16), h[2] | ((unsigned)h[3] << 16),
@@ -72,7 +72,7 @@ __global__ void fold_pack_bf16_kernel(const void* __restrict__ W, int64_t ldw, i
 }
 
 // fp32 storage: row-major [KP][NP] with columns in packed order.
-__global__ void fold_pack_f32_kernel(const void* __restrict__ W, int64_t ldw, int w_dtype,
+__global__ void fold_pack_f32_kernel(const void* __restrict__ W, int64_t sk, int64_t sn, int w_dtype,
                                      const float* __restrict__ g, int64_t K, int64_t N, int glu,
                                      int64_t KP, int64_t NP, float* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -80,7 +80,7 @@ __global__ void fold_pack_f32_kernel(const void* __restrict__ W, int64_t ldw, in
   const int64_t k = i / NP, p = i % NP;
   const int64_t n = logical_col(p, N, glu);
   double v = 0.0;
-  if (n >= 0 && k < K) v = (g ? (double)g[k] : 1.0) * load_w(W, k * ldw + n, w_dtype);
+  if (n >= 0 && k < K) v = (g ? (double)g[k] : 1.0) * load_w(W, k * sk + n * sn, w_dtype);
   out[i] = (float)v;  // one round to nearest even
 }
 
@@ -97,7 +97,7 @@ __device__ __forceinline__ double packed_at(const void* ws, int ws_dtype, int64_
 
 // LayerNorm extras for a linear layout (packed column == logical column).
 __global__ void fold_colsum_kernel(const void* __restrict__ ws, int ws_dtype, const void* __restrict__ W,
-                                   int64_t ldw, int w_dtype, const float* __restrict__ beta, int64_t K,
+                                   int64_t sk, int64_t sn, int w_dtype, const float* __restrict__ beta, int64_t K,
                                    int64_t N, int64_t KP, int64_t NP, float* __restrict__ colsum,
                                    float* __restrict__ cstar) {
   const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -105,7 +105,7 @@ __global__ void fold_colsum_kernel(const void* __restrict__ ws, int ws_dtype, co
   double cs = 0.0, cb = 0.0;
   for (int64_t k = 0; k < K; ++k) {
     if (colsum) cs += packed_at(ws, ws_dtype, k, n, KP, NP);
-    if (cstar) cb += (double)beta[k] * load_w(W, k * ldw + n, w_dtype);
+    if (cstar) cb += (double)beta[k] * load_w(W, k * sk + n * sn, w_dtype);
   }
   if (colsum) colsum[n] = (float)cs;
   if (cstar) cstar[n] = (float)cb;
@@ -133,17 +133,17 @@ hipError_t launch_fold(const FoldArgs& p) {
   if (p.ws_dtype == kDtypeBf16) {
     const int64_t nchunks = KP * NP / 8;
     hipLaunchKernelGGL(fold_pack_bf16_kernel, dim3(blocks_for(nchunks, 256)), dim3(256), 0, p.stream, p.W,
-                       p.ldw, p.w_dtype, p.g, p.K, p.N, p.glu, NP / 16, nchunks,
+                       p.sk, p.sn, p.w_dtype, p.g, p.K, p.N, p.glu, NP / 16, nchunks,
                        reinterpret_cast<u32x4*>(p.ws));
   } else {
     hipLaunchKernelGGL(fold_pack_f32_kernel, dim3(blocks_for(KP * NP, 256)), dim3(256), 0, p.stream, p.W,
-                       p.ldw, p.w_dtype, p.g, p.K, p.N, p.glu, KP, NP, reinterpret_cast<float*>(p.ws));
+                       p.sk, p.sn, p.w_dtype, p.g, p.K, p.N, p.glu, KP, NP, reinterpret_cast<float*>(p.ws));
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.colsum || p.cstar) {
     hipLaunchKernelGGL(fold_colsum_kernel, dim3(blocks_for(p.N, 128)), dim3(128), 0, p.stream, p.ws,
-                       p.ws_dtype, p.W, p.ldw, p.w_dtype, p.beta, p.K, p.N, KP, NP, p.colsum, p.cstar);
+                       p.ws_dtype, p.W, p.sk, p.sn, p.w_dtype, p.beta, p.K, p.N, KP, NP, p.colsum, p.cstar);
     e = hipGetLastError();
   }
   return e;

@@ -45,7 +45,7 @@ def _load():
     P, I64, I, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
     sig = {
         "fold_weights_size": ([I64, I64, I, I], ctypes.c_size_t),
-        "fold_weights": ([P, I64, I, P, P, I64, I64, I, P, I, P, P, P], I),
+        "fold_weights": ([P, I64, I64, I, P, P, I64, I64, I, P, I, P, P, P], I),
         "unpack_weights": ([P, I64, I64, I, I, P, I64, P], I),
         "flashnorm_linear": ([P, I64, I64, I64, I, P, I64, F, P, P, I64, I, P, P], I),
         "flashnorm_linear_ex": ([P, I64, I64, I64, I, P, I64, F, P, P, I64, I, P, I, P], I),
@@ -129,20 +129,59 @@ def fold_weights_size(K: int, N: int, layout: int = FN_LAYOUT_LINEAR, ws_dtype: 
     return _load().fold_weights_size(K, N, layout, ws_dtype)
 
 
+# The C ABI takes raw device pointers and sizes the kernels' reads from the shape
+# arguments, so the binding refuses, before any call, tensors that the library would
+# read or write out of bounds: host tensors, tensors on different GPUs, outputs whose
+# shape is not [M, N], and packed weights or workspaces smaller than the shapes need.
+def _guard(where, tensors=(), packed=None, outs=(), nbytes=()):
+    """packed = (W_star, K, N, layout, dtype code); outs = ((tensor, rows, cols), ...);
+    nbytes = ((tensor, bytes needed, name), ...).  Size checks come first, then devices."""
+    if packed is not None:
+        Wst, K, N, layout, code = packed
+        need = fold_weights_size(K, N, layout, code)
+        # need == 0: invalid geometry, which the library itself rejects with its status
+        if need and Wst.numel() * Wst.element_size() < need:
+            raise ValueError(f"{where}: the packed weight holds {Wst.numel() * Wst.element_size()} bytes; "
+                             f"K = {K}, N = {N} need {need} (fold_weights_size)")
+        if not Wst.is_contiguous():
+            raise ValueError(f"{where}: the packed weight must be contiguous")
+    for t, rows, cols in outs:
+        if t is not None and tuple(t.shape) != (rows, cols):
+            raise ValueError(f"{where}: output of shape {tuple(t.shape)}, expected ({rows}, {cols})")
+    for t, need, name in nbytes:
+        if t is not None and t.numel() * t.element_size() < need:
+            raise ValueError(f"{where}: {name} holds {t.numel() * t.element_size()} bytes; {need} needed")
+    dev = None
+    for t in tensors:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{where}: every tensor must be a GPU tensor (got one on {t.device})")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"{where}: tensors on {dev} and {t.device}; all must be on one GPU")
+
+
 def fold_weights(W: torch.Tensor, g, beta=None, layout: int = FN_LAYOUT_LINEAR, ws_dtype=None,
                  colsum: bool = False, c_star: bool = False, stream=None):
     """Fold g into W (and beta into c*) and pack.  W is the logical [K, N] weight
-    ([K, 2F] = [Wg | Wu] for a GLU).  g = None packs W unchanged.  Returns
-    (W_star, colsum or None, c_star or None); W_star is an opaque uint8 device buffer."""
+    ([K, 2F] = [Wg | Wu] for a GLU), any strides: a torch linear layer's [N, K]
+    weight is passed as ``weight.t()`` and read in place.  g = None packs W
+    unchanged.  Returns (W_star, colsum or None, c_star or None); W_star is an
+    opaque uint8 device buffer."""
     K, N = W.shape
     ws_code = _dt(W) if ws_dtype is None else (ws_dtype if isinstance(ws_dtype, int) else _dt(torch.empty(0, dtype=ws_dtype)))
     nbytes = fold_weights_size(K, N, layout, ws_code)
     if nbytes == 0:
         raise ValueError("invalid fold geometry")
+    _guard("fold_weights", (W, g, beta))
     Ws = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
     cs = torch.empty(N, dtype=torch.float32, device=W.device) if colsum else None
     cb = torch.empty(N, dtype=torch.float32, device=W.device) if c_star else None
-    _check(_load().fold_weights(_ptr(W), _ld(W), _dt(W), _ptr(_vec(g, K, "g")), _ptr(_vec(beta, K, "beta")),
+    if W.dim() != 2:
+        raise ValueError("W must be a 2-D [K, N] tensor")
+    _check(_load().fold_weights(_ptr(W), W.stride(0), W.stride(1), _dt(W), _ptr(_vec(g, K, "g")), _ptr(_vec(beta, K, "beta")),
                                 K, N, layout, _ptr(Ws), ws_code, _ptr(cs), _ptr(cb), _stream(stream)),
            "fold_weights")
     return Ws, cs, cb
@@ -150,6 +189,7 @@ def fold_weights(W: torch.Tensor, g, beta=None, layout: int = FN_LAYOUT_LINEAR, 
 
 def unpack_weights(W_star: torch.Tensor, K: int, N: int, layout: int = FN_LAYOUT_LINEAR,
                    ws_dtype: int = FN_BF16, stream=None) -> torch.Tensor:
+    _guard("unpack_weights", (W_star,), packed=(W_star, K, N, layout, ws_dtype))
     out = torch.zeros(K, N, dtype=_torch_dtype(ws_dtype), device=W_star.device)
     _check(_load().unpack_weights(_ptr(W_star), K, N, layout, ws_dtype, _ptr(out), N, _stream(stream)),
            "unpack_weights")
@@ -159,6 +199,8 @@ def unpack_weights(W_star: torch.Tensor, K: int, N: int, layout: int = FN_LAYOUT
 def flashnorm_linear(a: torch.Tensor, W_star: torch.Tensor, N: int, eps: float, bias=None, out=None,
                      inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     M, K = a.shape
+    _guard("flashnorm_linear", (a, W_star, bias, out, inv_rms), packed=(W_star, K, N, FN_LAYOUT_LINEAR, _dt(a)),
+           outs=((out, M, N),))
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     _check(_load().flashnorm_linear_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star), N, eps,
                                        _ptr(_vec(bias, N, "bias")), _ptr(y), _ld(y), _dt(y),
@@ -170,6 +212,8 @@ def flashnorm_linear(a: torch.Tensor, W_star: torch.Tensor, N: int, eps: float, 
 def flashnorm_glu(a: torch.Tensor, W_star_gu: torch.Tensor, F: int, eps: float, out=None,
                   path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     M, K = a.shape
+    _guard("flashnorm_glu", (a, W_star_gu, out), packed=(W_star_gu, K, 2 * F, FN_LAYOUT_GLU, _dt(a)),
+           outs=((out, M, F),))
     o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
     _check(_load().flashnorm_glu_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star_gu), F, eps, _ptr(o), _ld(o),
                                     _dt(o), path, _stream(stream)), "flashnorm_glu")
@@ -180,6 +224,8 @@ def flashnorm_glu_act(a: torch.Tensor, W_star_gu: torch.Tensor, F: int, eps: flo
                       inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     """GLU-variant FFN input projection (act = FN_GLU_*); inv_rms receives s = 1/RMSe(a) where allowed."""
     M, K = a.shape
+    _guard("flashnorm_glu_act", (a, W_star_gu, out, inv_rms), packed=(W_star_gu, K, 2 * F, FN_LAYOUT_GLU, _dt(a)),
+           outs=((out, M, F),))
     o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
     _check(_load().flashnorm_glu_act(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star_gu), F, eps, act, _ptr(o),
                                      _ld(o), _dt(o), _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
@@ -191,6 +237,8 @@ def flashnorm_linear_relu(a: torch.Tensor, W_star: torch.Tensor, N: int, eps: fl
                           out=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     """ReLU FFN up projection with the scale deferred: y = relu(a W*), inv_rms = 1/RMSe(a)."""
     M, K = a.shape
+    _guard("flashnorm_linear_relu", (a, W_star, out, inv_rms), packed=(W_star, K, N, FN_LAYOUT_LINEAR, _dt(a)),
+           outs=((out, M, N),))
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     _check(_load().flashnorm_linear_relu(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star), N, eps, _ptr(y), _ld(y),
                                          _dt(y), _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
@@ -202,6 +250,8 @@ def rowscale_linear(x: torch.Tensor, W_packed: torch.Tensor, N: int, row_scale: 
                     path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     """y = (x W) * row_scale[m]: applies a normalisation scale deferred to this layer's output."""
     M, K = x.shape
+    _guard("rowscale_linear", (x, W_packed, row_scale, out), packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(x)),
+           outs=((out, M, N),))
     y = out if out is not None else torch.empty(M, N, dtype=x.dtype, device=x.device)
     _check(_load().rowscale_linear(_ptr(x), M, K, _ld(x), _dt(x), _ptr(W_packed), N,
                                    _ptr(_vec(row_scale, M, "row_scale")), _ptr(y), _ld(y), _dt(y), path,
@@ -215,6 +265,8 @@ def flashnorm_qkv_rope(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv: in
     """Deferred RMSNorm -> fused [Wq|Wk|Wv] projection -> RoPE on Q and K (Fig. 5(b))."""
     M, K = a.shape
     N = (Hq + 2 * Hkv) * h
+    _guard("flashnorm_qkv_rope", (a, W_packed, positions, cos_tab, sin_tab, bias, out, inv_rms),
+           packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     if positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
         raise ValueError("positions must be a contiguous int32 tensor of M entries")
@@ -238,14 +290,12 @@ def flashnorm_qkv_headnorm(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv
     """Deferred RMSNorm -> fused [Wq|Wk|Wv] -> per-head RMSNorm of Q, K (and V with gv) -> RoPE (Prop. 3)."""
     M, K = a.shape
     N = (Hq + 2 * Hkv) * h
+    _guard("flashnorm_qkv_headnorm", (a, W_packed, gq, gk, gv, positions, cos_tab, sin_tab, out, inv_rms),
+           packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     P_rows = 0
     if positions is not None:
-        if positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
-            raise ValueError("positions must be a contiguous int32 tensor of M entries")
-        if cos_tab is None or sin_tab is None or cos_tab.shape != sin_tab.shape or cos_tab.shape[1:] != (h // 2,):
-            raise ValueError("cos_tab and sin_tab must be [P, h/2] fp32")
-        P_rows = cos_tab.shape[0]
+        P_rows = _rope_tables(M, h // 2, positions, cos_tab, sin_tab)
     _check(_load().flashnorm_qkv_headnorm(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_packed), Hq, Hkv, h, eps,
                                           _ptr(_vec(gq, h, "gq")), _ptr(_vec(gk, h, "gk")), _ptr(_vec(gv, h, "gv")),
                                           eps_head, _ptr(positions), _ptr(cos_tab), _ptr(sin_tab), P_rows, q_scale,
@@ -258,7 +308,9 @@ def baseline_qkv_headnorm(y: torch.Tensor, Hq: int, Hkv: int, h: int, gq, gk, gv
                           cos_tab=None, sin_tab=None, q_scale: float = 1.0, stream=None) -> torch.Tensor:
     """Unfused per-head norms (+ RoPE) on the Q and K (and V) heads of y, in place."""
     M = y.shape[0]
-    P_rows = cos_tab.shape[0] if (positions is not None and cos_tab is not None) else 0
+    _guard("baseline_qkv_headnorm", (y, gq, gk, gv, positions, cos_tab, sin_tab),
+           outs=((y, M, (Hq + 2 * Hkv) * h),))
+    P_rows = _rope_tables(M, h // 2, positions, cos_tab, sin_tab) if positions is not None else 0
     _check(_load().baseline_qkv_headnorm(_ptr(y), M, _ld(y), _dt(y), Hq, Hkv, h, _ptr(_vec(gq, h, "gq")),
                                          _ptr(_vec(gk, h, "gk")), _ptr(_vec(gv, h, "gv")), eps_head, _ptr(positions),
                                          _ptr(cos_tab), _ptr(sin_tab), P_rows, q_scale, _stream(stream)),
@@ -270,11 +322,23 @@ def baseline_rope(y: torch.Tensor, Hq: int, Hkv: int, h: int, positions: torch.T
                   sin_tab: torch.Tensor, q_scale: float, stream=None) -> torch.Tensor:
     """Unfused RoPE on the Q and K heads of y, in place (the rotation kernel of Fig. 5(a))."""
     M = y.shape[0]
-    if positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
-        raise ValueError("positions must be a contiguous int32 tensor of M entries")
+    _rope_tables(M, h // 2, positions, cos_tab, sin_tab)
+    _guard("baseline_rope", (y, positions, cos_tab, sin_tab), outs=((y, M, (Hq + 2 * Hkv) * h),))
     _check(_load().baseline_rope(_ptr(y), M, _ld(y), _dt(y), Hq, Hkv, h, _ptr(positions), _ptr(cos_tab),
                                  _ptr(sin_tab), cos_tab.shape[0], q_scale, _stream(stream)), "baseline_rope")
     return y
+
+
+def _rope_tables(M, half, positions, cos_tab, sin_tab):
+    """positions: contiguous int32 [M]; cos_tab, sin_tab: contiguous fp32 [P, half] of one shape."""
+    if positions is None or positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
+        raise ValueError("positions must be a contiguous int32 tensor of M entries")
+    for name, t in (("cos_tab", cos_tab), ("sin_tab", sin_tab)):
+        if t is None or t.dtype != torch.float32 or not t.is_contiguous() or t.dim() != 2 or t.shape[1] != half:
+            raise ValueError(f"{name} must be a contiguous fp32 [P, {half}] tensor")
+    if cos_tab.shape != sin_tab.shape:
+        raise ValueError("cos_tab and sin_tab differ in shape")
+    return cos_tab.shape[0]
 
 
 def _rotary_args(M, R, positions, cos_tab, sin_tab):
@@ -296,6 +360,8 @@ def flashnorm_mla_latent(a: torch.Tensor, W_packed: torch.Tensor, L: int, R: int
     """MLA down-projection [latent | rotary key] with the latent RMSNorm (Prop. 3: the input
     norm cancels in the latent) and RoPE on the R rotary columns."""
     M, K = a.shape
+    _guard("flashnorm_mla_latent", (a, W_packed, g_lat, positions, cos_tab, sin_tab, out, inv_rms),
+           packed=(W_packed, K, L + R, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, L + R),))
     y = out if out is not None else torch.empty(M, L + R, dtype=a.dtype, device=a.device)
     pos, cos_t, sin_t, P_rows = _rotary_args(M, R, positions, cos_tab, sin_tab)
     if R > 0 and inv_rms is None:
@@ -312,6 +378,7 @@ def baseline_mla_latent(y: torch.Tensor, L: int, R: int, g_lat: torch.Tensor, ep
                         cos_tab=None, sin_tab=None, stream=None) -> torch.Tensor:
     """Unfused latent RMSNorm + rotary key RoPE on y = [latent | key], in place."""
     M = y.shape[0]
+    _guard("baseline_mla_latent", (y, g_lat, positions, cos_tab, sin_tab), outs=((y, M, L + R),))
     pos, cos_t, sin_t, P_rows = _rotary_args(M, R, positions, cos_tab, sin_tab)
     _check(_load().baseline_mla_latent(_ptr(y), M, _ld(y), _dt(y), L, R, _ptr(_vec(g_lat, L, "g_lat")), eps_lat,
                                        _ptr(pos), _ptr(cos_t), _ptr(sin_t), P_rows, _stream(stream)),
@@ -323,6 +390,8 @@ def flashnorm_linear_unfolded(a: torch.Tensor, g: torch.Tensor, W_packed: torch.
                               bias=None, out=None, inv_rms=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     """Deferred RMSNorm -> linear with g applied at run time to an unfolded packed W."""
     M, K = a.shape
+    _guard("flashnorm_linear_unfolded", (a, g, W_packed, bias, out, inv_rms),
+           packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     _check(_load().flashnorm_linear_unfolded(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed),
                                              N, eps, _ptr(_vec(bias, N, "bias")), _ptr(y), _ld(y), _dt(y),
@@ -335,6 +404,8 @@ def flashnorm_glu_unfolded(a: torch.Tensor, g: torch.Tensor, W_packed_gu: torch.
                            out=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     """Deferred RMSNorm -> SwiGLU with g applied at run time to an unfolded packed [Wg | Wu]."""
     M, K = a.shape
+    _guard("flashnorm_glu_unfolded", (a, g, W_packed_gu, out), packed=(W_packed_gu, K, 2 * F, FN_LAYOUT_GLU, _dt(a)),
+           outs=((out, M, F),))
     o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
     _check(_load().flashnorm_glu_unfolded(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed_gu),
                                           F, eps, _ptr(o), _ld(o), _dt(o), path, _stream(stream)),
@@ -345,6 +416,8 @@ def flashnorm_glu_unfolded(a: torch.Tensor, g: torch.Tensor, W_packed_gu: torch.
 def flashnorm_layernorm_linear(a: torch.Tensor, W_star: torch.Tensor, colsum: torch.Tensor, c_star, N: int,
                                eps: float, out=None, path: int = FN_PATH_AUTO, stream=None) -> torch.Tensor:
     M, K = a.shape
+    _guard("flashnorm_layernorm_linear", (a, W_star, colsum, c_star, out),
+           packed=(W_star, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     _check(_load().flashnorm_layernorm_linear_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star),
                                                  _ptr(_vec(colsum, N, "colsum")), _ptr(_vec(c_star, N, "c_star")),
@@ -357,8 +430,17 @@ def _ws(a, x_ws):
     return x_ws if x_ws is not None else torch.empty_like(a, memory_format=torch.contiguous_format)
 
 
+def _baseline_guard(where, a, g, beta, W_packed, N, layout, x_ws, out, ncols):
+    M, K = a.shape
+    _guard(where, (a, g, beta, W_packed, x_ws, out), packed=(W_packed, K, N, layout, _dt(a)),
+           outs=((out, M, ncols),), nbytes=((x_ws, M * K * a.element_size(), "the workspace x_ws"),))
+    if x_ws is not None and (x_ws.dtype != a.dtype or not x_ws.is_contiguous()):
+        raise ValueError(f"{where}: the workspace must be contiguous, in the activations' dtype")
+
+
 def baseline_rmsnorm_linear(a, g, W_packed, N, eps, x_ws=None, out=None, path=FN_PATH_AUTO, stream=None):
     M, K = a.shape
+    _baseline_guard("baseline_rmsnorm_linear", a, g, None, W_packed, N, FN_LAYOUT_LINEAR, x_ws, out, N)
     x = _ws(a, x_ws)
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     _check(_load().baseline_rmsnorm_linear(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed),
@@ -369,6 +451,7 @@ def baseline_rmsnorm_linear(a, g, W_packed, N, eps, x_ws=None, out=None, path=FN
 
 def baseline_rmsnorm_glu(a, g, W_packed_gu, F, eps, x_ws=None, out=None, path=FN_PATH_AUTO, stream=None):
     M, K = a.shape
+    _baseline_guard("baseline_rmsnorm_glu", a, g, None, W_packed_gu, 2 * F, FN_LAYOUT_GLU, x_ws, out, F)
     x = _ws(a, x_ws)
     o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
     _check(_load().baseline_rmsnorm_glu(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed_gu),
@@ -380,6 +463,7 @@ def baseline_rmsnorm_glu(a, g, W_packed_gu, F, eps, x_ws=None, out=None, path=FN
 def baseline_layernorm_linear(a, g, beta, W_packed, N, eps, x_ws=None, out=None, path=FN_PATH_AUTO,
                               stream=None):
     M, K = a.shape
+    _baseline_guard("baseline_layernorm_linear", a, g, beta, W_packed, N, FN_LAYOUT_LINEAR, x_ws, out, N)
     x = _ws(a, x_ws)
     y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
     _check(_load().baseline_layernorm_linear(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")),

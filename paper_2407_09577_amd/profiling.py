@@ -42,7 +42,14 @@ def kernel_sources_sha256(kernel: str) -> str:
 
 
 def _rows(d, name):
+    """Rows of rocprofv3's CSV ``name`` under output directory ``d`` (at its top level, or in
+    the per-host/per-process subdirectories rocprofv3 may create)."""
     path = os.path.join(d, name)
+    if not os.path.exists(path):
+        found = sorted(glob.glob(os.path.join(d, "**", "*" + name), recursive=True))
+        if not found:
+            raise FileNotFoundError(f"no {name} under {d}")
+        path = found[0]
     with open(path) as f:
         return list(csv.DictReader(f))
 

@@ -117,21 +117,26 @@ def test_glu_and_layernorm_validation(fnlib):
 
 def test_fold_validation(fnlib):
     lib = fnlib.lib()
-    f = lambda **kw: lib.fold_weights(kw.get("W", A), kw.get("ldw", 32), kw.get("wdt", 1), kw.get("g", X),
+    f = lambda **kw: lib.fold_weights(kw.get("W", A), kw.get("sk", 32), kw.get("sn", 1), kw.get("wdt", 1), kw.get("g", X),
                                       kw.get("beta", None), kw.get("K", 64), kw.get("N", 32),
                                       kw.get("layout", 0), kw.get("ws", W), kw.get("wsdt", 1),
                                       kw.get("colsum", None), kw.get("cstar", None), None)
     assert f(W=0) == -1
     assert f(ws=0) == -1
-    assert f(ldw=16) == -2
-    assert f(N=31, layout=1, ldw=32) == -2
+    assert f(sk=-32) == -2                         # negative strides
+    assert f(sn=-1) == -2
+    assert f(N=31, layout=1) == -2
+    assert f(sk=1 << 40) == -9                     # element offsets must stay below 2^62
+    assert f(sn=1 << 31) == -9
     assert f(layout=3) == -6
     assert f(wdt=4) == -3
     assert f(cstar=X) == -1                        # c* needs beta
     assert f(layout=1, colsum=X) == -5             # LayerNorm extras: linear layout only
     assert f(ws=W + 4) == -4
     assert f(ws=A + 16) == -8                      # packed output overlaps W
-    assert f(K=1 << 15, N=1 << 15, ldw=1 << 15) == -9
+    assert f(K=1 << 15, N=1 << 15, sk=1 << 15) == -9
+    assert f(ws=A + 64 * 32 * 2 - 16) == -8        # overlaps the last element of the row-major view
+    assert f(sk=1, sn=64, ws=A + 32 * 64 * 2 - 16) == -8   # and of the transposed view
     u = lambda **kw: lib.unpack_weights(kw.get("ws", W), 64, 32, 0, 1, kw.get("out", Y), kw.get("ldo", 32), None)
     assert u(ws=0) == -1
     assert u(ldo=8) == -2
@@ -288,3 +293,61 @@ def test_mla_latent_validation(fnlib):
     assert bl(y=Y + 4) == -4
     assert bl(dt=5) == -3
     assert bl(M=0) == 0
+
+
+# ----------------------------------------------------------- the Python binding's own guards
+# The C ABI cannot see tensor sizes or devices, so the binding refuses, before any call,
+# arguments that would make a kernel read or write outside an allocation.  These run on
+# host tensors: the size checks come before the device check, so each rejection is the
+# one named.
+def _bf16(*shape):
+    import torch
+    return torch.zeros(*shape, dtype=torch.bfloat16)
+
+
+def test_binding_rejects_short_packed_weight(fnlib):
+    M, K, N = 4, 64, 32
+    need = fnlib.fold_weights_size(K, N, fnlib.FN_LAYOUT_LINEAR, fnlib.FN_BF16)
+    import torch
+    short = torch.zeros(need - 16, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="packed weight holds"):
+        fnlib.flashnorm_linear(_bf16(M, K), short, N, 1e-6)
+    # a weight folded for fewer columns, reused for more
+    with pytest.raises(ValueError, match="packed weight holds"):
+        fnlib.flashnorm_linear(_bf16(M, K), torch.zeros(need, dtype=torch.uint8), 2 * N, 1e-6)
+    glu_need = fnlib.fold_weights_size(K, 2 * N, fnlib.FN_LAYOUT_GLU, fnlib.FN_BF16)
+    with pytest.raises(ValueError, match="packed weight holds"):
+        fnlib.flashnorm_glu(_bf16(M, K), torch.zeros(glu_need - 1024, dtype=torch.uint8), N, 1e-6)
+    with pytest.raises(ValueError, match="packed weight holds"):
+        fnlib.flashnorm_layernorm_linear(_bf16(M, 2 * K), torch.zeros(need, dtype=torch.uint8),
+                                         torch.zeros(N), None, N, 1e-6)
+    with pytest.raises(ValueError, match="packed weight holds"):
+        fnlib.baseline_rmsnorm_linear(_bf16(M, K), torch.ones(K), short, N, 1e-6)
+
+
+def test_binding_rejects_wrong_output_and_workspace(fnlib):
+    import torch
+    M, K, N = 4, 64, 32
+    Ws = torch.zeros(fnlib.fold_weights_size(K, N, fnlib.FN_LAYOUT_LINEAR, fnlib.FN_BF16), dtype=torch.uint8)
+    with pytest.raises(ValueError, match="output of shape"):
+        fnlib.flashnorm_linear(_bf16(M, K), Ws, N, 1e-6, out=_bf16(M - 1, N))
+    with pytest.raises(ValueError, match="workspace"):
+        fnlib.baseline_rmsnorm_linear(_bf16(M, K), torch.ones(K), Ws, N, 1e-6, x_ws=_bf16(M - 1, K))
+    with pytest.raises(ValueError, match="output of shape"):
+        fnlib.baseline_rope(_bf16(M, 100), 1, 1, 32, torch.zeros(M, dtype=torch.int32), torch.zeros(8, 16),
+                            torch.zeros(8, 16), 1.0)
+    with pytest.raises(ValueError, match="cos_tab"):
+        fnlib.baseline_rope(_bf16(M, 96), 1, 1, 32, torch.zeros(M, dtype=torch.int32), torch.zeros(8, 8),
+                            torch.zeros(8, 8), 1.0)
+
+
+def test_binding_rejects_host_tensors(fnlib):
+    import torch
+    M, K, N = 4, 64, 32
+    Ws = torch.zeros(fnlib.fold_weights_size(K, N, fnlib.FN_LAYOUT_LINEAR, fnlib.FN_BF16), dtype=torch.uint8)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        fnlib.flashnorm_linear(_bf16(M, K), Ws, N, 1e-6)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        fnlib.fold_weights(_bf16(K, N), torch.ones(K))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        fnlib.flashnorm_layernorm_linear(_bf16(M, K), Ws, torch.zeros(N), None, N, 1e-6)

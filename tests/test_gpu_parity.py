@@ -51,6 +51,36 @@ def to_np(t):
     return t.detach().float().cpu().double().numpy()
 
 
+def row_scale_dev(got, ref):
+    """max over rows of |<y_m, r_m> / <r_m, r_m> - 1|: the least-squares scale of each output
+    row against the oracle's.  The bf16 roundings of W* and of the output are unbiased and
+    average out over a row's columns (~1e-4 at N = 4096), so a systematic error of the row
+    statistics (a lost k block of the sum of squares shifts the scale by 1/(2 * blocks) ~ 0.4%
+    at K = 4096) shows here although it stays inside the 2e-2 row-normwise gate."""
+    got = np.asarray(got, dtype=np.float64)
+    den = np.einsum("ij,ij->i", ref, ref)
+    ok = den > 0
+    c = np.einsum("ij,ij->i", got, ref)[ok] / den[ok]
+    return float(np.max(np.abs(c - 1.0))) if c.size else 0.0
+
+
+SCALE_TOL = 1e-3  # per-row scale deviation allowed at full size (bf16); see row_scale_dev
+
+
+def tile_rows(M, tile=256, per_tile=16, seed=0):
+    """Rows covering every `tile`-row band of the output: both edge rows of each band and
+    per_tile - 2 random rows inside it.  Whole rows are compared, so every output tile of
+    every band is checked."""
+    rng = np.random.default_rng(seed)
+    rows = []
+    for t0 in range(0, M, tile):
+        t1 = min(M, t0 + tile)
+        rows += [t0, t1 - 1]
+        inner = np.arange(t0 + 1, t1 - 1)
+        rows += list(rng.choice(inner, size=min(per_tile - 2, inner.size), replace=False))
+    return np.array(sorted(set(rows)), dtype=np.int64)
+
+
 def sample_rows(M, n=48, seed=0):
     rng = np.random.default_rng(seed)
     fixed = [0, 1, 15, 16, 127, 128, 255, 256, M // 2, M - 2, M - 1]
@@ -76,14 +106,17 @@ def check_linear(fn, w, rows=None, path=0, bias=None):
 
 
 # ------------------------------------------------------------------ the five workloads
-def test_tiny_fp32_deferred_vs_standard(fn):
+def test_tiny_fp32_deferred_vs_standard(fn, record_parity):
     w = workloads.tiny_fp32()
-    assert check_linear(fn, w) <= TOL[torch.float32]
+    err = check_linear(fn, w)
+    record_parity("tiny_fp32 16x576x576 (all rows)", row_err=err)
+    assert err <= TOL[torch.float32], err
 
 
-def test_smollm2_prefill_full(fn):
+def test_smollm2_prefill_full(fn, record_parity):
     w = workloads.smollm2_prefill()
     err = check_linear(fn, w)
+    record_parity("smollm2_prefill 2048x576x1536 (all rows)", row_err=err)
     assert err <= TOL[torch.bfloat16], err
 
 
@@ -93,14 +126,36 @@ def test_smollm2_outlier_rows(fn):
     assert check_linear(fn, w, rows=rows) <= TOL[torch.bfloat16]
 
 
-def test_llama7b_qkv_prefill_sampled(fn):
-    w = workloads.llama7b_qkv_prefill()
-    err = check_linear(fn, w, rows=sample_rows(w.M, n=24))
+@pytest.fixture(scope="module")
+def llama_qkv():
+    """The Llama-7B QKV workload (4096 x 4096 -> 12288), drawn once for the tests that use it."""
+    return workloads.llama7b_qkv_prefill()
+
+
+def test_llama7b_qkv_prefill_all_rows(fn, llama_qkv, record_parity):
+    # Every row (so every 256 x 256 output tile) against the oracle, in the launch
+    # configuration the benchmark times; the deferred scale 1/RMSe is checked on its own
+    # at every row (Prop. 2; App. "RMS with epsilon"), and the per-row scale of the output.
+    w = llama_qkv
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV))
+    inv = torch.empty(w.M, dtype=torch.float32, device=DEV)
+    y = fn.flashnorm_linear(w.a.to(DEV), Ws, w.N, w.eps, inv_rms=inv)
+    torch.cuda.synchronize()
+    del Ws
+    ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+    got = to_np(y)
+    err, dev = row_err(got, ref), row_scale_dev(got, ref)
+    want = np.array([1.0 / oracle.rms(r, w.eps) for r in w.a.double().numpy()])
+    inv_err = float(np.max(np.abs(inv.cpu().double().numpy() / want - 1.0)))
+    record_parity("llama7b_qkv_prefill 4096x4096x12288 (all rows)", row_err=err, row_scale_dev=dev,
+                  inv_rms_rel=inv_err)
     assert err <= TOL[torch.bfloat16], err
+    assert dev <= SCALE_TOL, dev
+    assert inv_err <= 1e-5, inv_err
 
 
 @pytest.mark.parametrize("M", [1, 4, 16])
-def test_llama7b_swiglu_decode(fn, M):
+def test_llama7b_swiglu_decode(fn, M, record_parity):
     w = workloads.llama7b_swiglu_decode(M=M)
     a, W = w.a.to(DEV), w.W.to(DEV)
     Ws, _, _ = fn.fold_weights(W, w.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
@@ -109,19 +164,26 @@ def test_llama7b_swiglu_decode(fn, M):
     torch.cuda.synchronize()
     ref = oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)
     err = row_err(to_np(out), ref)
+    record_parity(f"llama7b_swiglu_decode M={M} (all rows)", row_err=err)
     assert err <= TOL[torch.bfloat16], err
 
 
-def test_layernorm_linear_sampled(fn):
+def test_layernorm_linear_all_rows(fn, record_parity):
+    # Every row of the deferred LayerNorm -> linear workload (4096^3) against the oracle's
+    # two-pass standard form, plus the per-row scale (catches an error in 1/sigma).
     w = workloads.layernorm_linear()
     a, W = w.a.to(DEV), w.W.to(DEV)
     Ws, cs, cb = fn.fold_weights(W, w.g.to(DEV), beta=w.beta.to(DEV), colsum=True, c_star=True)
     y = fn.flashnorm_layernorm_linear(a, Ws, cs, cb, w.N, w.eps)
     torch.cuda.synchronize()
-    rows = sample_rows(w.M, n=24)
-    ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps, rows=rows)
-    err = row_err(to_np(y)[rows], ref)
+    ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps)
+    got = to_np(y)
+    # c* = beta W is a row-independent offset: the scale check takes the centred part.
+    cstar = oracle.layernorm_linear(np.zeros((1, w.K)), w.g, w.beta, w.W, 1.0)[0]
+    err, dev = row_err(got, ref), row_scale_dev(got - cstar, ref - cstar)
+    record_parity("layernorm_linear 4096x4096x4096 (all rows)", row_err=err, row_scale_dev=dev)
     assert err <= TOL[torch.bfloat16], err
+    assert dev <= SCALE_TOL, dev
 
 
 # ------------------------------------------------------------------ ragged and edge shapes
@@ -176,6 +238,25 @@ def test_layernorm_ragged(fn, M, K, N, dtype, path):
     assert row_err(to_np(y), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("mean", [48.0])
+@pytest.mark.parametrize("dtype,M,K,N,path", [(torch.bfloat16, 512, 4096, 512, 0),
+                                              (torch.bfloat16, 512, 4096, 512, 1 | (15 << 8)),
+                                              (torch.bfloat16, 16, 4096, 512, 2),
+                                              (torch.float32, 32, 1024, 96, 0)])
+def test_layernorm_large_mean(fn, record_parity, mean, dtype, M, K, N, path):
+    # Rows far from zero mean (|mu| / sigma = 48 and 128): the kernels take the variance in
+    # one pass as E[a^2] - mu^2 (Sec. 3.5 exchanges the centring with the product), which
+    # cancels here; the oracle centres first (two passes).  The per-row scale of the centred
+    # output exposes an error of 1/sigma directly.
+    w = workloads.make("layernorm", M, K, N, dtype=dtype, eps=1e-5, seed=171 + K, a_mean=mean)
+    got, ref = _run_kind(fn, "layernorm", w, path)
+    cstar = oracle.layernorm_linear(np.zeros((1, K)), w.g, w.beta, w.W, 1.0)[0]
+    err, dev = row_err(got, ref), row_scale_dev(got - cstar, ref - cstar)
+    record_parity(f"layernorm |mu|/sigma={mean:g} {str(dtype)[6:]} {M}x{K}x{N} path {path}", row_err=err,
+                  row_scale_dev=dev)
+    assert err <= TOL[dtype], err
+
+
 def test_zero_rows_give_exact_zero(fn):
     w = workloads.make("linear", 40, 128, 48, eps=1e-6, seed=11)
     w.a[[0, 17, 39]] = 0
@@ -187,6 +268,65 @@ def test_zero_rows_give_exact_zero(fn):
         assert torch.all(y[0] == 0)
         if path == 1:
             assert torch.all(y[17] == 0) and torch.all(y[39] == 0)
+
+
+def _run_kind(fn, kind, w, path):
+    """The fused op of a workload kind on the GPU, and the oracle's standard form."""
+    a, W, g = w.a.to(DEV), w.W.to(DEV), w.g.to(DEV)
+    ws_dt = fn.FN_BF16 if w.dtype == torch.bfloat16 else fn.FN_F32
+    if kind == "glu":
+        Ws, _, _ = fn.fold_weights(W, g, layout=fn.FN_LAYOUT_GLU, ws_dtype=ws_dt)
+        y = fn.flashnorm_glu(a, Ws, w.out_features, w.eps, path=path)
+        ref = oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)
+    elif kind == "layernorm":
+        Ws, cs, cb = fn.fold_weights(W, g, beta=w.beta.to(DEV), colsum=True, c_star=True, ws_dtype=ws_dt)
+        y = fn.flashnorm_layernorm_linear(a, Ws, cs, cb, w.N, w.eps, path=path)
+        ref = oracle.layernorm_linear(w.a, w.g, w.beta, w.W, w.eps)
+    else:
+        Ws, _, _ = fn.fold_weights(W, g, ws_dtype=ws_dt)
+        y = fn.flashnorm_linear(a, Ws, w.N, w.eps, path=path)
+        ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+    torch.cuda.synchronize()
+    return to_np(y), ref
+
+
+NONFINITE_CASES = [(torch.bfloat16, 300, 1), (torch.bfloat16, 7, 2), (torch.float32, 20, 0)]
+
+
+@pytest.mark.parametrize("kind", ["linear", "glu", "layernorm"])
+@pytest.mark.parametrize("dtype,M,path", NONFINITE_CASES)
+def test_nonfinite_input_rows_stay_in_their_row(fn, kind, dtype, M, path):
+    # A row holding NaN, +Inf or -Inf: in the standard form its mean square is NaN or Inf,
+    # so every output of that row is NaN (App. "RMS with epsilon"; LayerNorm: Sec. 2).  The
+    # deferred form must give the same, and leave every other row finite and correct.
+    K, N = 200, 72
+    w = workloads.make(kind, M, K, N, dtype=dtype, eps=1e-5, seed=151 + M, a_mean=0.5 if kind == "layernorm" else 0)
+    bad = {1: float("-inf"), 3: float("nan"), M - 2: float("inf")}
+    for r, v in bad.items():
+        w.a[r, (r * 37) % K] = v
+    got, ref = _run_kind(fn, kind, w, path)
+    rows = sorted(bad)
+    assert np.isnan(ref[rows]).all()  # the oracle's standard form
+    assert np.isnan(got[rows]).all(), [int(np.isnan(got[r]).sum()) for r in rows]
+    good = [r for r in range(M) if r not in bad]
+    assert row_err(got[good], ref[good]) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("kind", ["linear", "glu", "layernorm"])
+@pytest.mark.parametrize("dtype,M,path", NONFINITE_CASES)
+def test_eps_zero_all_zero_row_is_nan(fn, kind, dtype, M, path):
+    # With eps = 0 an all-zero row divides 0 by RMS = 0 (LayerNorm: sigma = 0): NaN in the
+    # standard form (App. "RMS with epsilon" explains why eps is there); the deferred form
+    # multiplies a zero accumulator by an infinite scale, also NaN.  Other rows unaffected.
+    K, N = 200, 72
+    w = workloads.make(kind, M, K, N, dtype=dtype, eps=0.0, seed=161 + M, a_mean=0.5 if kind == "layernorm" else 0)
+    zr = M // 2
+    w.a[zr] = 0
+    got, ref = _run_kind(fn, kind, w, path)
+    assert np.isnan(ref[zr]).all()
+    assert np.isnan(got[zr]).all(), int(np.isnan(got[zr]).sum())
+    good = [r for r in range(M) if r != zr]
+    assert row_err(got[good], ref[good]) <= TOL[dtype]
 
 
 def test_negative_g(fn):
@@ -235,6 +375,39 @@ def test_fold_bitwise(fn, K, N, layout, dtype):
         assert np.all(np.abs(cs.cpu().double().numpy() - exp_cs) <= 1e-6 * scale + 1e-30)
         bscale = np.abs(w.beta.double().numpy()[:, None] * w.W.double().numpy()).sum(axis=0)
         assert np.all(np.abs(cb.cpu().double().numpy() - exp_cb) <= 1e-6 * bscale + 1e-30)
+
+
+@pytest.mark.parametrize("view", ["transposed", "strided"])
+@pytest.mark.parametrize("K,N,layout,dtype", [(200, 72, 0, torch.bfloat16), (136, 2 * 45, 1, torch.bfloat16),
+                                              (96, 40, 0, torch.float32)])
+def test_fold_strided_view_bitwise(fn, view, K, N, layout, dtype):
+    # A framework's linear weight is stored [N, K]; fold_weights reads it through its
+    # strides (the transposed view, no copy) and must pack the same bits as the oracle's
+    # fold of the logical [K, N] weight (Prop. 1), with colsum and c* (Sec. 3.4).
+    kind = "glu" if layout else "layernorm"
+    w = workloads.make(kind, 2, K, N // 2 if layout else N, dtype=dtype, seed=K + N + 1)
+    if view == "transposed":
+        Wdev = w.W.t().contiguous().to(DEV).t()          # strides (1, K)
+    else:
+        big = torch.zeros(K, 3 * N + 5, dtype=dtype)      # strides (3N + 5, 3): every third column
+        big[:, ::3][:, :N] = w.W
+        Wdev = big.to(DEV)[:, ::3][:, :N]
+    assert not Wdev.is_contiguous()
+    want_extras = layout == 0
+    Ws, cs, cb = fn.fold_weights(Wdev, w.g.to(DEV), beta=w.beta.to(DEV) if want_extras else None,
+                                 layout=layout, colsum=want_extras, c_star=want_extras)
+    Wref, csr, cbr = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), beta=w.beta.to(DEV) if want_extras else None,
+                                     layout=layout, colsum=want_extras, c_star=want_extras)
+    back = fn.unpack_weights(Ws, K, N, layout, fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32)
+    torch.cuda.synchronize()
+    storage = oracle.STORAGE_BF16 if dtype == torch.bfloat16 else oracle.STORAGE_F32
+    exp_ws, exp_cs, exp_cb = oracle.fold(w.W, w.g, w.beta if want_extras else None, storage=storage)
+    np.testing.assert_array_equal(back.double().cpu().numpy(), exp_ws)
+    assert torch.equal(Ws, Wref)  # the packed buffer does not depend on the view
+    if want_extras:
+        assert torch.equal(cs, csr) and torch.equal(cb, cbr)
+        scale = np.abs(exp_ws).sum(axis=0)
+        assert np.all(np.abs(cs.cpu().double().numpy() - exp_cs) <= 1e-6 * scale + 1e-30)
 
 
 def test_determinism_bitwise(fn):
@@ -305,6 +478,27 @@ def test_long_k_automatic_64_deep_steps(fn, K):
     assert torch.equal(y.cpu().view(torch.int16), y32.cpu().view(torch.int16))
 
 
+@pytest.mark.parametrize("K", [2048, 2088, 2112])
+def test_long_k_automatic_64_deep_steps_128x128(fn, K):
+    # 1024 x K -> 4096 selects the 128 x 128 tile, which takes 64-deep steps from K = 2048:
+    # 32 (even) steps at 2048, 33 (odd) with the lane check (2088) and without it (2112).
+    # Checked against the oracle and bitwise against the 32-deep steps of the same tile.
+    M, N = 1024, 4096
+    lin = workloads.make("linear", M, K, N, eps=1e-5, seed=K + 5, outlier_frac=0.01)
+    ln = workloads.make("layernorm", M, K, N, eps=1e-5, seed=K + 6, a_mean=0.5)
+    Ws, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
+    Wl, cs, cb = fn.fold_weights(ln.W.to(DEV), ln.g.to(DEV), ln.beta.to(DEV), colsum=True, c_star=True)
+    y = fn.flashnorm_linear(lin.a.to(DEV), Ws, N, lin.eps)
+    z = fn.flashnorm_layernorm_linear(ln.a.to(DEV), Wl, cs, cb, N, ln.eps)
+    y32 = fn.flashnorm_linear(lin.a.to(DEV), Ws, N, lin.eps, path=fn.FN_PATH_PREFILL | (13 << 8))
+    z32 = fn.flashnorm_layernorm_linear(ln.a.to(DEV), Wl, cs, cb, N, ln.eps, path=fn.FN_PATH_PREFILL | (13 << 8))
+    torch.cuda.synchronize()
+    assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
+    assert row_err(to_np(z), oracle.layernorm_linear(ln.a, ln.g, ln.beta, ln.W, ln.eps)) <= TOL[torch.bfloat16]
+    assert torch.equal(y.cpu().view(torch.int16), y32.cpu().view(torch.int16))
+    assert torch.equal(z.cpu().view(torch.int16), z32.cpu().view(torch.int16))
+
+
 @pytest.mark.parametrize("K", [192, 200, 576, 1032])
 def test_row_pitch_padding_never_enters(fn, K):
     # The bytes between rows (lda > K) hold NaN.  With K a multiple of 64 the
@@ -324,7 +518,8 @@ def test_row_pitch_padding_never_enters(fn, K):
     Ws, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
     Wg, _, _ = fn.fold_weights(glu.W.to(DEV), glu.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
     Wl, cs, cb = fn.fold_weights(ln.W.to(DEV), ln.g.to(DEV), ln.beta.to(DEV), colsum=True, c_star=True)
-    for path in (0, fn.FN_PATH_PREFILL | (15 << 8), fn.FN_PATH_PREFILL | (4 << 8), fn.FN_PATH_PREFILL | (13 << 8)):
+    for path in (0, fn.FN_PATH_PREFILL | (15 << 8), fn.FN_PATH_PREFILL | (4 << 8), fn.FN_PATH_PREFILL | (13 << 8),
+                 fn.FN_PATH_PREFILL | (18 << 8), fn.FN_PATH_PREFILL | (19 << 8)):
         y = fn.flashnorm_linear(padded(lin.a), Ws, N, lin.eps, path=path)
         o = fn.flashnorm_glu(padded(glu.a), Wg, F, glu.eps, path=path)
         z = fn.flashnorm_layernorm_linear(padded(ln.a), Wl, cs, cb, N, ln.eps, path=path)
@@ -550,13 +745,22 @@ def test_linear_unfolded(fn, dtype, M, K, N, path):
     np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
 
 
-def test_llama7b_qkv_unfolded_sampled(fn):
-    # The full QKV projection, in the tile the benchmark times for it.
-    w = workloads.llama7b_qkv_prefill()
-    y, _ = _unfolded_linear(fn, w)
-    rows = sample_rows(w.M, n=24)
-    err = row_err(to_np(y)[rows], oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps, rows=rows))
+def test_llama7b_qkv_unfolded_sampled(fn, llama_qkv, record_parity):
+    # The full QKV projection, in the tile the benchmark times for it: 16 rows of every
+    # 256-row band (both edges included), so every output tile is compared.
+    w = llama_qkv
+    y, inv = _unfolded_linear(fn, w)
+    rows = tile_rows(w.M)
+    ref = oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps, rows=rows)
+    got = to_np(y)[rows]
+    err, dev = row_err(got, ref), row_scale_dev(got, ref)
+    want = np.array([1.0 / oracle.rms(r, w.eps) for r in w.a.double().numpy()])
+    inv_err = float(np.max(np.abs(inv.cpu().double().numpy() / want - 1.0)))
+    record_parity("llama7b_qkv_prefill unfolded (16 rows per 256-row band)", row_err=err, row_scale_dev=dev,
+                  inv_rms_rel=inv_err)
     assert err <= TOL[torch.bfloat16], err
+    assert dev <= SCALE_TOL, dev
+    assert inv_err <= 1e-5, inv_err
 
 
 @pytest.mark.parametrize("dtype,M,K,F,path", [(torch.bfloat16, 300, 328, 80, 1), (torch.bfloat16, 7, 1032, 72, 2),
@@ -619,10 +823,10 @@ def test_qkv_rope(fn, dtype, M, K, Hq, Hkv, h, path, bias):
     np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
 
 
-def test_llama7b_qkv_rope_sampled(fn):
+def test_llama7b_qkv_rope_sampled(fn, llama_qkv, record_parity):
     # Llama-7B attention input: 32 query and 32 key/value heads of 128, two sequences of
-    # 2048 tokens, in the tile the QKV workload runs in.
-    w = workloads.llama7b_qkv_prefill()
+    # 2048 tokens, in the tile the QKV workload runs in; 16 rows of every 256-row band.
+    w = llama_qkv
     h, H = 128, 32
     cos, sin = workloads.rope_tables(4096, h)
     pos = workloads.positions(w.M, 2048)
@@ -630,10 +834,11 @@ def test_llama7b_qkv_rope_sampled(fn):
     y = fn.flashnorm_qkv_rope(w.a.to(DEV), Ws, H, H, h, w.eps, pos.to(DEV), cos.to(DEV), sin.to(DEV),
                               1.0 / math.sqrt(h))
     torch.cuda.synchronize()
-    rows = sample_rows(w.M, n=16)
+    rows = tile_rows(w.M)
     ref = oracle.rmsnorm_qkv_rope(w.a, w.g, w.W, w.eps, H, H, h, pos.numpy(), cos, sin, 1.0 / math.sqrt(h),
                                   rows=rows)
     err = row_err(to_np(y)[rows], ref)
+    record_parity("llama7b_qkv_prefill + RoPE (16 rows per 256-row band)", row_err=err)
     assert err <= TOL[torch.bfloat16], err
 
 
@@ -770,10 +975,10 @@ def test_qkv_headnorm(fn, M, K, Hq, Hkv, h, with_gv, rope):
     np.testing.assert_allclose(inv.cpu().double().numpy(), want, rtol=2e-6)
 
 
-def test_llama7b_qkv_headnorm_sampled(fn):
+def test_llama7b_qkv_headnorm_sampled(fn, llama_qkv, record_parity):
     # The Llama-7B QKV shape with QK-norm and RoPE (32 + 32 + 32 heads of 128), in the
-    # 256 x 256 tile.
-    w = workloads.llama7b_qkv_prefill()
+    # 256 x 256 tile; 16 rows of every 256-row band.
+    w = llama_qkv
     h, H = 128, 32
     g = torch.Generator().manual_seed(7)
     gq, gk = torch.rand(h, generator=g) + 0.5, torch.rand(h, generator=g) + 0.5
@@ -783,10 +988,11 @@ def test_llama7b_qkv_headnorm_sampled(fn):
     y = fn.flashnorm_qkv_headnorm(w.a.to(DEV), Ws, H, H, h, w.eps, gq.to(DEV), gk.to(DEV), None, 1e-6,
                                   positions=pos.to(DEV), cos_tab=cos.to(DEV), sin_tab=sin.to(DEV), q_scale=h ** -0.5)
     torch.cuda.synchronize()
-    rows = sample_rows(w.M, n=12)
+    rows = tile_rows(w.M)
     ref = oracle.rmsnorm_qkv_headnorm(w.a, w.g, w.W, w.eps, H, H, h, gq, gk, None, 1e-6, pos=pos.numpy(),
                                       cos_tab=cos, sin_tab=sin, q_scale=h ** -0.5, rows=rows)
     err = row_err(to_np(y)[rows], ref)
+    record_parity("llama7b_qkv_prefill + QK-norm + RoPE (16 rows per 256-row band)", row_err=err)
     assert err <= TOL[torch.bfloat16], err
 
 
@@ -975,7 +1181,7 @@ def test_mla_latent_standard_form_without_latent_eps(fn):
     assert row_err(to_np(y), ref) <= TOL[torch.bfloat16]
 
 
-def test_mla_latent_unit_rms_at_full_size(fn):
+def test_mla_latent_unit_rms_at_full_size(fn, record_parity):
     # DeepSeek-V2 width (K = 5120 -> 512 + 64) in the launch configuration the benchmark
     # times: sampled rows against the oracle, and at every row the latent divided by g_lat
     # has RMS 1 (eps_lat = 0) up to the bf16 rounding of the output.
@@ -988,10 +1194,12 @@ def test_mla_latent_unit_rms_at_full_size(fn):
     y = fn.flashnorm_mla_latent(w.a.to(DEV), Ws, L, R, g_lat.to(DEV), 0.0, w.eps, pos.to(DEV), cos.to(DEV),
                                 sin.to(DEV))
     torch.cuda.synchronize()
-    rows = sample_rows(w.M, n=16)
+    rows = tile_rows(w.M, tile=128, per_tile=8)
     ref = oracle.rmsnorm_mla_latent(w.a, w.g, w.W, w.eps, L, g_lat, 0.0, pos.numpy(), cos, sin, rows=rows)
     got = to_np(y)
-    assert row_err(got[rows], ref) <= TOL[torch.bfloat16]
+    err = row_err(got[rows], ref)
+    record_parity("mla_kv_down 4096x5120 -> 512+64 (8 rows per 128-row band)", row_err=err)
+    assert err <= TOL[torch.bfloat16]
     lat = got[:, :L] / g_lat.double().numpy()
     np.testing.assert_allclose(np.sqrt(np.mean(lat * lat, axis=1)), 1.0, atol=4e-3)
 
