@@ -75,7 +75,9 @@ int validate_op(const OpDesc& d, int y_dtype) {
   if (y_dtype != d.dtype) return FN_ERR_DTYPE;
   const int base_path = d.path & 0xff, tile = d.path >> FN_PATH_TILE_SHIFT;
   if (base_path < FN_PATH_AUTO || base_path > FN_PATH_DECODE) return FN_ERR_VALUE;
-  if (tile < 0 || tile >= (base_path == FN_PATH_DECODE ? fn::kDecodeCfgCount : (int)fn::TILE_COUNT))
+  if (tile < 0 || tile >= (base_path == FN_PATH_DECODE ? fn::kDecodeCfgCount
+                            : d.dtype == FN_F32        ? fn::kF32CfgCount
+                                                       : (int)fn::TILE_COUNT))
     return FN_ERR_VALUE;
   if (d.K > kMaxLd) return FN_ERR_SIZE;
   if (d.K % (d.dtype == FN_BF16 ? 8 : 4)) return FN_ERR_SHAPE;
@@ -108,6 +110,7 @@ int run_op(const OpDesc& d) {
   if (d.dtype == FN_F32) {
     fn::F32Args p{(const float*)d.a, (int)d.M, (int)d.K, (int)d.lda, (const float*)d.ws, NP, KP,
                   (int)d.ncols, (float*)d.y, (int)d.ldy, d.epi, d.ep, d.stream, d.gs};
+    p.cfg = d.path >> FN_PATH_TILE_SHIFT;
     return status_of(fn::launch_f32(p));
   }
   const int base_path = d.path & 0xff;
@@ -130,6 +133,7 @@ EpiArgs make_ep(float eps, int64_t K) {
   EpiArgs ep{};
   ep.eps = eps;
   ep.inv_k = 1.0f / (float)K;
+  ep.inv_kd = 1.0 / (double)K;
   return ep;
 }
 

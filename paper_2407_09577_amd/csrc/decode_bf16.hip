@@ -33,8 +33,9 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
 
   // Per-wave partials for the cross-wave combine (unused with one wave).
   __shared__ f32x4 red[KSPLIT > 1 ? KSPLIT : 1][NCB][64];
-  __shared__ float red_ss[KSPLIT > 1 ? KSPLIT : 1][16];
-  __shared__ float red_sa[KSPLIT > 1 ? KSPLIT : 1][16];
+  using ST = StatT<EPI>;
+  __shared__ ST red_ss[KSPLIT > 1 ? KSPLIT : 1][16];
+  __shared__ ST red_sa[KSPLIT > 1 ? KSPLIT : 1][16];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -56,7 +57,7 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
   f32x4 acc[NCB];
 #pragma unroll
   for (int c = 0; c < NCB; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float ss = 0.f, sa = 0.f;
+  ST ss = ST(0), sa = ST(0);
 
   // One set = U k blocks of this wave (kb, kb + KSPLIT, ...): U activation
   // fragments and U x NCB weight fragments, one 16-byte load per lane each.
@@ -89,8 +90,12 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       bf16x8 av = __builtin_bit_cast(bf16x8, af[u]);
-      if constexpr (kSS) ss = sumsq8(av, ss);
-      if constexpr (kSA) sa = sum8(av, sa);
+      if constexpr (kSA) {  // LayerNorm: the fragment's fp32 partials, added in fp64
+        ss += (double)sumsq8(av, 0.0f);
+        sa += (double)sum8(av, 0.0f);
+      } else if constexpr (kSS) {
+        ss = sumsq8(av, ss);
+      }
       if constexpr (GS) {  // a_k g_k, rounded once to bf16
         float o[8];
 #pragma unroll
@@ -163,9 +168,9 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
 
   const int m = lrow;
   if (m >= M) return;
-  float ss_t = ss, sa_t = sa;
+  ST ss_t = ss, sa_t = sa;
   if constexpr (KSPLIT > 1) {
-    ss_t = sa_t = 0.f;
+    ss_t = sa_t = ST(0);
 #pragma unroll
     for (int w = 0; w < KSPLIT; ++w) {
       ss_t += red_ss[w][m];

@@ -195,6 +195,7 @@ constexpr bool epi_exports_s(int e) {
 struct EpiArgs {
   float eps;
   float inv_k;          // 1/K
+  double inv_kd;        // 1/K in fp64 (LayerNorm statistics)
   const float* bias;    // EPI_RMS: optional [N]
   const float* colsum;  // EPI_LN: [N]
   const float* cstar;   // EPI_LN: optional [N]

@@ -8,19 +8,30 @@
 // bias / GLU / LayerNorm mean correction, and rounds once to bf16 on the store.
 #pragma once
 
+#include <type_traits>
+
 #include "fn_device.h"
 
 namespace fn {
 
+// Accumulator type of a kind's row sums.  LayerNorm takes its variance in one pass as
+// E[a^2] - mu^2, which cancels when |mu| >> sigma (the two terms agree in their leading
+// digits): its sums are kept in fp64.  The kernels add exact-or-nearly-exact fp32
+// partials of a few elements (the squares of bf16 values are exact in fp32) into the
+// fp64 totals, so the sums and the variance carry no fp32 accumulation error.
+template <int EPI>
+using StatT = std::conditional_t<EPI == EPI_LN, double, float>;
+
 struct RowStat {
   float s;   // 1/RMSe(a) (RMSNorm kinds), 1/MSe(a) (ReGLU, bilinear), 1/sigma (LayerNorm),
              // the given row scale (EPI_ROWSCALE); 1 for the baselines
-  float mu;  // LayerNorm mean (0 otherwise)
+  float mu;  // LayerNorm mean of the values the product consumed (of a - p where the
+             // kernel shifts the activations by a pivot p; 0 for the other kinds)
   int pos;   // EPI_ROPE: the token's position (0 otherwise)
 };
 
 template <int EPI>
-__device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& ep) {
+__device__ __forceinline__ RowStat row_stat(StatT<EPI> ss, StatT<EPI> sa, const EpiArgs& ep) {
   RowStat st{1.0f, 0.0f, 0};
   if constexpr (EPI == EPI_RMS || EPI == EPI_GLU || EPI == EPI_GLU_DEFER || EPI == EPI_RELU_DEFER ||
                 EPI == EPI_ROPE || EPI == EPI_HEADNORM) {
@@ -31,13 +42,13 @@ __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& e
     // and Bilinear GLU"; ReLU(s t) = s ReLU(t) for s >= 0)
     st.s = 1.0f / fmaf(ss, ep.inv_k, ep.eps);
   } else if constexpr (EPI == EPI_LN) {
-    float mu = sa * ep.inv_k;
-    // one-pass variance, clamped at 0 against cancellation; a NaN (a row holding NaN or
+    // mu = sa/K, var = ss/K - mu^2 in fp64, clamped at 0; a NaN (a row holding NaN or
     // Inf) stays NaN, so that row's outputs are NaN as in the standard form
-    float var = fmaf(ss, ep.inv_k, -mu * mu);
-    var = var < 0.0f ? 0.0f : var;
-    st.mu = mu;
-    st.s = rsqrtf(var + ep.eps);
+    const double mu = sa * ep.inv_kd;
+    double var = fma(ss, ep.inv_kd, -mu * mu);
+    var = var < 0.0 ? 0.0 : var;
+    st.mu = (float)mu;
+    st.s = rsqrtf((float)(var + (double)ep.eps));
   }
   (void)ss;
   (void)sa;
@@ -48,7 +59,7 @@ __device__ __forceinline__ RowStat row_stat(float ss, float sa, const EpiArgs& e
 // Row statistics of output row m (< M for the rows that are stored): the kinds
 // that apply a scale computed elsewhere read it here.
 template <int EPI>
-__device__ __forceinline__ RowStat row_stat_at(float ss, float sa, const EpiArgs& ep, int m, int M) {
+__device__ __forceinline__ RowStat row_stat_at(StatT<EPI> ss, StatT<EPI> sa, const EpiArgs& ep, int m, int M) {
   RowStat st = row_stat<EPI>(ss, sa, ep);
   if constexpr (EPI == EPI_ROWSCALE) st.s = m < M ? ep.row_scale[m] : 0.0f;
   if constexpr (EPI == EPI_ROPE) st.pos = m < M ? ep.rope_pos[m] : 0;

@@ -91,9 +91,12 @@ struct F32Args {
   int epi;
   EpiArgs ep;
   hipStream_t stream;
-  bool gs;  // run-time g (ep.g_rt) applied to the activations; unfolded W
+  bool gs;      // run-time g (ep.g_rt) applied to the activations; unfolded W
+  int cfg = 0;  // tile configuration (0 = automatic), see launch_f32
 };
 hipError_t launch_f32(const F32Args& p);
+// fp32 tile configurations: 0 automatic, 1 = 64-row tiles, 2 = 16-row tiles with four k groups.
+constexpr int kF32CfgCount = 3;
 
 struct FoldArgs {
   const void* W;

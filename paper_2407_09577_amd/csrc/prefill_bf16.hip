@@ -170,9 +170,18 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   for (int i = 0; i < FN; ++i)
 #pragma unroll
     for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float ss[FM], sa[FM];
+  // Row sums.  In the K loop a wave keeps only the row blocks whose statistics it
+  // takes (row block WNC + WN t is its t-th, see multiply_interleaved); after the loop
+  // ss / sa hold the totals of all FM row blocks of its sub-tile.
+  using ST = StatT<EPI>;
+  static_assert(!(kSS || kSA) || GS || FM % WN == 0, "each wave takes whole row blocks' statistics");
+  constexpr int TW = (FM / WN) > 0 ? FM / WN : 1;
+  ST ssw[TW], saw[TW];
 #pragma unroll
-  for (int j = 0; j < FM; ++j) ss[j] = sa[j] = 0.f;
+  for (int t = 0; t < TW; ++t) ssw[t] = saw[t] = ST(0);
+  ST ss[FM], sa[FM];
+#pragma unroll
+  for (int j = 0; j < FM; ++j) ss[j] = sa[j] = ST(0);
 
   bf16x8 af0[FMK], wf0[FNK];
   bf16x8 af1[PF ? FMK : 1], wf1[PF ? FNK : 1];
@@ -192,10 +201,16 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 
   // Row statistics of fragment j (row block j % FM): squares (and sums, for
   // LayerNorm) of its 8 elements per lane, as packed bf16 dot products
-  // accumulated in fp32.
+  // accumulated in fp32 (LayerNorm: the fragment's fp32 partials, added in fp64).
+  // j % FM is WNC + WN t for this wave's mainloop copy WNC.
   auto stats_one = [&](int j, const bf16x8 (&af)[FMK]) __attribute__((always_inline)) {
-    if constexpr (kSS) ss[j % FM] = sumsq8(af[j], ss[j % FM]);
-    if constexpr (kSA) sa[j % FM] = sum8(af[j], sa[j % FM]);
+    const int t = (j % FM) / WN;
+    if constexpr (kSA) {
+      ssw[t] += (double)sumsq8(af[j], 0.0f);
+      saw[t] += (double)sum8(af[j], 0.0f);
+    } else if constexpr (kSS) {
+      ssw[t] = sumsq8(af[j], ssw[t]);
+    }
   };
 
   // GS: scale the activation fragments of block b in place, g applied per k
@@ -407,34 +422,32 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     for (int j = 0; j < FM; ++j) ss[j] = row_tot[0][wm * TM + j * 16 + lrow];
   } else
   // Row statistics: lanes l, l^16, l^32, l^48 hold disjoint k of the same row.
-  // Each fragment's totals live in the one wave of the row band that squared it;
-  // they reach the other WN-1 waves through LDS.
+  // Row block WN t + wn's totals live in this wave (the one of the row band that
+  // squared it); they reach the other WN-1 waves through LDS.
   if constexpr (kSS || kSA) {
 #pragma unroll
-    for (int j = 0; j < FM; ++j) {
+    for (int t = 0; t < TW; ++t) {
       if constexpr (kSS) {
-        ss[j] += __shfl_xor(ss[j], 16);
-        ss[j] += __shfl_xor(ss[j], 32);
+        ssw[t] += __shfl_xor(ssw[t], 16);
+        ssw[t] += __shfl_xor(ssw[t], 32);
       }
       if constexpr (kSA) {
-        sa[j] += __shfl_xor(sa[j], 16);
-        sa[j] += __shfl_xor(sa[j], 32);
+        saw[t] += __shfl_xor(saw[t], 16);
+        saw[t] += __shfl_xor(saw[t], 32);
       }
     }
     if constexpr (WN > 1) {
       // The totals reuse the ring: wait for this wave's last (zero-filling)
       // transfers, and for every wave to finish reading the last block.
-      static_assert(STAGES * STAGE >= 2 * BM * (int)sizeof(float), "ring too small for row totals");
-      float (*row_tot)[BM] = reinterpret_cast<float (*)[BM]>(smem);
+      static_assert(STAGES * STAGE >= 2 * BM * (int)sizeof(ST), "ring too small for row totals");
+      ST (*row_tot)[BM] = reinterpret_cast<ST (*)[BM]>(smem);
       wait_vmcnt<0>();
       __syncthreads();
       if (lane < 16) {
 #pragma unroll
-        for (int j = 0; j < FM; ++j) {
-          if (j % WN == wn) {
-            row_tot[0][wm * TM + j * 16 + lane] = ss[j];
-            row_tot[1][wm * TM + j * 16 + lane] = sa[j];
-          }
+        for (int t = 0; t < TW; ++t) {
+          row_tot[0][wm * TM + (wn + WN * t) * 16 + lane] = ssw[t];
+          row_tot[1][wm * TM + (wn + WN * t) * 16 + lane] = saw[t];
         }
       }
       __syncthreads();
@@ -442,6 +455,12 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       for (int j = 0; j < FM; ++j) {
         ss[j] = row_tot[0][wm * TM + j * 16 + lrow];
         sa[j] = row_tot[1][wm * TM + j * 16 + lrow];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < FM; ++j) {
+        ss[j] = ssw[j];
+        sa[j] = saw[j];
       }
     }
   }

@@ -238,16 +238,21 @@ def test_layernorm_ragged(fn, M, K, N, dtype, path):
     assert row_err(to_np(y), ref) <= TOL[dtype]
 
 
-@pytest.mark.parametrize("mean", [48.0])
-@pytest.mark.parametrize("dtype,M,K,N,path", [(torch.bfloat16, 512, 4096, 512, 0),
-                                              (torch.bfloat16, 512, 4096, 512, 1 | (15 << 8)),
-                                              (torch.bfloat16, 16, 4096, 512, 2),
-                                              (torch.float32, 32, 1024, 96, 0)])
+LARGE_MEAN_CASES = [(mean, *case) for mean in (48.0, 128.0)
+                    for case in [(torch.bfloat16, 512, 4096, 512, 0), (torch.bfloat16, 512, 4096, 512, 1 | (15 << 8)),
+                                 (torch.bfloat16, 16, 4096, 512, 2), (torch.float32, 32, 1024, 96, 0),
+                                 (torch.float32, 100, 1024, 96, 1 << 8)]]
+# fp32 only at 1024: bf16 has a spacing of 8 there, so N(1024, 1) rounds to constant rows
+LARGE_MEAN_CASES += [(1024.0, torch.float32, 32, 1024, 96, 0), (1024.0, torch.float32, 100, 1024, 96, 1 << 8)]
+
+
+@pytest.mark.parametrize("mean,dtype,M,K,N,path", LARGE_MEAN_CASES)
 def test_layernorm_large_mean(fn, record_parity, mean, dtype, M, K, N, path):
-    # Rows far from zero mean (|mu| / sigma = 48 and 128): the kernels take the variance in
-    # one pass as E[a^2] - mu^2 (Sec. 3.5 exchanges the centring with the product), which
-    # cancels here; the oracle centres first (two passes).  The per-row scale of the centred
-    # output exposes an error of 1/sigma directly.
+    # Rows far from zero mean (|mu| / sigma = 48, 128, fp32 also 1024): the kernels take the variance
+    # in one pass as E[a^2] - mu^2 (Sec. 3.5 exchanges the centring with the product), which
+    # cancels in fp32 (the former fp32 sums missed the bf16 gate at 128); the sums are now
+    # fp64, and the fp32 kernel also shifts the rows by a pivot.  The oracle centres first
+    # (two passes).  The per-row scale of the centred output exposes an error of 1/sigma.
     w = workloads.make("layernorm", M, K, N, dtype=dtype, eps=1e-5, seed=171 + K, a_mean=mean)
     got, ref = _run_kind(fn, "layernorm", w, path)
     cstar = oracle.layernorm_linear(np.zeros((1, K)), w.g, w.beta, w.W, 1.0)[0]
@@ -255,6 +260,19 @@ def test_layernorm_large_mean(fn, record_parity, mean, dtype, M, K, N, path):
     record_parity(f"layernorm |mu|/sigma={mean:g} {str(dtype)[6:]} {M}x{K}x{N} path {path}", row_err=err,
                   row_scale_dev=dev)
     assert err <= TOL[dtype], err
+    assert dev <= (SCALE_TOL if dtype == torch.bfloat16 else TOL[dtype]), dev
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+@pytest.mark.parametrize("kind", ["linear", "glu", "layernorm"])
+@pytest.mark.parametrize("M,K,N", [(37, 96, 40), (70, 200, 136), (16, 576, 576), (130, 1032, 72)])
+def test_fp32_tile_configs(fn, cfg, kind, M, K, N):
+    # Both fp32 configurations (64-row tiles; 16-row tiles with K split over four thread
+    # groups, added in a fixed order) on ragged shapes, against the oracle at 1e-5.
+    w = workloads.make(kind, M, K, N, dtype=torch.float32, eps=1e-5, seed=181 + M + K + cfg,
+                       a_mean=0.5 if kind == "layernorm" else 0.0, outlier_frac=0.05)
+    got, ref = _run_kind(fn, kind, w, cfg << 8)
+    assert row_err(got, ref) <= TOL[torch.float32]
 
 
 def test_zero_rows_give_exact_zero(fn):
