@@ -177,8 +177,14 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   static_assert(!(kSS || kSA) || GS || FM % WN == 0, "each wave takes whole row blocks' statistics");
   constexpr int TW = (FM / WN) > 0 ? FM / WN : 1;
   ST ssw[TW], saw[TW];
+  // LayerNorm: fp32 partials of up to four k blocks (at most 64 elements per lane, whose
+  // squares and sums are exact in fp32 when the values are of one magnitude, the case
+  // where the variance would cancel), flushed into the fp64 totals.
+  float tss[kSA ? TW : 1], tsa[kSA ? TW : 1];
 #pragma unroll
   for (int t = 0; t < TW; ++t) ssw[t] = saw[t] = ST(0);
+#pragma unroll
+  for (int t = 0; t < (kSA ? TW : 1); ++t) tss[t] = tsa[t] = 0.0f;
   ST ss[FM], sa[FM];
 #pragma unroll
   for (int j = 0; j < FM; ++j) ss[j] = sa[j] = ST(0);
@@ -206,10 +212,20 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   auto stats_one = [&](int j, const bf16x8 (&af)[FMK]) __attribute__((always_inline)) {
     const int t = (j % FM) / WN;
     if constexpr (kSA) {
-      ssw[t] += (double)sumsq8(af[j], 0.0f);
-      saw[t] += (double)sum8(af[j], 0.0f);
+      tss[t] = sumsq8(af[j], tss[t]);
+      tsa[t] = sum8(af[j], tsa[t]);
     } else if constexpr (kSS) {
       ssw[t] = sumsq8(af[j], ssw[t]);
+    }
+  };
+  auto flush_ln = [&]() __attribute__((always_inline)) {
+    if constexpr (kSA) {
+#pragma unroll
+      for (int t = 0; t < TW; ++t) {
+        ssw[t] += (double)tss[t];
+        saw[t] += (double)tsa[t];
+        tss[t] = tsa[t] = 0.0f;
+      }
     }
   };
 
@@ -354,6 +370,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         sync_block();
         scale_fetch(kb + 3);
         multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true, true);
+        if (kb & 2) flush_ln();  // every fourth block
       }
       auto tail_even = [&]() __attribute__((always_inline)) {
         wait_vmcnt<kAheadWait>();
@@ -372,6 +389,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         __builtin_amdgcn_s_waitcnt(0xc07f);
         multiply_interleaved(wnc, nkb - 1, af0, wf0, af1, wf1, false);
       }
+      flush_ln();
     } else {
       for (int kb = 0; kb < nkb; ++kb) {
         wait_vmcnt<(STAGES - 2) * LOADS>();
@@ -387,7 +405,9 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
           const int h = t / (FN * FM), i = t % (FN * FM) / FM, j = t % FM;
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[h * FN + i], af0[h * FM + j], acc[i][j], 0, 0, 0);
         }
+        if ((kb & 3) == 3) flush_ln();
       }
+      flush_ln();
     }
   };
   // One copy of the main loop per column-wave index (wave-uniform dispatch); a
