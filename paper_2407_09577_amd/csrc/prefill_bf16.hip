@@ -177,9 +177,10 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   static_assert(!(kSS || kSA) || GS || FM % WN == 0, "each wave takes whole row blocks' statistics");
   constexpr int TW = (FM / WN) > 0 ? FM / WN : 1;
   ST ssw[TW], saw[TW];
-  // LayerNorm: fp32 partials of up to four k blocks (at most 64 elements per lane, whose
+  // LayerNorm: fp32 partials of four 32-deep k blocks (32 elements per lane, whose
   // squares and sums are exact in fp32 when the values are of one magnitude, the case
-  // where the variance would cancel), flushed into the fp64 totals.
+  // where the variance would cancel), flushed into the fp64 totals.  The grouping is
+  // by 32-deep blocks whatever the ring step depth, so both depths round alike.
   float tss[kSA ? TW : 1], tsa[kSA ? TW : 1];
 #pragma unroll
   for (int t = 0; t < TW; ++t) ssw[t] = saw[t] = ST(0);
@@ -370,7 +371,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         sync_block();
         scale_fetch(kb + 3);
         multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true, true);
-        if (kb & 2) flush_ln();  // every fourth block
+        if (((kb + 2) * KD) % 4 == 0) flush_ln();  // every fourth 32-deep block
       }
       auto tail_even = [&]() __attribute__((always_inline)) {
         wait_vmcnt<kAheadWait>();
@@ -405,7 +406,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
           const int h = t / (FN * FM), i = t % (FN * FM) / FM, j = t % FM;
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf0[h * FN + i], af0[h * FM + j], acc[i][j], 0, 0, 0);
         }
-        if ((kb & 3) == 3) flush_ln();
+        if (((kb + 1) * KD) % 4 == 0) flush_ln();
       }
       flush_ln();
     }
