@@ -280,6 +280,23 @@ int flashnorm_glu_unfolded(const void* a, int64_t M, int64_t K, int64_t lda, int
 int baseline_rmsnorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
                             const float* g, const void* W_packed, int64_t N, float eps, void* x_ws,
                             void* y, int64_t ldy, int path, void* stream);
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): baseline_rmsnorm_linear without the
+ * x_ws argument.  The normalised activations go to a workspace the library holds in a
+ * static device array of FN_NOALLOC_SCRATCH_BYTES (32 MiB) on each GPU it runs on,
+ * kept until the process ends; the call itself allocates nothing (no hipMalloc, no
+ * hipFree, no allocating library routine).
+ *   M * K * sizeof(a_dtype) above FN_NOALLOC_SCRATCH_BYTES: FN_ERR_SIZE, nothing launched.
+ *   The first call on a device looks up that device's array (FN_ERR_HIP if that fails).
+ *   Every call on one GPU shares that GPU's array: calls that overlap on one GPU (on
+ *   different streams, or from different threads) race and give undefined results;
+ *   calls on one stream are ordered and safe.  The array keeps the last call's
+ *   normalised activations; each call overwrites all it reads, so nothing needs clearing.
+ * Other arguments, results and errors as for baseline_rmsnorm_linear. */
+#define FN_NOALLOC_SCRATCH_BYTES (32 * 1024 * 1024)
+int baseline_rmsnorm_linear_noalloc(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
+                                    const float* g, const void* W_packed, int64_t N, float eps,
+                                    void* y, int64_t ldy, int path, void* stream);
 int baseline_rmsnorm_glu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype,
                          const float* g, const void* W_packed_gu, int64_t F, float eps,
                          void* x_ws, void* out, int64_t ldo, int path, void* stream);

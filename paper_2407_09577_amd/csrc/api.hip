@@ -4,10 +4,36 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "flashnorm.h"
 #include "fn_launch.h"
 
+// The one piece of library-owned device memory: the workspace of
+// baseline_rmsnorm_linear_noalloc, for callers that cannot allocate (see the header).
+// Every GPU the library runs on holds its own copy until the process ends.  In host
+// code this name is only a handle: its device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[FN_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+// Device address of `scratch` on the current device, looked up once per device (with
+// that device current) and kept; nullptr if the lookup fails.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
 
 using fn::EpiArgs;
 
@@ -492,6 +518,21 @@ int baseline_rmsnorm_linear(const void* a, int64_t M, int64_t K, int64_t lda, in
                             const void* W_packed, int64_t N, float eps, void* x_ws, void* y, int64_t ldy,
                             int path, void* stream) {
   return baseline_common(a, M, K, lda, a_dtype, g, nullptr, W_packed, N, 0, eps, x_ws, y, ldy, path, stream);
+}
+
+int baseline_rmsnorm_linear_noalloc(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,
+                                    const void* W_packed, int64_t N, float eps, void* y, int64_t ldy, int path,
+                                    void* stream) {
+  if (!dtype_ok(a_dtype)) return FN_ERR_DTYPE;
+  if (M < 0 || K <= 0) return FN_ERR_SHAPE;
+  if (M == 0)  // validated and done, without touching the device
+    return baseline_common(a, M, K, lda, a_dtype, g, nullptr, W_packed, N, 0, eps, nullptr, y, ldy, path, stream);
+  if (M * K * elem_size(a_dtype) > FN_NOALLOC_SCRATCH_BYTES) return FN_ERR_SIZE;
+  void* ws = scratch_on_current_device();
+  if (!ws) return FN_ERR_HIP;
+  // The normalisation kernel writes every element of the [M, K] workspace before the
+  // product reads it, so nothing needs clearing between calls.
+  return baseline_common(a, M, K, lda, a_dtype, g, nullptr, W_packed, N, 0, eps, ws, y, ldy, path, stream);
 }
 
 int baseline_rmsnorm_glu(const void* a, int64_t M, int64_t K, int64_t lda, int a_dtype, const float* g,

@@ -56,6 +56,7 @@ def _load():
         "baseline_rmsnorm_linear": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P], I),
         "baseline_rmsnorm_glu": ([P, I64, I64, I64, I, P, P, I64, F, P, P, I64, I, P], I),
         "baseline_layernorm_linear": ([P, I64, I64, I64, I, P, P, P, I64, F, P, P, I64, I, P], I),
+        "baseline_rmsnorm_linear_noalloc": ([P, I64, I64, I64, I, P, P, I64, F, P, I64, I, P], I),
         "flashnorm_glu_act": ([P, I64, I64, I64, I, P, I64, F, I, P, I64, I, P, I, P], I),
         "flashnorm_linear_relu": ([P, I64, I64, I64, I, P, I64, F, P, I64, I, P, I, P], I),
         "rowscale_linear": ([P, I64, I64, I64, I, P, I64, P, P, I64, I, I, P], I),
@@ -446,6 +447,22 @@ def baseline_rmsnorm_linear(a, g, W_packed, N, eps, x_ws=None, out=None, path=FN
     _check(_load().baseline_rmsnorm_linear(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed),
                                            N, eps, _ptr(x), _ptr(y), _ld(y), path, _stream(stream)),
            "baseline_rmsnorm_linear")
+    return y
+
+
+FN_NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024
+
+
+def baseline_rmsnorm_linear_noalloc(a, g, W_packed, N, eps, out=None, path=FN_PATH_AUTO, stream=None):
+    """baseline_rmsnorm_linear with the library's static device workspace (no x_ws):
+    the C call allocates nothing; pass ``out`` to allocate nothing here either."""
+    M, K = a.shape
+    _guard("baseline_rmsnorm_linear_noalloc", (a, g, W_packed, out),
+           packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
+    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    _check(_load().baseline_rmsnorm_linear_noalloc(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")),
+                                                   _ptr(W_packed), N, eps, _ptr(y), _ld(y), path, _stream(stream)),
+           "baseline_rmsnorm_linear_noalloc")
     return y
 
 

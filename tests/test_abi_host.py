@@ -351,3 +351,17 @@ def test_binding_rejects_host_tensors(fnlib):
         fnlib.fold_weights(_bf16(K, N), torch.ones(K))
     with pytest.raises(ValueError, match="GPU tensor"):
         fnlib.flashnorm_layernorm_linear(_bf16(M, K), Ws, torch.zeros(N), None, N, 1e-6)
+
+
+def test_noalloc_baseline_validation(fnlib):
+    # The static-workspace entry point rejects activations larger than its array before
+    # touching the device, and M == 0 is a no-op (no device call at all).
+    lib = fnlib.lib()
+    f = lambda **kw: lib.baseline_rmsnorm_linear_noalloc(A, kw.get("M", 4), kw.get("K", 64), kw.get("K", 64),
+                                                         kw.get("dt", 1), X, W, 32, 1e-6, Y, 32, 0, None)
+    cap = fnlib.FN_NOALLOC_SCRATCH_BYTES
+    assert f(M=cap // (2 * 4096) + 1, K=4096) == -9      # one row more than fits (bf16)
+    assert f(M=cap // (4 * 4096) + 1, K=4096, dt=0) == -9  # fp32
+    assert f(M=-1) == -2
+    assert f(dt=7) == -3
+    assert f(M=0) == 0
