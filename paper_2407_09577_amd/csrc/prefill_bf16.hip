@@ -24,6 +24,12 @@
 
 namespace fn {
 
+// Activation fragment order in LDS (see the kernel): half-wave-major when true,
+// row-major with an XOR swizzle when false.  Measured on MI355X, the half-wave order's
+// faster fragment reads do not shorten the Llama-7B QKV projection (319.6 vs 318.3 us)
+// and its two-row transfer groups cost the 128-row tiles 3-6%, so row-major stays.
+constexpr bool kActHalfWave = false;
+
 // Wait until at most `ahead` k blocks of this wave's ring transfers (LOADS each)
 // are still outstanding, i.e. everything issued before them has landed.
 // `ahead` is wave-uniform and at most A; the counter needs an immediate, so the
@@ -112,15 +118,21 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // Fragment f of a stage: f < A_FRAGS is activation row block f, otherwise weight
   // column block f - A_FRAGS.  Wave w moves fragments w, w + NW, ...
   const int lrow = lane & 15;
-  // Activation transfers move 16 rows x 64 bytes per fragment with lane i on
-  // row i / 4, so 4 consecutive lanes read 64 contiguous bytes (one coalesced
-  // access); row r's four 16-byte chunks are stored in the order chunk ^ swz(r),
-  // which keeps the fragment reads (lane L: row L % 16, chunk L / 16) free of
-  // LDS bank conflicts.
+  // Activation fragment layout in LDS.  A transfer writes lane i's 16 bytes to unit i
+  // of the fragment, and the matrix-core operand needs lane L to read row L % 16,
+  // k chunk L / 16.  Half-wave-major order: unit u holds row (u / 2) % 16, chunk
+  // 2 (u / 32) + u % 2, so two consecutive transfer lanes read 32 contiguous bytes of
+  // one row, and the fragment reads (unit 32 (q / 2) + 2 m + q % 2 for row m, chunk q)
+  // run at ~185 B/clk per CU on MI355X.  Row-major orders (unit 4 r + chunk, with or
+  // without an XOR swizzle of the chunks) let four lanes read one 64-byte row segment
+  // but their fragment reads run at ~125 B/clk (linear unit order: ~230).
+  const int t_row = kActHalfWave ? (lane >> 1) & 15 : lane >> 2;  // row of this lane's transfer
   auto swz = [](int r) { return ((r >> 1) ^ (r >> 3)) & 3; };
-  const int t_row = lane >> 2;
-  const int lk = ((lane & 3) ^ swz(t_row)) * 8;  // k offset of this lane's transfer chunk
-  const unsigned a_rd = (unsigned)((lrow * 4 + ((lane >> 4) ^ swz(lrow))) * 16);
+  const int lk = kActHalfWave ? (2 * (lane >> 5) + (lane & 1)) * 8            // k offset of the chunk
+                              : ((lane & 3) ^ swz(t_row)) * 8;
+  const unsigned a_rd = kActHalfWave
+                            ? (unsigned)((32 * (lane >> 5) + 2 * lrow + ((lane >> 4) & 1)) * 16)
+                            : (unsigned)((lrow * 4 + ((lane >> 4) ^ swz(lrow))) * 16);
   // Weight column blocks past the packed width (last column tile only) read the
   // next k block's fragments, or zeros past the buffer's end; the columns they
   // feed lie beyond every output column and are never stored.
@@ -173,19 +185,38 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // Row sums.  In the K loop a wave keeps only the row blocks whose statistics it
   // takes (row block WNC + WN t is its t-th, see multiply_interleaved); after the loop
   // ss / sa hold the totals of all FM row blocks of its sub-tile.
+  //
+  // The RMS kinds take the sums of squares on the matrix cores, from the activation
+  // fragments the product consumes: for a fragment F (16 rows m x 32 k) the product
+  // F F^T is the 16 x 16 Gram block whose diagonal holds each row's sum of squares over
+  // the fragment; added block after block they give the totals over K.  Measured on
+  // MI355X, one extra 16x16x32 op per fragment costs about a third of the four packed
+  // dot products it replaces, which compete for the same pipe.  Row m's diagonal
+  // element sits in lane 20 (m / 4) + m % 4, component m % 4.
+  //
+  // LayerNorm (sums and squares) keeps packed dot products: fp32 partials of four
+  // 32-deep k blocks (32 elements per lane, whose squares and sums are exact in fp32
+  // when the values are of one magnitude, the case where the variance would cancel)
+  // flushed into fp64 totals.  The grouping is by 32-deep blocks whatever the ring step
+  // depth, so both depths round alike.  (Its Gram and all-ones products need 16 more
+  // registers in the loop than the 256-wide tile has.)
   using ST = StatT<EPI>;
   static_assert(!(kSS || kSA) || GS || FM % WN == 0, "each wave takes whole row blocks' statistics");
   constexpr int TW = (FM / WN) > 0 ? FM / WN : 1;
-  ST ssw[TW], saw[TW];
-  // LayerNorm: fp32 partials of four 32-deep k blocks (32 elements per lane, whose
-  // squares and sums are exact in fp32 when the values are of one magnitude, the case
-  // where the variance would cancel), flushed into the fp64 totals.  The grouping is
-  // by 32-deep blocks whatever the ring step depth, so both depths round alike.
+  constexpr bool kGram = kSS && !kSA && !GS;
+  f32x4 gsq[kGram ? TW : 1];
   float tss[kSA ? TW : 1], tsa[kSA ? TW : 1];
+  ST ssw[TW], saw[TW];
 #pragma unroll
   for (int t = 0; t < TW; ++t) ssw[t] = saw[t] = ST(0);
 #pragma unroll
+  for (int t = 0; t < (kGram ? TW : 1); ++t) gsq[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
   for (int t = 0; t < (kSA ? TW : 1); ++t) tss[t] = tsa[t] = 0.0f;
+  // This lane's Gram component: the diagonal one when the lane holds a diagonal element.
+  auto diag_of = [&](const f32x4& g) __attribute__((always_inline)) {
+    return (lane & 2) ? ((lane & 1) ? g[3] : g[2]) : ((lane & 1) ? g[1] : g[0]);
+  };
   ST ss[FM], sa[FM];
 #pragma unroll
   for (int j = 0; j < FM; ++j) ss[j] = sa[j] = ST(0);
@@ -206,17 +237,16 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     }
   };
 
-  // Row statistics of fragment j (row block j % FM): squares (and sums, for
-  // LayerNorm) of its 8 elements per lane, as packed bf16 dot products
-  // accumulated in fp32 (LayerNorm: the fragment's fp32 partials, added in fp64).
-  // j % FM is WNC + WN t for this wave's mainloop copy WNC.
+  // Row statistics of fragment j (row block j % FM): its Gram block added on the
+  // matrix cores (RMS kinds), or its squares and sums as packed bf16 dot products
+  // (LayerNorm).  j % FM is WNC + WN t for this wave's mainloop copy WNC.
   auto stats_one = [&](int j, const bf16x8 (&af)[FMK]) __attribute__((always_inline)) {
     const int t = (j % FM) / WN;
     if constexpr (kSA) {
       tss[t] = sumsq8(af[j], tss[t]);
       tsa[t] = sum8(af[j], tsa[t]);
-    } else if constexpr (kSS) {
-      ssw[t] = sumsq8(af[j], ssw[t]);
+    } else if constexpr (kGram) {
+      gsq[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[j], af[j], gsq[t], 0, 0, 0);
     }
   };
   auto flush_ln = [&]() __attribute__((always_inline)) {
@@ -423,18 +453,19 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
     default: if constexpr (WN > 3) mainloop(std::integral_constant<int, 3>{}); break;
   }
 
-  // GS: the squares were taken by the wave that scaled each row block: lanes
-  // 4r .. 4r+3 hold disjoint k of row r.  Totals reach the waves through LDS.
+  // GS: the squares were taken by the wave that scaled each row block: the four
+  // transfer lanes of row r (half-wave order: 2r, 2r+1, 2r+32, 2r+33; row-major:
+  // 4r .. 4r+3) hold disjoint k of it.  Totals reach the waves through LDS.
   if constexpr (GS) {
     float (*row_tot)[BM] = reinterpret_cast<float (*)[BM]>(smem);
 #pragma unroll
     for (int t = 0; t < SPW; ++t) {
       ss_own[t] += __shfl_xor(ss_own[t], 1);
-      ss_own[t] += __shfl_xor(ss_own[t], 2);
+      ss_own[t] += __shfl_xor(ss_own[t], kActHalfWave ? 32 : 2);
     }
     wait_vmcnt<0>();
     __syncthreads();
-    if ((lane & 3) == 0) {
+    if ((lane & (kActHalfWave ? 33 : 3)) == 0) {
 #pragma unroll
       for (int t = 0; t < SPW; ++t) row_tot[0][(wave + NW * t) * 16 + t_row] = ss_own[t];
     }
@@ -442,19 +473,24 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
 #pragma unroll
     for (int j = 0; j < FM; ++j) ss[j] = row_tot[0][wm * TM + j * 16 + lrow];
   } else
-  // Row statistics: lanes l, l^16, l^32, l^48 hold disjoint k of the same row.
-  // Row block WN t + wn's totals live in this wave (the one of the row band that
-  // squared it); they reach the other WN-1 waves through LDS.
+  // Row statistics.  Gram: row m's sum of squares is in the diagonal lane
+  // 20 (m / 4) + m % 4 and is broadcast to the lanes of row m (m = lane % 16).  Dot
+  // products: lanes l, l^16, l^32, l^48 hold disjoint k of the same row.  Row block
+  // WN t + wn's totals live in this wave (the one of the row band that took them); they
+  // reach the other WN-1 waves through LDS.
   if constexpr (kSS || kSA) {
+    const int diag_lane = (lane & 15) + 16 * ((lane & 15) >> 2);
 #pragma unroll
     for (int t = 0; t < TW; ++t) {
-      if constexpr (kSS) {
+      if constexpr (kGram) {
+        ssw[t] = __shfl(diag_of(gsq[t]), diag_lane);
+      } else {
         ssw[t] += __shfl_xor(ssw[t], 16);
         ssw[t] += __shfl_xor(ssw[t], 32);
-      }
-      if constexpr (kSA) {
-        saw[t] += __shfl_xor(saw[t], 16);
-        saw[t] += __shfl_xor(saw[t], 32);
+        if constexpr (kSA) {
+          saw[t] += __shfl_xor(saw[t], 16);
+          saw[t] += __shfl_xor(saw[t], 32);
+        }
       }
     }
     if constexpr (WN > 1) {

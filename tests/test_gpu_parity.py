@@ -795,8 +795,11 @@ def test_glu_unfolded(fn, dtype, M, K, F, path):
 
 @pytest.mark.parametrize("M,path", [(260, 1), (5, 2)])
 def test_unfolded_matches_folded_where_g_is_one(fn, M, path):
-    # With g = 1 both forms multiply the same bf16 values and take the squares in
-    # the same order: identical bits.
+    # With g = 1 both forms multiply the same bf16 values.  The few-row kernel takes the
+    # squares in the same order on both paths: identical bits.  The tile kernel takes
+    # them on the matrix cores (Gram blocks) on the folded path and as dot products on
+    # the run-time-g path, so the scales may differ in the last fp32 bits: at most one
+    # bf16 step apart, and almost every output identical.
     w = workloads.make("linear", M, 264, 136, eps=1e-6, seed=17)
     a, W = w.a.to(DEV), w.W.to(DEV)
     ones = torch.ones(w.K, dtype=torch.float32, device=DEV)
@@ -804,7 +807,12 @@ def test_unfolded_matches_folded_where_g_is_one(fn, M, path):
     yf = fn.flashnorm_linear(a, Wp, w.N, w.eps, path=path)
     yu = fn.flashnorm_linear_unfolded(a, ones, Wp, w.N, w.eps, path=path)
     torch.cuda.synchronize()
-    assert torch.equal(yf.view(torch.int16), yu.view(torch.int16))
+    if path == 2:
+        assert torch.equal(yf.view(torch.int16), yu.view(torch.int16))
+    else:
+        steps = (yf.view(torch.int16).int() - yu.view(torch.int16).int()).abs()
+        assert int(steps.max()) <= 1
+        assert float((steps == 0).float().mean()) >= 0.99
 
 
 # ------------------------------------------- fused QKV projection with RoPE (Fig. 5)
