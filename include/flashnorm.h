@@ -72,8 +72,11 @@ typedef enum { FN_PATH_AUTO = 0, FN_PATH_PREFILL = 1, FN_PATH_DECODE = 2 } fn_pa
 
 /* Tuning override: bits 8..15 of a path argument may name one of the library's
  * kernel configurations for the selected path (prefill tile shapes, or decode
- * work splits with FN_PATH_DECODE; for fp32 operands, 1 = 64-row tiles and
- * 2 = 16-row tiles with K split over four thread groups; 0 = automatic choice);
+ * work splits with FN_PATH_DECODE; for fp32 operands, 1 = 64-row tiles,
+ * 2 = 16-row tiles with K split over four thread groups, 3 = the few-row kernel:
+ * 16-row tiles of 4, 8 or 16 columns (8 or 16 for a GLU, 64 with per-head norms,
+ * the width chosen by the workgroup count) with K split over 256 / width thread
+ * groups; 0 = automatic choice);
  * values it does not know return FN_ERR_VALUE.  Results are identical for every configuration up to
  * floating-point summation order. */
 #define FN_PATH_TILE_SHIFT 8

@@ -95,8 +95,9 @@ struct F32Args {
   int cfg = 0;  // tile configuration (0 = automatic), see launch_f32
 };
 hipError_t launch_f32(const F32Args& p);
-// fp32 tile configurations: 0 automatic, 1 = 64-row tiles, 2 = 16-row tiles with four k groups.
-constexpr int kF32CfgCount = 3;
+// fp32 tile configurations: 0 automatic, 1 = 64-row tiles, 2 = 16-row tiles with four k groups,
+// 3 = 16-row tiles 4 to 64 columns wide with K split over up to 64 thread groups.
+constexpr int kF32CfgCount = 4;
 
 struct FoldArgs {
   const void* W;

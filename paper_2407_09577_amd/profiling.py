@@ -25,15 +25,23 @@ ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def kernel_sources_sha256(kernel: str) -> str:
-    """SHA-256 over the source file that defines ``kernel`` (``fn::<name>_kernel`` lives in
-    ``csrc/<name>.hip``) and every shared header, i.e. everything its code is built from."""
-    m = re.search(r"(\w+)_kernel", kernel)
-    if not m:
+def kernel_source(kernel: str) -> str:
+    """The csrc/*.hip file that defines the __global__ function ``kernel`` (a name such as
+    ``fn::f32_few_rows_kernel<...>`` or ``f32_few_rows_kernel``)."""
+    base = re.split(r"[<(]", kernel)[0].split("::")[-1].split()[-1]
+    if not base.endswith("_kernel"):
         raise ValueError(f"not a kernel name: {kernel}")
-    src = os.path.join(HERE, "csrc", m.group(1).split("::")[-1] + ".hip")
-    if not os.path.exists(src):
-        raise ValueError(f"no source {src} for {kernel}")
+    pat = re.compile(r"__global__[^;{]*?\b" + re.escape(base) + r"\s*\(", re.S)
+    for src in sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip"))):
+        if pat.search(open(src).read()):
+            return src
+    raise ValueError(f"no source defines {base}")
+
+
+def kernel_sources_sha256(kernel: str) -> str:
+    """SHA-256 over the source file that defines ``kernel`` and every shared header, i.e.
+    everything its code is built from."""
+    src = kernel_source(kernel)
     h = hashlib.sha256()
     for path in [src] + sorted(glob.glob(os.path.join(HERE, "csrc", "*.h"))):
         h.update(os.path.basename(path).encode())

@@ -43,7 +43,7 @@ int main() {
   REJECT(FN_ERR_ALIGN, lin(4, 128, 128, FN_BF16, A + 2, Y, 64, 1e-6f, 0));
   REJECT(FN_ERR_VALUE, lin(4, 128, 128, FN_BF16, A, Y, 64, -1.0f, 0));
   REJECT(FN_ERR_VALUE, lin(4, 128, 128, FN_BF16, A, Y, 64, 1e-6f, 7));
-  REJECT(FN_ERR_VALUE, lin(4, 128, 128, FN_F32, A, Y, 64, 1e-6f, 3 << FN_PATH_TILE_SHIFT));
+  REJECT(FN_ERR_VALUE, lin(4, 128, 128, FN_F32, A, Y, 64, 1e-6f, 4 << FN_PATH_TILE_SHIFT));
   REJECT(FN_ERR_ALIAS, lin(4, 128, 128, FN_BF16, A, A + 64, 64, 1e-6f, 0));
   REJECT(FN_ERR_SIZE, lin(4, 1 << 22, 1 << 22, FN_BF16, A, Y, 64, 1e-6f, 0));
   REJECT(FN_ERR_UNSUPPORTED, lin(32, 128, 128, FN_BF16, A, Y, 64, 1e-6f, FN_PATH_DECODE));

@@ -241,9 +241,10 @@ def test_layernorm_ragged(fn, M, K, N, dtype, path):
 LARGE_MEAN_CASES = [(mean, *case) for mean in (48.0, 128.0)
                     for case in [(torch.bfloat16, 512, 4096, 512, 0), (torch.bfloat16, 512, 4096, 512, 1 | (15 << 8)),
                                  (torch.bfloat16, 16, 4096, 512, 2), (torch.float32, 32, 1024, 96, 0),
-                                 (torch.float32, 100, 1024, 96, 1 << 8)]]
+                                 (torch.float32, 100, 1024, 96, 1 << 8), (torch.float32, 40, 1024, 96, 2 << 8)]]
 # fp32 only at 1024: bf16 has a spacing of 8 there, so N(1024, 1) rounds to constant rows
-LARGE_MEAN_CASES += [(1024.0, torch.float32, 32, 1024, 96, 0), (1024.0, torch.float32, 100, 1024, 96, 1 << 8)]
+LARGE_MEAN_CASES += [(1024.0, torch.float32, 32, 1024, 96, 0), (1024.0, torch.float32, 100, 1024, 96, 1 << 8),
+                     (1024.0, torch.float32, 40, 1024, 96, 2 << 8)]
 
 
 @pytest.mark.parametrize("mean,dtype,M,K,N,path", LARGE_MEAN_CASES)
@@ -263,12 +264,15 @@ def test_layernorm_large_mean(fn, record_parity, mean, dtype, M, K, N, path):
     assert dev <= (SCALE_TOL if dtype == torch.bfloat16 else TOL[dtype]), dev
 
 
-@pytest.mark.parametrize("cfg", [1, 2])
+@pytest.mark.parametrize("cfg", [1, 2, 3])
 @pytest.mark.parametrize("kind", ["linear", "glu", "layernorm"])
-@pytest.mark.parametrize("M,K,N", [(37, 96, 40), (70, 200, 136), (16, 576, 576), (130, 1032, 72)])
+@pytest.mark.parametrize("M,K,N", [(37, 96, 40), (70, 200, 136), (16, 576, 576), (130, 1032, 72), (16, 264, 2048),
+                                   (9, 136, 4096)])
 def test_fp32_tile_configs(fn, cfg, kind, M, K, N):
-    # Both fp32 configurations (64-row tiles; 16-row tiles with K split over four thread
-    # groups, added in a fixed order) on ragged shapes, against the oracle at 1e-5.
+    # Every fp32 configuration (64-row tiles; 16-row tiles with K split over four thread
+    # groups; the few-row kernel, whose tiles are 4, 8 or 16 columns wide by the workgroup
+    # count (the last two shapes take the wider ones), partials added in a fixed order) on
+    # ragged shapes, against the oracle at 1e-5.
     w = workloads.make(kind, M, K, N, dtype=torch.float32, eps=1e-5, seed=181 + M + K + cfg,
                        a_mean=0.5 if kind == "layernorm" else 0.0, outlier_frac=0.05)
     got, ref = _run_kind(fn, kind, w, cfg << 8)
@@ -838,6 +842,7 @@ def _qkv_rope_case(fn, M, K, Hq, Hkv, h, dtype, P, seq, seed, bias=False, path=0
                                                      (torch.bfloat16, 7, 520, 2, 2, 4, 2),
                                                      (torch.bfloat16, 16, 4096, 8, 8, 128, 0),
                                                      (torch.float32, 37, 96, 2, 1, 8, 0),
+                                                     (torch.float32, 900, 96, 4, 3, 64, 0),
                                                      (torch.float32, 5, 64, 1, 1, 4, 0)])
 @pytest.mark.parametrize("bias", [False, True])
 def test_qkv_rope(fn, dtype, M, K, Hq, Hkv, h, path, bias):
@@ -1116,8 +1121,11 @@ def test_random_shapes_all_ops(fn, seed):
 
 
 @pytest.mark.parametrize("M,K,Hq,Hkv,h,with_gv,rope", [(37, 96, 2, 1, 16, True, True), (20, 64, 1, 1, 64, False, True),
-                                                       (9, 64, 3, 1, 8, False, False), (70, 128, 1, 2, 32, True, True)])
+                                                       (9, 64, 3, 1, 8, False, False), (70, 128, 1, 2, 32, True, True),
+                                                       (900, 64, 4, 3, 64, True, True)])
 def test_qkv_headnorm_fp32(fn, M, K, Hq, Hkv, h, with_gv, rope):
+    # Few rows run the few-row kernel (64-column tiles with per-head norms); 900 rows make
+    # enough 64 x 64 tiles for the 64-row kernel.
     N = (Hq + 2 * Hkv) * h
     w = workloads.make("linear", M, K, N, dtype=torch.float32, eps=1e-5, seed=171 + M + h)
     g = torch.Generator().manual_seed(h)
