@@ -5,6 +5,8 @@
 // wants its own kernel instead of a padded prefill tile).  A workgroup owns NCB
 // packed column blocks of 16 columns (for a GLU, whole gate/up block pairs) and
 // its KSPLIT waves split K: wave w takes the 32-row k blocks w, w + KSPLIT, ...
+// (or, with CW column waves, each of CW waves owns NCB blocks over all of K and
+// the waves share the activation fragments through LDS).
 // Each weight fragment is one 16-byte load per lane (non-temporal: it is read
 // exactly once), fed directly to a 16x16x32 bf16 matrix-core op together with
 // the matching 16-row activation fragment (rows >= M read as zero), so the
@@ -22,14 +24,20 @@
 
 namespace fn {
 
-template <int NCB, int KSPLIT, int U, bool DB, int CPOL, int EPI, bool GS = false>
-__global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
+template <int NCB, int KSPLIT, int U, bool DB, int CPOL, int EPI, bool GS = false, int CW = 1>
+__global__ __launch_bounds__(KSPLIT * CW * 64) void decode_bf16_kernel(
     const __bf16* __restrict__ a, int M, int K, int lda, const __bf16* __restrict__ ws, int NP,
     int KP, int ncols, __bf16* __restrict__ y, int ldy, EpiArgs ep) {
   constexpr bool kSS = epi_needs_ss(EPI);
   constexpr bool kSA = EPI == EPI_LN;
   constexpr int NOUT = epi_is_glu(EPI) ? NCB / 2 : NCB;  // output blocks per workgroup
   static_assert(!epi_is_glu(EPI) || NCB % 2 == 0, "GLU needs gate/up block pairs");
+  // CW > 1: the workgroup's CW waves own NCB column blocks each over all of K and share
+  // the activation fragments: wave w loads fragments u = w, w + CW, ... of each set into
+  // LDS, and every wave reads all U of them (one activation load per set per wave
+  // instead of U; the activation is read from L2 by the workgroup once, not CW times).
+  static_assert(CW == 1 || (KSPLIT == 1 && DB && !GS && U % CW == 0), "shared activations: column waves");
+  constexpr int UA = U / CW;  // activation fragments each wave loads per set
 
   // Per-wave partials for the cross-wave combine (unused with one wave).
   __shared__ f32x4 red[KSPLIT > 1 ? KSPLIT : 1][NCB][64];
@@ -38,16 +46,18 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
   __shared__ ST red_sa[KSPLIT > 1 ? KSPLIT : 1][16];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int cb0 = blockIdx.x * NCB;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int cb0 = (blockIdx.x * CW + (CW > 1 ? wave : 0)) * NCB;
   const int KB = KP / kKB;
 
   const __amdgpu_buffer_rsrc_t rs_a = make_rsrc(a, (uint32_t)(((int64_t)(M - 1) * lda + K) * 2));
   // Column blocks past the packed width (last workgroup only) read the next k
   // block's fragments, or zeros past the end; their outputs are never stored.
   const int npb = NP / 16;
+  // (CW > 1: a wave wholly past the packed width gets an empty range and reads zeros.)
+  const int64_t w_extent = ((int64_t)KB * npb - cb0) * kFragBytes;
   const __amdgpu_buffer_rsrc_t rs_w =
-      make_rsrc(ws + (int64_t)cb0 * (kFragBytes / 2), (uint32_t)(((int64_t)KB * npb - cb0) * kFragBytes));
+      make_rsrc(ws + (int64_t)cb0 * (kFragBytes / 2), (uint32_t)(w_extent > 0 ? w_extent : 0));
 
   const int lrow = lane & 15;
   const int lk = (lane >> 4) * 8;
@@ -60,7 +70,7 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
   const int t_row = lane >> 2, t_k = (lane & 3) * 8;
   const bool row_ok = t_row < M;
   const unsigned a_row_off = (unsigned)(t_row * lda * 2);
-  __shared__ u32x4 a_slot[KSPLIT][U][64];
+  __shared__ u32x4 a_slot[CW > 1 ? 2 : KSPLIT][U][64];
   const unsigned a_rd = (unsigned)(4 * lrow + (lane >> 4));  // unit of (row lrow, chunk lane / 16)
 
   f32x4 acc[NCB];
@@ -83,7 +93,10 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
       const int k = kb * kKB + lk;
       const int kt = kb * kKB + t_k;
       const bool kb_ok = kb < KB;
-      af[u] = load_buf16(rs_a, (kb_ok && row_ok && kt < K) ? a_row_off + (unsigned)kt * 2 : kOobOffset);
+      if (CW == 1 || u % CW == 0) {  // CW > 1: this wave's fragment u + wave, kept in af[u / CW]
+        const int kba = kb + (CW > 1 ? wave : 0), kta = kt + (CW > 1 ? wave * kKB : 0);
+        af[u / CW] = load_buf16(rs_a, (kba < KB && row_ok && kta < K) ? a_row_off + (unsigned)kta * 2 : kOobOffset);
+      }
       if constexpr (GS) {
         // k >= K lies past the range of rs_g (K * 4 bytes) and reads zeros; the
         // offsets stay unconditional, which keeps the loop free of branches.
@@ -126,8 +139,44 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     }
   };
 
+  // CW > 1: the set's activation fragments through a double-buffered LDS stage.
+  auto compute_shared = [&](int buf, const u32x4 (&af)[U], const u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < UA; ++i) a_slot[buf][i * CW + wave][lane] = af[i];  // row-contiguous units
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bf16x8 av = __builtin_bit_cast(bf16x8, a_slot[buf][u][a_rd]);  // matrix-core order
+      if constexpr (kSA) {
+        ss += (double)sumsq8(av, 0.0f);
+        sa += (double)sum8(av, 0.0f);
+      } else if constexpr (kSS) {
+        ss = sumsq8(av, ss);
+      }
+#pragma unroll
+      for (int c = 0; c < NCB; ++c)
+        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[u][c]), av, acc[c], 0, 0, 0);
+    }
+  };
+
   constexpr int STEP = KSPLIT * U;  // k blocks per set across the workgroup
-  if constexpr (DB) {
+  if constexpr (CW > 1) {
+    // Every wave of the workgroup walks the same sets (the barrier in each set needs
+    // it); a slot is rewritten two sets later, after every wave has passed the
+    // barrier of the set in between, i.e. finished reading it.
+    u32x4 af0[U], wf0[U][NCB], af1[U], wf1[U][NCB];
+    load_set(0, af0, wf0, gv0);
+    for (int kb0 = 0; kb0 < KB; kb0 += 2 * STEP) {
+      load_set(kb0 + STEP, af1, wf1, gv1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_shared(0, af0, wf0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_set(kb0 + 2 * STEP, af0, wf0, gv0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_shared(1, af1, wf1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else if constexpr (DB) {
     // Double-buffered register sets: the next set's loads are issued before the
     // current set is consumed, so every wave keeps a full set in flight.  Sets
     // past K are issued as zero-returning loads, which keeps the loop uniform.
@@ -225,11 +274,12 @@ __global__ __launch_bounds__(KSPLIT * 64) void decode_bf16_kernel(
     epilogue(std::false_type{});
 }
 
-template <int NCB, int KSPLIT, int U, int EPI, bool DB = false, int CPOL = 0, bool GS = false>
+template <int NCB, int KSPLIT, int U, int EPI, bool DB = false, int CPOL = 0, bool GS = false, int CW = 1>
 static hipError_t launch_decode_cfg(const DecodeArgs& p) {
-  const int nblocks = (p.NP / 16 + NCB - 1) / NCB;
-  hipLaunchKernelGGL((decode_bf16_kernel<NCB, KSPLIT, U, DB, CPOL, EPI, GS>), dim3(nblocks), dim3(KSPLIT * 64), 0,
-                     p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y, p.ldy, p.ep);
+  const int nblocks = (p.NP / 16 + NCB * CW - 1) / (NCB * CW);
+  hipLaunchKernelGGL((decode_bf16_kernel<NCB, KSPLIT, U, DB, CPOL, EPI, GS, CW>), dim3(nblocks),
+                     dim3(KSPLIT * CW * 64), 0, p.stream, p.a, p.M, p.K, p.lda, p.ws, p.NP, p.KP, p.ncols, p.y,
+                     p.ldy, p.ep);
   return hipGetLastError();
 }
 
@@ -238,19 +288,24 @@ static hipError_t launch_decode_cfg(const DecodeArgs& p) {
 // waves in flight over the chip stream the weights fastest, so narrow outputs
 // split K over more waves of one workgroup (combined in LDS in a fixed order)
 // instead of leaving most compute units idle:
-//   npb >= 1088          8 blocks x 2 waves x 2 per set (M <= 8), else 2 x 1 x 2
+//   npb >= 1088          4 column waves x 2 blocks each, 4 per set, sharing the
+//                        activation fragments (1-2% faster than one wave per
+//                        workgroup at M = 1..16 on the Llama-7B SwiGLU shape)
 //   544 <= npb < 1088    4 blocks x 4 waves x 1
 //   272 <= npb < 544     2 blocks x 4 waves x 2
 //   npb < 272            2 blocks x 8 waves x 1
-// With run-time g the wide case keeps 2 x 1 x 4 for M > 8 (the g loads want
-// four blocks per set).
+// With run-time g the wide case takes 8 x 2 x 2 (M <= 8) or 2 x 1 x 4 (the g
+// loads want four blocks per set).
 template <int EPI, bool GS>
 static hipError_t launch_decode_auto(const DecodeArgs& p) {
   const int npb = p.NP / 16;
   if (npb >= 1088) {
-    if (p.M <= 8) return launch_decode_cfg<8, 2, 2, EPI, true, kCachePolicyNT, GS>(p);
-    if constexpr (GS) return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT, GS>(p);
-    else return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT, GS>(p);
+    if constexpr (GS) {
+      if (p.M <= 8) return launch_decode_cfg<8, 2, 2, EPI, true, kCachePolicyNT, GS>(p);
+      return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT, GS>(p);
+    } else {
+      return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT, false, 4>(p);
+    }
   }
   if (npb >= 544) return launch_decode_cfg<4, 4, 1, EPI, true, kCachePolicyNT, GS>(p);
   if (npb >= 272) return launch_decode_cfg<2, 4, 2, EPI, true, kCachePolicyNT, GS>(p);
@@ -291,6 +346,11 @@ static hipError_t launch_decode_epi(const DecodeArgs& p) {
     case 16: return launch_decode_cfg<2, 8, 2, EPI, true, kCachePolicyNT>(p);
     case 17: return launch_decode_cfg<4, 4, 1, EPI, true, kCachePolicyNT>(p);
     case 18: return launch_decode_cfg<2, 8, 1, EPI, true, kCachePolicyNT>(p);
+    case 19: return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT, false, 4>(p);
+    case 20: return launch_decode_cfg<2, 1, 2, EPI, true, kCachePolicyNT, false, 2>(p);
+    case 21: return launch_decode_cfg<2, 1, 4, EPI, true, kCachePolicyNT, false, 2>(p);
+    case 22: return launch_decode_cfg<4, 1, 4, EPI, true, kCachePolicyNT, false, 2>(p);
+    case 23: return launch_decode_cfg<2, 1, 4, EPI, true, 0, false, 4>(p);
   }
   return hipErrorInvalidValue;
   }

@@ -78,7 +78,7 @@ struct DecodeArgs {
   bool gs;  // run-time g (ep.g_rt) applied to the activations; unfolded W
 };
 hipError_t launch_decode_bf16(const DecodeArgs& p);
-constexpr int kDecodeCfgCount = 19;
+constexpr int kDecodeCfgCount = 24;
 
 struct F32Args {
   const float* a;

@@ -553,7 +553,7 @@ def test_row_pitch_padding_never_enters(fn, K):
 
 # ------------------------------------------------------------------ every kernel configuration
 PREFILL_TILES = list(range(1, 20))   # forced through the high byte of the path argument
-DECODE_CFGS = list(range(1, 19))
+DECODE_CFGS = list(range(1, 24))
 
 
 @pytest.mark.parametrize("tile", PREFILL_TILES)
@@ -590,9 +590,13 @@ def test_every_decode_config(fn, cfg, M):
     lin = workloads.make("linear", M, 1032, 88, eps=1e-6, seed=cfg * 5 + M)
     Wl, _, _ = fn.fold_weights(lin.W.to(DEV), lin.g.to(DEV))
     y = fn.flashnorm_linear(lin.a.to(DEV), Wl, 88, lin.eps, path=fn.FN_PATH_DECODE | (cfg << 8))
+    ln = workloads.make("layernorm", M, 1032, 40, eps=1e-5, seed=cfg * 11 + M, a_mean=0.5)
+    Wn, cs, cb = fn.fold_weights(ln.W.to(DEV), ln.g.to(DEV), beta=ln.beta.to(DEV), colsum=True, c_star=True)
+    z = fn.flashnorm_layernorm_linear(ln.a.to(DEV), Wn, cs, cb, 40, ln.eps, path=fn.FN_PATH_DECODE | (cfg << 8))
     torch.cuda.synchronize()
     assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
     assert row_err(to_np(y), oracle.rmsnorm_linear(lin.a, lin.g, lin.W, lin.eps)) <= TOL[torch.bfloat16]
+    assert row_err(to_np(z), oracle.layernorm_linear(ln.a, ln.g, ln.beta, ln.W, ln.eps)) <= TOL[torch.bfloat16]
 
 
 # The automatic decode split changes with the number of packed 16-column blocks
