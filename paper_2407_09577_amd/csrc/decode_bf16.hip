@@ -33,9 +33,9 @@ __global__ __launch_bounds__(KSPLIT * CW * 64) void decode_bf16_kernel(
   constexpr int NOUT = epi_is_glu(EPI) ? NCB / 2 : NCB;  // output blocks per workgroup
   static_assert(!epi_is_glu(EPI) || NCB % 2 == 0, "GLU needs gate/up block pairs");
   // CW > 1: the workgroup's CW waves own NCB column blocks each over all of K and share
-  // the activation fragments: wave w loads fragments u = w, w + CW, ... of each set into
-  // LDS, and every wave reads all U of them (one activation load per set per wave
-  // instead of U; the activation is read from L2 by the workgroup once, not CW times).
+  // the activation fragments: wave w loads fragments w, w + CW, ... of each set of U k
+  // blocks into LDS, and every wave reads all U of them (the activation is read from
+  // L2 by the workgroup once, not CW times).
   static_assert(CW == 1 || (KSPLIT == 1 && DB && !GS && U % CW == 0), "shared activations: column waves");
   constexpr int UA = U / CW;  // activation fragments each wave loads per set
 
@@ -93,10 +93,7 @@ __global__ __launch_bounds__(KSPLIT * CW * 64) void decode_bf16_kernel(
       const int k = kb * kKB + lk;
       const int kt = kb * kKB + t_k;
       const bool kb_ok = kb < KB;
-      if (CW == 1 || u % CW == 0) {  // CW > 1: this wave's fragment u + wave, kept in af[u / CW]
-        const int kba = kb + (CW > 1 ? wave : 0), kta = kt + (CW > 1 ? wave * kKB : 0);
-        af[u / CW] = load_buf16(rs_a, (kba < KB && row_ok && kta < K) ? a_row_off + (unsigned)kta * 2 : kOobOffset);
-      }
+      af[u] = load_buf16(rs_a, (kb_ok && row_ok && kt < K) ? a_row_off + (unsigned)kt * 2 : kOobOffset);
       if constexpr (GS) {
         // k >= K lies past the range of rs_g (K * 4 bytes) and reads zeros; the
         // offsets stay unconditional, which keeps the loop free of branches.
@@ -139,11 +136,50 @@ __global__ __launch_bounds__(KSPLIT * CW * 64) void decode_bf16_kernel(
     }
   };
 
-  // CW > 1: the set's activation fragments through a double-buffered LDS stage.
-  auto compute_shared = [&](int buf, const u32x4 (&af)[U], const u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
+  // CW > 1: activation fragments through a double-buffered LDS stage, loaded one set
+  // ahead of the weights.  Set s: its weights W(s) were issued during set s-1 and its
+  // activations act(s) during set s-2 and written to LDS slot s % 2 during set s-1.
+  // Waiting for W(s) therefore also covers act(s+1) (issued before it; loads return in
+  // order), so the activations' L2 latency never holds up the weight stream.
+  // A set's activations are 16 rows x U 64-byte k-block segments, i.e. U KiB: load
+  // ι = i CW + wave (i < UA) takes units 64 ι .. 64 ι + 63 of them in row-major order, so
+  // each load covers whole 4 U x 16-byte row runs (full 128-byte lines for U >= 2, half
+  // the L2 requests of one 16-row fragment per load), and the unit lands in LDS at
+  // k block u, row r, chunk c, where the matrix-core order reads it.
+  auto act_unit = [&](int i, int& r, int& u, int& c) __attribute__((always_inline)) {
+    const int n = (i * CW + wave) * 64 + lane;
+    r = n / (4 * U);
+    u = (n % (4 * U)) / 4;
+    c = n % 4;
+  };
+  auto load_act = [&](int kb0, u32x4 (&af)[UA]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < UA; ++i) a_slot[buf][i * CW + wave][lane] = af[i];  // row-contiguous units
-    __syncthreads();
+    for (int i = 0; i < UA; ++i) {
+      int r, u, c;
+      act_unit(i, r, u, c);
+      const int kb = kb0 + u;
+      const int kt = kb * kKB + c * 8;
+      af[i] = load_buf16(rs_a, (kb < KB && r < M && kt < K) ? (unsigned)(r * lda + kt) * 2 : kOobOffset);
+    }
+  };
+  auto load_w = [&](int kb0, u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kb = kb0 + u;
+#pragma unroll
+      for (int c = 0; c < NCB; ++c)
+        wf[u][c] = load_buf16<CPOL>(rs_w, kb < KB ? (unsigned)((kb * npb + c) * kFragBytes + lane * 16) : kOobOffset);
+    }
+  };
+  auto put_act = [&](int buf, const u32x4 (&af)[UA]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < UA; ++i) {
+      int r, u, c;
+      act_unit(i, r, u, c);
+      a_slot[buf][u][4 * r + c] = af[i];
+    }
+  };
+  auto compute_shared = [&](int buf, const u32x4 (&wf)[U][NCB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bf16x8 av = __builtin_bit_cast(bf16x8, a_slot[buf][u][a_rd]);  // matrix-core order
@@ -161,19 +197,29 @@ __global__ __launch_bounds__(KSPLIT * CW * 64) void decode_bf16_kernel(
 
   constexpr int STEP = KSPLIT * U;  // k blocks per set across the workgroup
   if constexpr (CW > 1) {
-    // Every wave of the workgroup walks the same sets (the barrier in each set needs
-    // it); a slot is rewritten two sets later, after every wave has passed the
-    // barrier of the set in between, i.e. finished reading it.
-    u32x4 af0[U], wf0[U][NCB], af1[U], wf1[U][NCB];
-    load_set(0, af0, wf0, gv0);
+    // Every wave of the workgroup walks the same sets (one barrier per set).  The
+    // barrier of set s orders the slot writes of set s-1 (act(s)) before this set's
+    // reads, and every wave's reads of slot (s+1) % 2 during set s-1 before its
+    // rewrite with act(s+1) here.
+    u32x4 a0[UA], a1[UA], w0[U][NCB], w1[U][NCB];
+    load_act(0, a0);
+    load_act(STEP, a1);
+    load_w(0, w0);
+    put_act(0, a0);
     for (int kb0 = 0; kb0 < KB; kb0 += 2 * STEP) {
-      load_set(kb0 + STEP, af1, wf1, gv1);
+      load_act(kb0 + 2 * STEP, a0);
+      load_w(kb0 + STEP, w1);
       __builtin_amdgcn_sched_barrier(0);
-      compute_shared(0, af0, wf0);
+      __syncthreads();
+      put_act(1, a1);
+      compute_shared(0, w0);
       __builtin_amdgcn_sched_barrier(0);
-      load_set(kb0 + 2 * STEP, af0, wf0, gv0);
+      load_act(kb0 + 3 * STEP, a1);
+      load_w(kb0 + 2 * STEP, w0);
       __builtin_amdgcn_sched_barrier(0);
-      compute_shared(1, af1, wf1);
+      __syncthreads();
+      put_act(0, a0);
+      compute_shared(1, w1);
       __builtin_amdgcn_sched_barrier(0);
     }
   } else if constexpr (DB) {
