@@ -71,7 +71,8 @@ __device__ __forceinline__ i32x4 make_rsrc_sgpr(const void* base, uint32_t bytes
 // before unrelated LDS reads: the kernels order them with explicit vmcnt waits
 // and barriers.  lds_base must be wave-uniform.  M0 is written here without being
 // declared (the compiler reserves it and rejects the clobber); these kernels use
-// M0 for nothing else.
+// M0 for nothing else, which tests/test_lds_dma_m0.py checks on the built code
+// object (every M0 write feeds the transfer right after it, no implicit M0 reader).
 __device__ __forceinline__ void load_lds16(i32x4 rsrc, const void* lds_base, unsigned voffset) {
   const unsigned m0 = __builtin_amdgcn_readfirstlane(
       (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_base);
