@@ -379,6 +379,8 @@ def main():
                       kernels_per_step="2 (fused projection, latent pass); roofline.achieved uses the whole step")
     if prof is not None:
         config["traffic_profile"] = prof["path"]
+        if "kernel_timed_avg_duration_us" in prof:
+            config["profile_kernel_timed_avg_us"] = float(prof["kernel_timed_avg_duration_us"])
     if ms_unf is not None:
         config["unfused_ms_per_step"] = ms_unf
         config["unfused_over_fused"] = ms_unf / ms  # speedup of the fused op (x)

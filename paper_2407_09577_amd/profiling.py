@@ -1,7 +1,8 @@
 """Summaries of rocprofv3 runs of the FlashNorm kernels (kept as text under profiles/).
 
 A summary records, for one kernel and workload: the commands that produced it,
-the kernel's average duration from ``--kernel-trace --stats``, the FETCH_SIZE and
+the kernel's average duration from ``--kernel-trace --stats`` (over all its dispatches,
+and over the last ``--timed-steps`` ones, the bench's timed region), the FETCH_SIZE and
 WRITE_SIZE counters per dispatch (KiB) scaled by the factors a plain device copy
 of known size yields on the same machine, the matrix-core busy fraction, and a
 SHA-256 of the kernel's source file and the shared headers.  bench.py reports the
@@ -77,8 +78,19 @@ def kernel_stats(d, kernel):
     raise ValueError(f"{kernel} not in {d}")
 
 
+def timed_avg_ns(d, name, last):
+    """Mean duration of the last `last` dispatches of kernel `name` (full name) in the
+    kernel trace: bench.py's timed region is its final graph replay of `steps` calls."""
+    durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in _rows(d, "run_kernel_trace.csv")
+            if r["Kernel_Name"] == name]
+    if len(durs) < last:
+        raise ValueError(f"{name}: {len(durs)} dispatches in the trace, fewer than {last}")
+    return sum(durs[-last:]) / last
+
+
 def summarize(a) -> str:
     name, calls, avg_ns = kernel_stats(a.trace, a.kernel) if a.trace else (a.kernel, 0, float("nan"))
+    timed_ns = timed_avg_ns(a.trace, name, a.timed_steps) if a.trace else float("nan")
     fetch_kib, nf = counter_mean(a.fetch, a.kernel, "FETCH_SIZE")
     write_kib, nw = counter_mean(a.write, a.kernel, "WRITE_SIZE")
     cal_fetch, _ = counter_mean(a.cal_fetch, "copyBuffer", "FETCH_SIZE")
@@ -96,7 +108,9 @@ def summarize(a) -> str:
         *[f"#   {c}" for c in a.command],
         f"kernel: {name}",
         f"kernel_trace_calls: {calls}",
-        f"kernel_avg_duration_us: {avg_ns / 1e3:.3f}",
+        f"kernel_avg_duration_us: {avg_ns / 1e3:.3f}  (all {calls} dispatches, warm-up included)",
+        f"kernel_timed_avg_duration_us: {timed_ns / 1e3:.3f}  (the last {a.timed_steps} dispatches: "
+        f"bench.py's timed graph replay)",
         f"fetch_size_kib_per_dispatch: {fetch_kib:.1f}  (mean of {nf} dispatches)",
         f"write_size_kib_per_dispatch: {write_kib:.1f}  (mean of {nw} dispatches)",
         f"copy_calibration: {a.copy_bytes} bytes copied; FETCH_SIZE {cal_fetch:.1f} KiB -> factor {f_fetch:.4f}; "
@@ -135,6 +149,7 @@ def main():
         p.add_argument(f"--{k}", required=True)
     p.add_argument("--trace", default=None, help="--kernel-trace --stats output of the same command")
     p.add_argument("--copy-bytes", type=int, required=True)
+    p.add_argument("--timed-steps", type=int, default=100, help="bench.py --steps of the traced command")
     p.add_argument("--xcds", type=int, default=8)
     p.add_argument("--simds", type=int, default=1024)
     p.add_argument("--command", action="append", default=[])
