@@ -1124,6 +1124,30 @@ def test_random_shapes_all_ops(fn, seed):
         assert row_err(to_np(yh), rh) <= TOL[torch.bfloat16], (M, K, Hq, Hkv, h)
 
 
+@pytest.mark.parametrize("seed", [11, 12, 13])
+def test_random_shapes_fp32(fn, seed):
+    # fp32 operands on ragged shapes drawn from a fixed seed, through the automatic choice
+    # (64-row tiles, 16 x 64 tiles, or the few-row kernel at 4, 8 or 16 columns), at 1e-5.
+    rng = np.random.default_rng(seed)
+    for _ in range(8):
+        M = int(rng.choice([1, 3, 16, 17, 40, 100, 257, 700]))
+        K = int(rng.integers(1, 160)) * 4
+        N = int(rng.choice([int(rng.integers(1, 30)) * 8, int(rng.integers(50, 350)) * 8]))
+        kind = str(rng.choice(["linear", "glu", "layernorm", "unfolded"]))
+        w = workloads.make("linear" if kind == "unfolded" else kind, M, K, N // 2 if kind == "glu" else N,
+                           dtype=torch.float32, eps=1e-5, seed=int(rng.integers(1 << 30)),
+                           a_mean=0.5 if kind == "layernorm" else 0.0, outlier_frac=0.05)
+        if kind == "unfolded":
+            Wp, _, _ = fn.fold_weights(w.W.to(DEV), None, ws_dtype=fn.FN_F32)
+            y = fn.flashnorm_linear_unfolded(w.a.to(DEV), w.g.to(DEV), Wp, w.N, w.eps,
+                                             out=padded_out(M, w.N, torch.float32, align=4))
+            torch.cuda.synchronize()
+            got, ref = to_np(y), oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)
+        else:
+            got, ref = _run_kind(fn, kind, w, 0)
+        assert row_err(got, ref) <= TOL[torch.float32], (kind, M, K, N)
+
+
 @pytest.mark.parametrize("M,K,Hq,Hkv,h,with_gv,rope", [(37, 96, 2, 1, 16, True, True), (20, 64, 1, 1, 64, False, True),
                                                        (9, 64, 3, 1, 8, False, False), (70, 128, 1, 2, 32, True, True),
                                                        (900, 64, 4, 3, 64, True, True)])
