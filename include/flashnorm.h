@@ -48,7 +48,7 @@ typedef enum {
   FN_ERR_SHAPE = -2,       /* M < 0, K <= 0, N <= 0, leading dimension too small, K not a multiple of 8 (bf16) or 4 (fp32) */
   FN_ERR_DTYPE = -3,       /* unknown dtype, or dtypes that do not match */
   FN_ERR_ALIGN = -4,       /* a pointer is not 16-byte aligned or a leading dimension breaks row alignment */
-  FN_ERR_UNSUPPORTED = -5, /* valid request this build does not implement (e.g. a forced path that cannot run it) */
+  FN_ERR_UNSUPPORTED = -5, /* valid request the library does not implement (e.g. a forced path that cannot run it) */
   FN_ERR_VALUE = -6,       /* eps negative or not finite; unknown layout or path */
   FN_ERR_HIP = -7,         /* the HIP runtime reported an error while launching */
   FN_ERR_ALIAS = -8,       /* the output overlaps an input */

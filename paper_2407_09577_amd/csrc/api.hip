@@ -631,7 +631,7 @@ const char* flashnorm_status_string(int status) {
     case FN_ERR_SHAPE: return "FN_ERR_SHAPE: invalid shape or leading dimension";
     case FN_ERR_DTYPE: return "FN_ERR_DTYPE: unknown or mismatched dtype";
     case FN_ERR_ALIGN: return "FN_ERR_ALIGN: pointer or leading dimension breaks 16-byte alignment";
-    case FN_ERR_UNSUPPORTED: return "FN_ERR_UNSUPPORTED: request not implemented by this build";
+    case FN_ERR_UNSUPPORTED: return "FN_ERR_UNSUPPORTED: request not implemented by the library";
     case FN_ERR_VALUE: return "FN_ERR_VALUE: invalid eps, layout or path";
     case FN_ERR_HIP: return "FN_ERR_HIP: HIP runtime error at launch";
     case FN_ERR_ALIAS: return "FN_ERR_ALIAS: output overlaps an input";
