@@ -56,6 +56,8 @@ def parse_args():
     p.add_argument("--rope-h", type=int, default=0,
                    help="qkv_rope head width (default 128 for Llama-7B, else 64); Hq = Hkv = N / (3 h)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--repeats", type=int, default=5,
+                   help="further timed passes after the reported one, for the spread across passes")
     p.add_argument("--no-unfused", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle timing sample")
     p.add_argument("--eager", action="store_true",
@@ -197,10 +199,12 @@ class Setup:
         """Read a once, read W* once, write the output once."""
         return self.M * self.K * self.es + self.ws_bytes + self.M * self.ncols * self.es
 
-    def time_steps(self, fn_step, steps, warmup, graph=True):
+    def time_steps(self, fn_step, steps, warmup, graph=True, repeats=0):
         """Average ms per step over `steps` steps, HIP events on the launch stream.
         graph=True captures the steps into one HIP graph and times its replay, so
-        small kernels are not limited by Python launch overhead."""
+        small kernels are not limited by Python launch overhead.  With repeats > 0 the
+        timed region is followed by `repeats` more timed passes, whose per-step averages
+        are returned as well (the spread across passes)."""
         torch = self.torch
         for i in range(warmup):
             fn_step(i)
@@ -234,7 +238,21 @@ class Setup:
                 fn_step(warmup + i)
         end.record(stream)
         torch.cuda.synchronize()
-        return start.elapsed_time(end) / steps  # ms per step
+        ms = start.elapsed_time(end) / steps  # ms per step
+        if not repeats:
+            return ms
+        more = []
+        for _ in range(repeats):
+            start.record(stream)
+            if g is not None:
+                g.replay()
+            else:
+                for i in range(steps):
+                    fn_step(warmup + i)
+            end.record(stream)
+            torch.cuda.synchronize()
+            more.append(start.elapsed_time(end) / steps)
+        return ms, more
 
 
 def cpu_baseline(w, unit, target_s, flops_per_row, bytes_total, s=None):
@@ -327,7 +345,8 @@ def main():
 
     torch.cuda.synchronize()
     graph = not args.eager
-    ms = s.time_steps(s.run, args.steps, args.warmup, graph)
+    timed = s.time_steps(s.run, args.steps, args.warmup, graph, repeats=args.repeats)
+    ms, passes = timed if isinstance(timed, tuple) else (timed, [])
     ms_unf = None if args.no_unfused else s.time_steps(s.run_unfused, args.steps, args.warmup, graph)
 
     t = ms * 1e-3
@@ -381,6 +400,12 @@ def main():
         config["traffic_profile"] = prof["path"]
         if "kernel_timed_avg_duration_us" in prof:
             config["profile_kernel_timed_avg_us"] = float(prof["kernel_timed_avg_duration_us"])
+    if passes:
+        allp = sorted([ms] + passes)
+        pick = lambda q: allp[min(len(allp) - 1, int(round(q * (len(allp) - 1))))]
+        config["us_per_step_passes"] = {"passes": len(allp), "median": pick(0.5) * 1e3, "min": allp[0] * 1e3,
+                                        "p90": pick(0.9) * 1e3, "max": allp[-1] * 1e3,
+                                        "mean": sum(allp) / len(allp) * 1e3}
     if ms_unf is not None:
         config["unfused_ms_per_step"] = ms_unf
         config["unfused_over_fused"] = ms_unf / ms  # speedup of the fused op (x)

@@ -80,7 +80,7 @@ def kernel_stats(d, kernel):
 
 def timed_avg_ns(d, name, last):
     """Mean duration of the last `last` dispatches of kernel `name` (full name) in the
-    kernel trace: bench.py's timed region is its final graph replay of `steps` calls."""
+    kernel trace: bench.py ends with timed graph replays of `steps` calls each."""
     durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in _rows(d, "run_kernel_trace.csv")
             if r["Kernel_Name"] == name]
     if len(durs) < last:
@@ -110,7 +110,7 @@ def summarize(a) -> str:
         f"kernel_trace_calls: {calls}",
         f"kernel_avg_duration_us: {avg_ns / 1e3:.3f}  (all {calls} dispatches, warm-up included)",
         f"kernel_timed_avg_duration_us: {timed_ns / 1e3:.3f}  (the last {a.timed_steps} dispatches: "
-        f"bench.py's timed graph replay)",
+        f"bench.py's last timed graph replay)",
         f"fetch_size_kib_per_dispatch: {fetch_kib:.1f}  (mean of {nf} dispatches)",
         f"write_size_kib_per_dispatch: {write_kib:.1f}  (mean of {nw} dispatches)",
         f"copy_calibration: {a.copy_bytes} bytes copied; FETCH_SIZE {cal_fetch:.1f} KiB -> factor {f_fetch:.4f}; "
