@@ -39,7 +39,7 @@ struct Vec16 {
 #pragma unroll
       for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(v[i]);
     }
-    *reinterpret_cast<u32x4*>(p) = w;
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p));  // as the fused kernels' output stores
   }
 };
 

@@ -278,6 +278,13 @@ __device__ __forceinline__ void stage4(char* tile, int r, int c, u32x2 val) {
   *reinterpret_cast<u32x2*>(tile + stage_pos<UPR>(r, byte >> 4) * 16 + (byte & 8)) = val;
 }
 
+// Output stores of whole 16-byte units carry the non-temporal hint: the kernel never
+// reads its output back, and on MI355X the hint shortened the SmolLM2-width prefill by
+// ~18% (no L2 allocation for 6.3 MB of output) and the Llama-7B shapes by ~1%.
+__device__ __forceinline__ void store_out16(__bf16* p, u32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
 // Copy a staged ROWS x (UPR*8) bf16 tile to y[m0.., n0..]: thread tid of NT
 // moves 16-byte units in row-major order.  y + n0 and ldy keep 16-byte alignment.
 template <int ROWS, int UPR, int NT>
@@ -287,7 +294,7 @@ __device__ __forceinline__ void copy_tile_out(const char* tile, __bf16* __restri
   for (int q = tid; q < ROWS * UPR; q += NT) {
     const int r = q / UPR, u = q % UPR;
     const u32x4 v = *reinterpret_cast<const u32x4*>(tile + stage_pos<UPR>(r, u) * 16);
-    *reinterpret_cast<u32x4*>(y + (int64_t)(m0 + r) * ldy + n0 + u * 8) = v;
+    store_out16(y + (int64_t)(m0 + r) * ldy + n0 + u * 8, v);
   }
 }
 

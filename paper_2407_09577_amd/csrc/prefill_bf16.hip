@@ -619,8 +619,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
           if (m0 + row < M && n0 + v * 8 < ncols) {
             const u32x2 lo = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o));
             const u32x2 hi = pack4_bf16(*reinterpret_cast<const float(*)[4]>(o + 4));
-            *reinterpret_cast<u32x4*>(y + (int64_t)(m0 + row) * ldy + n0 + v * 8) =
-                u32x4{lo[0], lo[1], hi[0], hi[1]};
+            store_out16(y + (int64_t)(m0 + row) * ldy + n0 + v * 8, u32x4{lo[0], lo[1], hi[0], hi[1]});
           }
         }
       }
