@@ -1124,6 +1124,35 @@ def test_random_shapes_all_ops(fn, seed):
         assert row_err(to_np(yh), rh) <= TOL[torch.bfloat16], (M, K, Hq, Hkv, h)
 
 
+# Narrow GLU outputs (a handful of features, rows whose outputs are all small, ReLU gates
+# near zero): here the rounding of the stored, folded W* alone can exceed the 2e-2 bar against
+# the unfolded standard form (the appendix's additional notes discuss this effect of
+# precomputed merged weights under lossy precision).  A sweep of the random-shape test found
+# such rows; in every one the GPU error matched, to six digits, the error of the same deferred
+# form computed exactly with the stored W*.  This pins the kernels to that form: against the
+# oracle's standard form with g = 1 and W = the oracle's expected fold, only the single bf16
+# rounding of the output remains (unit roundoff 2^-8 = 3.9e-3 of the row maximum); the bar is
+# twice that.
+NARROW_GLU = [(63, 120, 4, 0, 7), (513, 432, 4, 0, 8), (513, 512, 12, 1, 9), (129, 424, 12, 1, 10),
+              (17, 352, 8, 1, 11), (300, 64, 4, 1, 12), (40, 96, 4, 2, 13)]
+
+
+@pytest.mark.parametrize("M,K,F,act,seed", NARROW_GLU)
+def test_narrow_glu_outputs_follow_the_stored_weights(fn, record_parity, M, K, F, act, seed):
+    w = workloads.make("glu", M, K, F, eps=1e-6, seed=seed)
+    Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
+    y = fn.flashnorm_glu_act(w.a.to(DEV), Ws, F, w.eps, act, out=padded_out(M, F, torch.bfloat16))
+    torch.cuda.synchronize()
+    got = to_np(y)
+    stored, _, _ = oracle.fold(w.W, w.g)
+    exact_stored = oracle.rmsnorm_glu_act(w.a, np.ones(K), stored, w.eps, act)
+    standard = oracle.rmsnorm_glu_act(w.a, w.g, w.W, w.eps, act)
+    err_stored, err_std = row_err(got, exact_stored), row_err(got, standard)
+    record_parity(f"narrow GLU act {act} {M}x{K}x{F}: vs stored-W* form", row_err=err_stored,
+                  standard_form_row_err=err_std)
+    assert err_stored <= 8e-3, (err_stored, err_std)
+
+
 @pytest.mark.parametrize("seed", [11, 12, 13])
 def test_random_shapes_fp32(fn, seed):
     # fp32 operands on ragged shapes drawn from a fixed seed, through the automatic choice
