@@ -1148,8 +1148,14 @@ def test_narrow_glu_outputs_follow_the_stored_weights(fn, record_parity, M, K, F
     exact_stored = oracle.rmsnorm_glu_act(w.a, np.ones(K), stored, w.eps, act)
     standard = oracle.rmsnorm_glu_act(w.a, w.g, w.W, w.eps, act)
     err_stored, err_std = row_err(got, exact_stored), row_err(got, standard)
+    extra = {}
+    if act == fn.FN_GLU_SWIGLU:
+        Wp, _, _ = fn.fold_weights(w.W.to(DEV), None, layout=fn.FN_LAYOUT_GLU)
+        yu = fn.flashnorm_glu_unfolded(w.a.to(DEV), w.g.to(DEV), Wp, F, w.eps, out=padded_out(M, F, torch.bfloat16))
+        torch.cuda.synchronize()
+        extra["unfolded_standard_form_row_err"] = row_err(to_np(yu), standard)
     record_parity(f"narrow GLU act {act} {M}x{K}x{F}: vs stored-W* form", row_err=err_stored,
-                  standard_form_row_err=err_std)
+                  standard_form_row_err=err_std, **extra)
     assert err_stored <= 8e-3, (err_stored, err_std)
 
 
