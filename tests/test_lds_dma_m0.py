@@ -12,37 +12,12 @@ gfx950 build of ``csrc/prefill_bf16.hip``, disassembled with the ROCm LLVM tools
 A toolchain that starts using M0 in these kernels fails here, on the CPU, before any
 kernel runs.
 """
-import os
 import re
-import shutil
-import subprocess
 
-import pytest
+from _codeobj import disassemble
 
-ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-OBJ = os.path.join(ROOT, "paper_2407_09577_amd", "_build", "prefill_bf16.hip.o")
-LLVM = "/opt/rocm/llvm/bin"
-TARGET = "hipv4-amdgcn-amd-amdhsa--gfx950"
 IMPLICIT_M0 = re.compile(r"\b(v_movrel\w*|s_movrel\w*|s_sendmsg\w*|ds_gws\w*|ds_\w*addtid\w*|v_interp\w*|"
                          r"s_ttracedata)\b")
-
-
-def _disassemble(tmp_path):
-    for tool in ("clang-offload-bundler", "llvm-objdump"):
-        if not os.path.exists(os.path.join(LLVM, tool)):
-            pytest.skip(f"{tool} not installed")
-    if shutil.which("objcopy") is None:
-        pytest.skip("objcopy not installed")
-    if not os.path.exists(OBJ):
-        pytest.skip("library not built")
-    fat, co = tmp_path / "fat.bin", tmp_path / "prefill.co"
-    subprocess.run(["objcopy", f"--dump-section=.hip_fatbin={fat}", OBJ], check=True, capture_output=True)
-    subprocess.run([os.path.join(LLVM, "clang-offload-bundler"), "--unbundle", "--type=o", f"--input={fat}",
-                    f"--targets={TARGET}", f"--output={co}"], check=True, capture_output=True)
-    out = subprocess.run([os.path.join(LLVM, "llvm-objdump"), "-d", "--mcpu=gfx950", str(co)], check=True,
-                         capture_output=True, text=True).stdout
-    # instruction text only (drop the address / encoding comment)
-    return [ln.split("//")[0].strip() for ln in out.splitlines() if ln.startswith("\t")]
 
 
 def m0_violations(ins):
@@ -71,7 +46,7 @@ def test_checker_flags_other_m0_uses():
 
 
 def test_m0_only_feeds_lds_dma(tmp_path):
-    ins = _disassemble(tmp_path)
+    ins = disassemble("prefill_bf16.hip", tmp_path)
     assert len(ins) > 1000
     assert any(t.startswith("buffer_load") and t.endswith(" lds") for t in ins), "no LDS-DMA transfer found"
     assert m0_violations(ins) == []
