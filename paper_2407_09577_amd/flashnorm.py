@@ -126,6 +126,16 @@ def _vec(t, n, name):
     return t
 
 
+def _new_out(M: int, N: int, like: torch.Tensor) -> torch.Tensor:
+    """A new [M, N] output in like's dtype and device.  Its rows are padded to a multiple of
+    16 bytes, the row pitch the kernels' vector stores require (FN_ERR_ALIGN otherwise), so
+    any N works; the result is then a view of the first N columns."""
+    per = 16 // like.element_size()
+    ld = (N + per - 1) // per * per
+    buf = torch.empty(M, ld, dtype=like.dtype, device=like.device)
+    return buf if ld == N else buf[:, :N]
+
+
 def fold_weights_size(K: int, N: int, layout: int = FN_LAYOUT_LINEAR, ws_dtype: int = FN_BF16) -> int:
     return _load().fold_weights_size(K, N, layout, ws_dtype)
 
@@ -202,7 +212,7 @@ def flashnorm_linear(a: torch.Tensor, W_star: torch.Tensor, N: int, eps: float, 
     M, K = a.shape
     _guard("flashnorm_linear", (a, W_star, bias, out, inv_rms), packed=(W_star, K, N, FN_LAYOUT_LINEAR, _dt(a)),
            outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     _check(_load().flashnorm_linear_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star), N, eps,
                                        _ptr(_vec(bias, N, "bias")), _ptr(y), _ld(y), _dt(y),
                                        _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
@@ -215,7 +225,7 @@ def flashnorm_glu(a: torch.Tensor, W_star_gu: torch.Tensor, F: int, eps: float, 
     M, K = a.shape
     _guard("flashnorm_glu", (a, W_star_gu, out), packed=(W_star_gu, K, 2 * F, FN_LAYOUT_GLU, _dt(a)),
            outs=((out, M, F),))
-    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    o = out if out is not None else _new_out(M, F, a)
     _check(_load().flashnorm_glu_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star_gu), F, eps, _ptr(o), _ld(o),
                                     _dt(o), path, _stream(stream)), "flashnorm_glu")
     return o
@@ -227,7 +237,7 @@ def flashnorm_glu_act(a: torch.Tensor, W_star_gu: torch.Tensor, F: int, eps: flo
     M, K = a.shape
     _guard("flashnorm_glu_act", (a, W_star_gu, out, inv_rms), packed=(W_star_gu, K, 2 * F, FN_LAYOUT_GLU, _dt(a)),
            outs=((out, M, F),))
-    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    o = out if out is not None else _new_out(M, F, a)
     _check(_load().flashnorm_glu_act(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star_gu), F, eps, act, _ptr(o),
                                      _ld(o), _dt(o), _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
            "flashnorm_glu_act")
@@ -240,7 +250,7 @@ def flashnorm_linear_relu(a: torch.Tensor, W_star: torch.Tensor, N: int, eps: fl
     M, K = a.shape
     _guard("flashnorm_linear_relu", (a, W_star, out, inv_rms), packed=(W_star, K, N, FN_LAYOUT_LINEAR, _dt(a)),
            outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     _check(_load().flashnorm_linear_relu(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star), N, eps, _ptr(y), _ld(y),
                                          _dt(y), _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
            "flashnorm_linear_relu")
@@ -253,7 +263,7 @@ def rowscale_linear(x: torch.Tensor, W_packed: torch.Tensor, N: int, row_scale: 
     M, K = x.shape
     _guard("rowscale_linear", (x, W_packed, row_scale, out), packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(x)),
            outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=x.dtype, device=x.device)
+    y = out if out is not None else _new_out(M, N, x)
     _check(_load().rowscale_linear(_ptr(x), M, K, _ld(x), _dt(x), _ptr(W_packed), N,
                                    _ptr(_vec(row_scale, M, "row_scale")), _ptr(y), _ld(y), _dt(y), path,
                                    _stream(stream)), "rowscale_linear")
@@ -268,7 +278,7 @@ def flashnorm_qkv_rope(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv: in
     N = (Hq + 2 * Hkv) * h
     _guard("flashnorm_qkv_rope", (a, W_packed, positions, cos_tab, sin_tab, bias, out, inv_rms),
            packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     if positions.dtype != torch.int32 or not positions.is_contiguous() or positions.numel() != M:
         raise ValueError("positions must be a contiguous int32 tensor of M entries")
     for name, t in (("cos_tab", cos_tab), ("sin_tab", sin_tab)):
@@ -293,7 +303,7 @@ def flashnorm_qkv_headnorm(a: torch.Tensor, W_packed: torch.Tensor, Hq: int, Hkv
     N = (Hq + 2 * Hkv) * h
     _guard("flashnorm_qkv_headnorm", (a, W_packed, gq, gk, gv, positions, cos_tab, sin_tab, out, inv_rms),
            packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     P_rows = 0
     if positions is not None:
         P_rows = _rope_tables(M, h // 2, positions, cos_tab, sin_tab)
@@ -363,7 +373,7 @@ def flashnorm_mla_latent(a: torch.Tensor, W_packed: torch.Tensor, L: int, R: int
     M, K = a.shape
     _guard("flashnorm_mla_latent", (a, W_packed, g_lat, positions, cos_tab, sin_tab, out, inv_rms),
            packed=(W_packed, K, L + R, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, L + R),))
-    y = out if out is not None else torch.empty(M, L + R, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, L + R, a)
     pos, cos_t, sin_t, P_rows = _rotary_args(M, R, positions, cos_tab, sin_tab)
     if R > 0 and inv_rms is None:
         inv_rms = torch.empty(M, dtype=torch.float32, device=a.device)
@@ -393,7 +403,7 @@ def flashnorm_linear_unfolded(a: torch.Tensor, g: torch.Tensor, W_packed: torch.
     M, K = a.shape
     _guard("flashnorm_linear_unfolded", (a, g, W_packed, bias, out, inv_rms),
            packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     _check(_load().flashnorm_linear_unfolded(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed),
                                              N, eps, _ptr(_vec(bias, N, "bias")), _ptr(y), _ld(y), _dt(y),
                                              _ptr(_vec(inv_rms, M, "inv_rms")), path, _stream(stream)),
@@ -407,7 +417,7 @@ def flashnorm_glu_unfolded(a: torch.Tensor, g: torch.Tensor, W_packed_gu: torch.
     M, K = a.shape
     _guard("flashnorm_glu_unfolded", (a, g, W_packed_gu, out), packed=(W_packed_gu, K, 2 * F, FN_LAYOUT_GLU, _dt(a)),
            outs=((out, M, F),))
-    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    o = out if out is not None else _new_out(M, F, a)
     _check(_load().flashnorm_glu_unfolded(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed_gu),
                                           F, eps, _ptr(o), _ld(o), _dt(o), path, _stream(stream)),
            "flashnorm_glu_unfolded")
@@ -419,7 +429,7 @@ def flashnorm_layernorm_linear(a: torch.Tensor, W_star: torch.Tensor, colsum: to
     M, K = a.shape
     _guard("flashnorm_layernorm_linear", (a, W_star, colsum, c_star, out),
            packed=(W_star, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     _check(_load().flashnorm_layernorm_linear_ex(_ptr(a), M, K, _ld(a), _dt(a), _ptr(W_star),
                                                  _ptr(_vec(colsum, N, "colsum")), _ptr(_vec(c_star, N, "c_star")),
                                                  N, eps, _ptr(y), _ld(y), _dt(y), path, _stream(stream)),
@@ -443,7 +453,7 @@ def baseline_rmsnorm_linear(a, g, W_packed, N, eps, x_ws=None, out=None, path=FN
     M, K = a.shape
     _baseline_guard("baseline_rmsnorm_linear", a, g, None, W_packed, N, FN_LAYOUT_LINEAR, x_ws, out, N)
     x = _ws(a, x_ws)
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     _check(_load().baseline_rmsnorm_linear(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed),
                                            N, eps, _ptr(x), _ptr(y), _ld(y), path, _stream(stream)),
            "baseline_rmsnorm_linear")
@@ -459,7 +469,7 @@ def baseline_rmsnorm_linear_noalloc(a, g, W_packed, N, eps, out=None, path=FN_PA
     M, K = a.shape
     _guard("baseline_rmsnorm_linear_noalloc", (a, g, W_packed, out),
            packed=(W_packed, K, N, FN_LAYOUT_LINEAR, _dt(a)), outs=((out, M, N),))
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     _check(_load().baseline_rmsnorm_linear_noalloc(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")),
                                                    _ptr(W_packed), N, eps, _ptr(y), _ld(y), path, _stream(stream)),
            "baseline_rmsnorm_linear_noalloc")
@@ -470,7 +480,7 @@ def baseline_rmsnorm_glu(a, g, W_packed_gu, F, eps, x_ws=None, out=None, path=FN
     M, K = a.shape
     _baseline_guard("baseline_rmsnorm_glu", a, g, None, W_packed_gu, 2 * F, FN_LAYOUT_GLU, x_ws, out, F)
     x = _ws(a, x_ws)
-    o = out if out is not None else torch.empty(M, F, dtype=a.dtype, device=a.device)
+    o = out if out is not None else _new_out(M, F, a)
     _check(_load().baseline_rmsnorm_glu(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")), _ptr(W_packed_gu),
                                         F, eps, _ptr(x), _ptr(o), _ld(o), path, _stream(stream)),
            "baseline_rmsnorm_glu")
@@ -482,7 +492,7 @@ def baseline_layernorm_linear(a, g, beta, W_packed, N, eps, x_ws=None, out=None,
     M, K = a.shape
     _baseline_guard("baseline_layernorm_linear", a, g, beta, W_packed, N, FN_LAYOUT_LINEAR, x_ws, out, N)
     x = _ws(a, x_ws)
-    y = out if out is not None else torch.empty(M, N, dtype=a.dtype, device=a.device)
+    y = out if out is not None else _new_out(M, N, a)
     _check(_load().baseline_layernorm_linear(_ptr(a), M, K, _ld(a), _dt(a), _ptr(_vec(g, K, "g")),
                                              _ptr(_vec(beta, K, "beta")), _ptr(W_packed), N, eps, _ptr(x),
                                              _ptr(y), _ld(y), path, _stream(stream)),

@@ -365,3 +365,17 @@ def test_noalloc_baseline_validation(fnlib):
     assert f(M=-1) == -2
     assert f(dt=7) == -3
     assert f(M=0) == 0
+
+
+def test_binding_pads_the_outputs_it_allocates(fnlib):
+    # Outputs the caller does not pass are allocated with a 16-byte row pitch (the pitch the
+    # kernels' vector stores need), so any output width works; widths that are already a
+    # multiple of 16 bytes get a plain contiguous tensor.
+    import torch
+    for dtype, per in ((torch.bfloat16, 8), (torch.float32, 4)):
+        like = torch.zeros(1, dtype=dtype)
+        for n in (1, per - 1, per, 45, 333, 1024):
+            y = fnlib._new_out(3, n, like)
+            assert tuple(y.shape) == (3, n) and y.dtype == dtype and y.stride(1) == 1
+            assert y.stride(0) % per == 0 and y.stride(0) - n < per
+            assert y.is_contiguous() == (n % per == 0)

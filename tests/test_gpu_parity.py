@@ -217,6 +217,25 @@ def test_glu_ragged(fn, M, K, F, path):
     assert row_err(to_np(out), oracle.rmsnorm_swiglu(w.a, w.g, w.W, w.eps)) <= TOL[torch.bfloat16]
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_outputs_allocated_by_the_binding_take_any_width(fn, dtype):
+    # No `out`: the binding allocates the output with a 16-byte row pitch, so widths that
+    # are not a multiple of 16 bytes work (a caller-provided output must itself have such a
+    # pitch), on the tile, decode and fp32 kernels.
+    for M in (3, 300):
+        w = workloads.make("linear", M, 136, 333, dtype=dtype, eps=1e-5, seed=M + 1)
+        Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), ws_dtype=fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32)
+        y = fn.flashnorm_linear(w.a.to(DEV), Ws, 333, w.eps)
+        g = workloads.make("glu", M, 136, 45, dtype=dtype, eps=1e-5, seed=M + 2)
+        Wg, _, _ = fn.fold_weights(g.W.to(DEV), g.g.to(DEV), layout=fn.FN_LAYOUT_GLU,
+                                   ws_dtype=fn.FN_BF16 if dtype == torch.bfloat16 else fn.FN_F32)
+        o = fn.flashnorm_glu(g.a.to(DEV), Wg, 45, g.eps)
+        torch.cuda.synchronize()
+        assert tuple(y.shape) == (M, 333) and tuple(o.shape) == (M, 45)
+        assert row_err(to_np(y), oracle.rmsnorm_linear(w.a, w.g, w.W, w.eps)) <= TOL[dtype]
+        assert row_err(to_np(o), oracle.rmsnorm_swiglu(g.a, g.g, g.W, g.eps)) <= TOL[dtype]
+
+
 def test_glu_fp32(fn):
     w = workloads.make("glu", 40, 96, 36, dtype=torch.float32, eps=1e-6, seed=5)
     Ws, _, _ = fn.fold_weights(w.W.to(DEV), w.g.to(DEV), layout=fn.FN_LAYOUT_GLU)
