@@ -13,7 +13,8 @@ namespace fn {
 // high byte of the path argument for tuning).
 enum Tile : int {
   TILE_AUTO = 0,
-  TILE_256x256 = 1,       // 4 waves of 128 x 128, 4-stage ring, register prefetch
+  TILE_256x256 = 1,       // 4 waves of 128 x 128, 4-stage ring, register prefetch; hand-scheduled
+                          // k blocks (inline asm) when K is a multiple of 64
   TILE_128x128 = 2,       // 4 waves of 64 x 64, 4-stage ring, register prefetch
   TILE_256x256_W8 = 3,    // 8 waves of 128 x 64, 4-stage ring
   TILE_128x96_W8 = 4,     // 8 waves of 32 x 48, register prefetch (GLU: 128 x 128)

@@ -21,6 +21,7 @@
 #include "fn_epilogue.h"
 #include "fn_launch.h"
 #include "fn_tile.h"
+#include "prefill_w4_step.inc"
 
 namespace fn {
 
@@ -398,6 +399,73 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
   // GS needs block kb+2 landed (and scaled during block kb) before block kb+1
   // reads it; otherwise block kb+1 must have landed before step kb.
   constexpr int kAheadWait = GS ? (STAGES - 3) * LOADS : (STAGES - 2) * LOADS;
+  // The 4-wave 256 x 256 tile (one wave of 128 x 128 per SIMD) with K a multiple of 64:
+  // each k block is one hand-scheduled inline-asm sequence (prefill_w4_step.inc, written by
+  // gen_prefill_w4_step.py) that interleaves the block's 64 matrix-core ops (and the Gram
+  // ops of the RMS kinds) with the next block's LDS reads, a later block's transfers and
+  // their address arithmetic; the compiler allocates its operands, the accumulators in
+  // AGPRs.  Compiled from the loop above, one wave per SIMD ran ~12% behind the 8-wave
+  // tile; the sequence runs 1-2% ahead of it (Llama-7B QKV shape, MI355X).  The wave keeps
+  // its own copy of the ring slot offsets and transfer offsets, which the sequence advances.
+  constexpr bool kAsmW4 = BM == 256 && BN == 256 && WM == 2 && WN == 2 && PF && !GS && KD == 1 && STAGES == 4 &&
+                          !KCHK && (EPI == EPI_RMS || EPI == EPI_GLU || EPI == EPI_NONE);
+  static_assert(!kAsmW4 || (STAGE == 0x8000 && FMK == 8 && FNK == 8 && (!kGram || TW == 4) && LOADS == 8 &&
+                            A_FRAGS / NW == 4),
+                "the asm step's fixed geometry");
+  unsigned w4_sn = 0x8000, w4_sl = 0, w4_vo[8];  // read slot of block kb+1, transfer slot of block kb+4
+  const unsigned w4_aconst = lds_ring + (unsigned)(wm * FM * kFragBytes) + a_rd;
+  const unsigned w4_wconst = lds_ring + (unsigned)(A_BYTES + wn * FN * kFragBytes + lane * 16);
+  const unsigned w4_mbase = __builtin_amdgcn_readfirstlane(lds_ring + (unsigned)(wave * kFragBytes));
+  const unsigned w4_dw = __builtin_amdgcn_readfirstlane((unsigned)npb * kFragBytes);
+  auto w4_init = [&]() __attribute__((always_inline)) {
+    if constexpr (kAsmW4) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)  // the transfers of block STAGES (issued during block 0)
+        w4_vo[i] = i < A_FRAGS / NW ? off0[i] + (unsigned)(STAGES * (kKB * 2))
+                                    : off0[i] + (unsigned)(STAGES * npb) * kFragBytes;
+    }
+  };
+  // One k block: the asm sequence on the 4-wave tile, else the compiled schedule.
+  auto mstep = [&](auto wnc, int kb, bf16x8 (&afc)[FMK], bf16x8 (&wfc)[FNK], bf16x8 (&afn)[FMK],
+                   bf16x8 (&wfn)[FNK], bool more, bool scale = false) __attribute__((always_inline)) {
+    if constexpr (kAsmW4) {
+      constexpr int WNC = decltype(wnc)::value;
+      u32x4 ca[8], cw[8], na[8], nw[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        ca[r] = __builtin_bit_cast(u32x4, afc[r]);
+        cw[r] = __builtin_bit_cast(u32x4, wfc[r]);
+      }
+      f32x4 gnone[4];
+      f32x4 (&g4)[4] = *reinterpret_cast<f32x4(*)[4]>(kGram ? &gsq[0] : &gnone[0]);
+      if (more) {
+        if constexpr (kGram && WNC == 0)
+          w4_step_full_gram0(acc, g4, na, nw, ca, cw, w4_vo, w4_sn, w4_sl, w4_aconst, w4_wconst, w4_mbase, w4_dw, rs_a,
+                             rs_w);
+        else if constexpr (kGram)
+          w4_step_full_gram1(acc, g4, na, nw, ca, cw, w4_vo, w4_sn, w4_sl, w4_aconst, w4_wconst, w4_mbase, w4_dw, rs_a,
+                             rs_w);
+        else
+          w4_step_full_plain(acc, g4, na, nw, ca, cw, w4_vo, w4_sn, w4_sl, w4_aconst, w4_wconst, w4_mbase, w4_dw, rs_a,
+                             rs_w);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          afn[r] = __builtin_bit_cast(bf16x8, na[r]);
+          wfn[r] = __builtin_bit_cast(bf16x8, nw[r]);
+        }
+      } else {
+        if constexpr (kGram && WNC == 0) w4_step_last_gram0(acc, g4, ca, cw);
+        else if constexpr (kGram) w4_step_last_gram1(acc, g4, ca, cw);
+        else w4_step_last_plain(acc, g4, ca, cw);
+        // Wait states between the last matrix-core ops and the first reads of their results
+        // (the compiler does not see the asm's ops).
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+      }
+    } else {
+      multiply_interleaved(wnc, kb, afc, wfc, afn, wfn, more, scale);
+    }
+  };
+
   auto mainloop = [&](auto wnc) __attribute__((always_inline)) {
     constexpr int WNC = decltype(wnc)::value;
     if constexpr (PF) {
@@ -413,23 +481,24 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
       }
 #pragma unroll
       for (int r = 0; r < NRD; ++r) read_one(0, r, af0, wf0);
+      w4_init();
       for (int kb = 0; kb < nkb - 2; kb += 2) {
         wait_vmcnt<kAheadWait>();
         sync_block();
         scale_fetch(kb + 2);
-        multiply_interleaved(wnc, kb, af0, wf0, af1, wf1, true, true);
+        mstep(wnc, kb, af0, wf0, af1, wf1, true, true);
         wait_vmcnt<kAheadWait>();
         sync_block();
         scale_fetch(kb + 3);
-        multiply_interleaved(wnc, kb + 1, af1, wf1, af0, wf0, true, true);
+        mstep(wnc, kb + 1, af1, wf1, af0, wf0, true, true);
         if (((kb + 2) * KD) % 4 == 0) flush_ln();  // every fourth 32-deep block
       }
       auto tail_even = [&]() __attribute__((always_inline)) {
         wait_vmcnt<kAheadWait>();
         sync_block();
-        multiply_interleaved(wnc, nkb - 2, af0, wf0, af1, wf1, true);
+        mstep(wnc, nkb - 2, af0, wf0, af1, wf1, true);
         __builtin_amdgcn_s_waitcnt(0xc07f);
-        multiply_interleaved(wnc, nkb - 1, af1, wf1, af0, wf0, false);
+        mstep(wnc, nkb - 1, af1, wf1, af0, wf0, false);
       };
       if constexpr (KD == 1) {
         tail_even();  // nkb is even
@@ -439,7 +508,7 @@ __global__ __launch_bounds__(WM* WN * 64, 1) void prefill_bf16_kernel(
         // Odd step count: the loop (or, for one step, the prologue) has read the
         // last step into af0.
         __builtin_amdgcn_s_waitcnt(0xc07f);
-        multiply_interleaved(wnc, nkb - 1, af0, wf0, af1, wf1, false);
+        mstep(wnc, nkb - 1, af0, wf0, af1, wf1, false);
       }
       flush_ln();
     } else {
@@ -815,6 +884,11 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
   int tile = p.tile;
   if (tile == TILE_AUTO) {
     tile = auto_tile(p.M, p.NP, epi_is_glu(EPI));
+    // Large shapes of the core RMS kinds (and the unfused baseline's GEMM) with K a multiple
+    // of 64 take the 4-wave tile with the hand-scheduled k block.
+    if constexpr (EPI == EPI_RMS || EPI == EPI_GLU || EPI == EPI_NONE) {
+      if (!p.gs && tile == TILE_256x256_W8_PF_SP && p.K % kKPad == 0) tile = TILE_256x256;
+    }
     if constexpr (EPI == EPI_RMS || EPI == EPI_LN || EPI == EPI_NONE) {
       if (!p.gs && tile == TILE_128x96_W8 && p.K >= kK64MinK96) tile = TILE_128x96_W8_K64;
       if (!p.gs && tile == TILE_128x128_W8T && p.K >= kK64MinK128) tile = TILE_128x128_W8T_K64;
@@ -853,7 +927,7 @@ static hipError_t launch_prefill_epi(const PrefillArgs& p) {
     return hipErrorInvalidValue;
   } else {
   switch (tile) {
-    case TILE_256x256: return launch_prefill_cfg<256, 256, 2, 2, 4, true, EPI>(p);
+    case TILE_256x256: return launch_prefill_cfg<256, 256, 2, 2, 4, true, EPI, false, false, true>(p);  // asm steps when K % 64 == 0
     case TILE_128x128: return launch_prefill_cfg<128, 128, 2, 2, 4, true, EPI>(p);
     case TILE_256x256_W8: return launch_prefill_cfg<256, 256, 2, 4, 4, false, EPI>(p);
     case TILE_128x96_W8:

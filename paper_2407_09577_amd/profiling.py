@@ -40,11 +40,12 @@ def kernel_source(kernel: str) -> str:
 
 
 def kernel_sources_sha256(kernel: str) -> str:
-    """SHA-256 over the source file that defines ``kernel`` and every shared header, i.e.
-    everything its code is built from."""
+    """SHA-256 over the source file that defines ``kernel`` and every shared header and
+    generated include, i.e. everything its code is built from."""
     src = kernel_source(kernel)
     h = hashlib.sha256()
-    for path in [src] + sorted(glob.glob(os.path.join(HERE, "csrc", "*.h"))):
+    shared = sorted(glob.glob(os.path.join(HERE, "csrc", "*.h")) + glob.glob(os.path.join(HERE, "csrc", "*.inc")))
+    for path in [src] + shared:
         h.update(os.path.basename(path).encode())
         h.update(open(path, "rb").read())
     return h.hexdigest()
